@@ -1,0 +1,1007 @@
+/*
+ * grand_oracle.c -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously correct CPU implementation of the batched dynamic
+ * update of a fixed-degree proximity-graph ANN index described in
+ * "GrAND: GPU-based Dynamic Graph Indexes for ANN Search" (Vamana with
+ * GrANDRobustPrune, Alg. 4-6; CAGRA find-and-replace variant, Alg. 7-8;
+ * BeamSearch, Alg. 1).  It exists so that tests, the smoke check and the
+ * benchmark's CPU-baseline leg can check the GPU library against the paper.
+ * Nothing in the product path may link, load or call it, and it shares no
+ * code, header or constant with the GPU library.
+ *
+ * Conventions (each reading of the paper is restated where it is applied):
+ *   - Every batch step reads the state at the start of the batch (or of the
+ *     previous phase) and writes only state owned by the item it processes,
+ *     so the OpenMP loops below give the same result for any thread count.
+ *   - All orders are the total order on (distance, id).
+ *   - INVALID = 0xFFFFFFFF pads adjacency rows.
+ *
+ * Parity pins: see tests/test_oracle_*.py.  The whole-graph state after many
+ * batches is "parity unpinned" beyond the invariants and property checks
+ * those tests apply: the paper prints no worked example of it.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+#include <omp.h>
+
+#define O_INVALID 0xFFFFFFFFu
+
+enum { O_OK = 0, O_E_ARG = -1, O_E_ID = -2, O_E_CAPACITY = -3, O_E_OOM = -5 };
+enum { O_VAMANA = 0, O_CAGRA = 1 };
+enum { O_F32 = 0, O_U8 = 1 };
+enum { O_L2 = 0, O_IP = 1 };
+enum { O_ALPHA_ON_DIST = 0, O_ALPHA_ON_L2 = 1 };
+
+typedef struct {
+    int32_t algo, dtype, metric, prune_rule;
+    uint32_t dim, capacity, R, L_build, P, c, k_repair, max_iters;
+    float alpha;
+    int32_t threads;
+} ocfg;
+
+typedef struct {
+    uint64_t searches, hops, dist_evals, prunes, dirty, records, cap_dropped;
+} ostats;
+
+typedef struct {
+    ocfg cfg;
+    size_t esize;              /* bytes per element */
+    uint8_t *vecs;             /* capacity x dim */
+    uint32_t *adj;             /* capacity x R */
+    uint32_t *deg;             /* capacity */
+    uint8_t *active;           /* capacity */
+    uint32_t medoid;
+    uint64_t n_active;
+    ostats st;
+    char err[256];
+} oindex;
+
+typedef struct { float d; uint32_t id; } okey;
+
+static int key_less(okey a, okey b) { return a.d < b.d || (a.d == b.d && a.id < b.id); }
+
+static int key_cmp(const void *pa, const void *pb) {
+    okey a = *(const okey *)pa, b = *(const okey *)pb;
+    if (key_less(a, b)) return -1;
+    if (key_less(b, a)) return 1;
+    return 0;
+}
+
+static int nthreads(const oindex *h) { return h->cfg.threads > 0 ? h->cfg.threads : omp_get_max_threads(); }
+
+static const void *vec_of(const oindex *h, uint32_t id) {
+    return h->vecs + (size_t)id * h->cfg.dim * h->esize;
+}
+
+/* ------------------------------------------------------------------------
+ * Dist (Alg. 1 takes a distance function; Section 5.1 uses Euclidean and
+ * inner-product datasets).  Reading: one function Dist everywhere,
+ *   L2: squared Euclidean distance, IP: negated inner product,
+ * accumulated exactly for uint8 (integers) and in fp64 for fp32, one fused
+ * multiply-add per dimension in dimension order, rounded once to fp32.
+ * A zero result is returned as +0.
+ * ---------------------------------------------------------------------- */
+static float dist_raw(const oindex *h, const void *a, const void *b) {
+    uint32_t d = h->cfg.dim;
+    float r;
+    if (h->cfg.dtype == O_U8) {
+        const uint8_t *x = a, *y = b;
+        int64_t s = 0;
+        if (h->cfg.metric == O_L2) {
+            for (uint32_t j = 0; j < d; j++) { int64_t t = (int64_t)x[j] - (int64_t)y[j]; s += t * t; }
+            r = (float)s;
+        } else {
+            for (uint32_t j = 0; j < d; j++) s += (int64_t)x[j] * (int64_t)y[j];
+            r = (float)(-s);
+        }
+    } else {
+        const float *x = a, *y = b;
+        double s = 0.0;
+        if (h->cfg.metric == O_L2) {
+            for (uint32_t j = 0; j < d; j++) { double t = (double)x[j] - (double)y[j]; s = fma(t, t, s); }
+            r = (float)s;
+        } else {
+            for (uint32_t j = 0; j < d; j++) s = fma((double)x[j], (double)y[j], s);
+            r = (float)(-s);
+        }
+    }
+    if (r == 0.0f) r = 0.0f;
+    return r;
+}
+
+static float dist_ids(const oindex *h, uint32_t a, uint32_t b) {
+    return dist_raw(h, vec_of(h, a), vec_of(h, b));
+}
+
+/* ------------------------------------------------------------------------
+ * BeamSearch (Alg. 1).  C starts as {s}; V is empty.  While some element of
+ * C is not in V (and |V| < max_iters, a cap added so the visited list has a
+ * bound): expand u, the (Dist, id)-smallest element of C \ V, add it to V,
+ * add every out-neighbour of u not already in C, and keep the l smallest.
+ * Dedupe is against C only: an id evicted from C can never re-enter, since
+ * the l-th smallest key never increases once C is full.
+ * Returns C (sorted, |C| <= l) and V in expansion order, with distances.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    okey *C; uint8_t *vis; uint32_t nC;
+    okey *V; uint32_t nV;
+    uint64_t evals;
+} osearch;
+
+static void beam_search(const oindex *h, const void *q, uint32_t s, uint32_t ell,
+                        uint32_t max_iters, osearch *out) {
+    const uint32_t R = h->cfg.R;
+    okey *C = out->C;
+    uint8_t *vis = out->vis;
+    uint32_t nC = 0, nV = 0;
+    uint64_t evals = 0;
+    C[0].d = dist_raw(h, q, vec_of(h, s));
+    C[0].id = s;
+    vis[0] = 0;
+    nC = 1;
+    evals++;
+    while (nV < max_iters) {
+        uint32_t i;
+        for (i = 0; i < nC; i++) if (!vis[i]) break;      /* argmin of C \ V */
+        if (i == nC) break;
+        vis[i] = 1;
+        out->V[nV++] = C[i];
+        uint32_t u = C[i].id;
+        for (uint32_t t = 0; t < R; t++) {
+            uint32_t v = h->adj[(size_t)u * R + t];
+            if (v == O_INVALID) continue;
+            int present = 0;
+            for (uint32_t j = 0; j < nC; j++) if (C[j].id == v) { present = 1; break; }
+            if (present) continue;
+            okey k = { dist_raw(h, q, vec_of(h, v)), v };
+            evals++;
+            /* sorted insert; C holds at most ell + R entries before the cut */
+            uint32_t pos = nC;
+            while (pos > 0 && key_less(k, C[pos - 1])) { C[pos] = C[pos - 1]; vis[pos] = vis[pos - 1]; pos--; }
+            C[pos] = k;
+            vis[pos] = 0;
+            nC++;
+        }
+        if (nC > ell) nC = ell;                             /* keep the l closest */
+    }
+    out->nC = nC;
+    out->nV = nV;
+    out->evals = evals;
+}
+
+static int search_alloc(osearch *s, uint32_t ell, uint32_t R, uint32_t max_iters) {
+    s->C = malloc(sizeof(okey) * (ell + R + 1));
+    s->vis = malloc(ell + R + 1);
+    s->V = malloc(sizeof(okey) * (max_iters + 1));
+    return s->C && s->vis && s->V;
+}
+
+static void search_free(osearch *s) { free(s->C); free(s->vis); free(s->V); }
+
+/* ------------------------------------------------------------------------
+ * GrANDRobustPrune (Alg. 4).  Candidates come with cached distances D_p
+ * (Section 3.1: distances from the search are reused, never recomputed).
+ * Candidates equal to p, INVALID or repeated are dropped; the rest are
+ * taken in (D_p, id) order.  The first valid candidate p* is selected; if R
+ * are selected the loop ends; otherwise every later valid p' with
+ * alpha * Dist(p*, p') <= D_p[p'] is invalidated.  Reading of the alpha
+ * test: alpha multiplies the same Dist used everywhere (squared L2), in
+ * fp64; the variant ALPHA_ON_L2 applies alpha to the Euclidean distance,
+ * i.e. alpha^2 * Dist <= D.  Output in selection order; returns |L|.
+ * ---------------------------------------------------------------------- */
+static uint32_t robust_prune(const oindex *h, uint32_t p, const okey *cand_in, uint32_t n,
+                             uint32_t *L, uint64_t *evals) {
+    const uint32_t R = h->cfg.R;
+    okey *cand = malloc(sizeof(okey) * (n + 1));
+    uint8_t *valid = malloc(n + 1);
+    uint32_t m = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        if (cand_in[i].id == p || cand_in[i].id == O_INVALID) continue;
+        cand[m++] = cand_in[i];
+    }
+    qsort(cand, m, sizeof(okey), key_cmp);
+    uint32_t w = 0;                     /* drop repeated ids (adjacent after the sort
+                                           only if their D agree; check all) */
+    for (uint32_t i = 0; i < m; i++) {
+        int dup = 0;
+        for (uint32_t j = 0; j < w; j++) if (cand[j].id == cand[i].id) { dup = 1; break; }
+        if (!dup) cand[w++] = cand[i];
+    }
+    m = w;
+    for (uint32_t i = 0; i < m; i++) valid[i] = 1;
+    double a = (double)h->cfg.alpha;
+    double coef = h->cfg.prune_rule == O_ALPHA_ON_L2 ? a * a : a;
+    uint32_t nl = 0;
+    for (uint32_t i = 0; i < m; i++) {
+        if (!valid[i]) continue;
+        L[nl++] = cand[i].id;             /* p* = argmin over valid candidates */
+        valid[i] = 0;
+        if (nl == R) break;
+        for (uint32_t j = i + 1; j < m; j++) {
+            if (!valid[j]) continue;
+            float dij = dist_ids(h, cand[i].id, cand[j].id);
+            (*evals)++;
+            if (coef * (double)dij <= (double)cand[j].d) valid[j] = 0;
+        }
+    }
+    free(cand);
+    free(valid);
+    return nl;
+}
+
+/* ------------------------------------------------------------------------
+ * Medoid (Alg. 5 starts from a pre-computed medoid; Section 6.2 notes a new
+ * medoid is installed when the medoid is deleted).  Reading: the active id
+ * minimising (fp64 squared distance to the centroid, id).  The centroid sums
+ * each dimension exactly for uint8, and for fp32 in a fixed order: blocks of
+ * 1024 consecutive ids summed in ascending id order, block sums added in
+ * block order; it is then divided by the active count.  The distance to the
+ * centroid is a fused multiply-add chain in dimension order.
+ * ---------------------------------------------------------------------- */
+#define O_CENTROID_BLOCK 1024u
+
+static uint32_t compute_medoid(const oindex *h) {
+    const uint32_t d = h->cfg.dim, cap = h->cfg.capacity;
+    uint64_t n = 0;
+    for (uint32_t i = 0; i < cap; i++) n += h->active[i] ? 1 : 0;
+    if (n == 0) return O_INVALID;
+    double *c = calloc(d, sizeof(double));
+    for (uint32_t j = 0; j < d; j++) {
+        if (h->cfg.dtype == O_U8) {
+            uint64_t s = 0;
+            for (uint32_t i = 0; i < cap; i++)
+                if (h->active[i]) s += ((const uint8_t *)vec_of(h, i))[j];
+            c[j] = (double)s / (double)n;
+        } else {
+            double t = 0.0;
+            for (uint32_t b0 = 0; b0 < cap; b0 += O_CENTROID_BLOCK) {
+                double sb = 0.0;
+                for (uint32_t i = b0; i < cap && i < b0 + O_CENTROID_BLOCK; i++)
+                    if (h->active[i]) sb = sb + (double)((const float *)vec_of(h, i))[j];
+                t = t + sb;
+            }
+            c[j] = t / (double)n;
+        }
+    }
+    double best = INFINITY;
+    uint32_t arg = O_INVALID;
+    for (uint32_t i = 0; i < cap; i++) {
+        if (!h->active[i]) continue;
+        double s = 0.0;
+        for (uint32_t j = 0; j < d; j++) {
+            double x = h->cfg.dtype == O_U8 ? (double)((const uint8_t *)vec_of(h, i))[j]
+                                            : (double)((const float *)vec_of(h, i))[j];
+            double t = x - c[j];
+            s = fma(t, t, s);
+        }
+        if (s < best) { best = s; arg = i; }   /* ascending ids: ties keep the smaller id */
+    }
+    free(c);
+    return arg;
+}
+
+/* ------------------------------------------------------------------------
+ * Reverse graph in CSR (Alg. 8, first two loops; Section 4.2): the exact
+ * transpose of all out-lists of active nodes.  Filling sources in ascending
+ * id order makes every row ascending by source id.
+ * ---------------------------------------------------------------------- */
+static uint64_t reverse_csr(const uint32_t *adj, const uint8_t *active, uint32_t cap, uint32_t R,
+                            uint32_t *offsets, uint32_t *srcs) {
+    uint32_t *cnt = calloc((size_t)cap + 1, sizeof(uint32_t));
+    for (uint32_t u = 0; u < cap; u++) {
+        if (!active[u]) continue;
+        for (uint32_t t = 0; t < R; t++) {
+            uint32_t v = adj[(size_t)u * R + t];
+            if (v != O_INVALID) cnt[v]++;
+        }
+    }
+    uint64_t acc = 0;
+    for (uint32_t v = 0; v < cap; v++) { offsets[v] = (uint32_t)acc; acc += cnt[v]; }
+    offsets[cap] = (uint32_t)acc;
+    if (srcs) {
+        for (uint32_t v = 0; v < cap; v++) cnt[v] = offsets[v];
+        for (uint32_t u = 0; u < cap; u++) {
+            if (!active[u]) continue;
+            for (uint32_t t = 0; t < R; t++) {
+                uint32_t v = adj[(size_t)u * R + t];
+                if (v != O_INVALID) srcs[cnt[v]++] = u;
+            }
+        }
+    }
+    free(cnt);
+    return acc;
+}
+
+/* ------------------------------------------------------------------------
+ * Reverse-edge records and their grouping (Alg. 5 and Alg. 6 scratch
+ * buffers).  A record (target, src, dist) asks to add src to target's list.
+ * Reading of the scratch capacity P: per target, records are taken as a
+ * set of sources (repeated (target, src) pairs count once) ordered by
+ * (dist, src), and the first P are kept; the race-dependent "first come"
+ * of the paper is replaced by this order.  Every target is dirty, also when
+ * its records were dropped by the cap.  A record with src == INVALID only
+ * marks its target dirty.
+ * ---------------------------------------------------------------------- */
+typedef struct { uint32_t t, s; float d; } orec;
+
+static int rec_cmp(const void *pa, const void *pb) {
+    const orec *a = pa, *b = pb;
+    if (a->t != b->t) return a->t < b->t ? -1 : 1;
+    int ai = a->s == O_INVALID, bi = b->s == O_INVALID;     /* markers last */
+    if (ai != bi) return ai ? 1 : -1;
+    if (a->d != b->d) return a->d < b->d ? -1 : 1;
+    if (a->s != b->s) return a->s < b->s ? -1 : 1;
+    return 0;
+}
+
+typedef struct {
+    uint32_t n_dirty;
+    uint32_t *dirty;     /* ascending */
+    uint32_t *gofs;      /* n_dirty + 1 offsets into gsrc */
+    uint32_t *gsrc;      /* kept sources per dirty node, in (dist, src) order */
+    uint64_t cap_dropped;
+} ogroups;
+
+static void group_records(const oindex *h, orec *rec, uint64_t n, ogroups *g) {
+    qsort(rec, n, sizeof(orec), rec_cmp);
+    g->dirty = malloc(sizeof(uint32_t) * (n + 1));
+    g->gofs = malloc(sizeof(uint32_t) * (n + 2));
+    g->gsrc = malloc(sizeof(uint32_t) * (n + 1));
+    g->n_dirty = 0;
+    g->cap_dropped = 0;
+    uint64_t ns = 0;
+    uint64_t i = 0;
+    while (i < n) {
+        uint64_t j = i;
+        while (j < n && rec[j].t == rec[i].t) j++;
+        g->dirty[g->n_dirty] = rec[i].t;
+        g->gofs[g->n_dirty] = (uint32_t)ns;
+        uint32_t kept = 0;
+        for (uint64_t k = i; k < j; k++) {
+            if (rec[k].s == O_INVALID) continue;
+            int dup = 0;
+            for (uint64_t q = g->gofs[g->n_dirty]; q < ns; q++) if (g->gsrc[q] == rec[k].s) { dup = 1; break; }
+            if (dup) continue;
+            if (kept < h->cfg.P) { g->gsrc[ns++] = rec[k].s; kept++; }
+            else g->cap_dropped++;
+        }
+        g->n_dirty++;
+        i = j;
+    }
+    g->gofs[g->n_dirty] = (uint32_t)ns;
+}
+
+static void groups_free(ogroups *g) { free(g->dirty); free(g->gofs); free(g->gsrc); }
+
+/* ------------------------------------------------------------------------
+ * Dirty rebuild (Alg. 5 final loop; Alg. 6 "Rebuild neighbourhood"):
+ * C = (N_out(u) U scratch_u) minus u and minus the delete batch; if |C| <= R
+ * it is installed as is (existing entries first, then new sources in group
+ * order), otherwise D_u is computed and GrANDRobustPrune(u, C, D_u) is
+ * installed.  Each dirty node owns its row, so the loop is race-free.
+ * ---------------------------------------------------------------------- */
+static void rebuild_dirty(oindex *h, const ogroups *g, const uint8_t *in_batch) {
+    const uint32_t R = h->cfg.R;
+    uint64_t prunes = 0, evals = 0;
+    #pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads(h)) reduction(+:prunes, evals)
+    for (uint32_t k = 0; k < g->n_dirty; k++) {
+        uint32_t u = g->dirty[k];
+        uint32_t ng = g->gofs[k + 1] - g->gofs[k];
+        uint32_t *C = malloc(sizeof(uint32_t) * (R + ng + 1));
+        uint32_t m = 0;
+        for (uint32_t pass = 0; pass < 2; pass++) {
+            uint32_t cnt = pass == 0 ? R : ng;
+            for (uint32_t t = 0; t < cnt; t++) {
+                uint32_t v = pass == 0 ? h->adj[(size_t)u * R + t] : g->gsrc[g->gofs[k] + t];
+                if (v == O_INVALID || v == u) continue;
+                if (in_batch && in_batch[v]) continue;
+                int dup = 0;
+                for (uint32_t q = 0; q < m; q++) if (C[q] == v) { dup = 1; break; }
+                if (!dup) C[m++] = v;
+            }
+        }
+        uint32_t *row = h->adj + (size_t)u * R;
+        if (m <= R) {
+            for (uint32_t t = 0; t < R; t++) row[t] = t < m ? C[t] : O_INVALID;
+            h->deg[u] = m;
+        } else {
+            okey *cand = malloc(sizeof(okey) * m);
+            for (uint32_t q = 0; q < m; q++) { cand[q].id = C[q]; cand[q].d = dist_ids(h, u, C[q]); }
+            evals += m;
+            uint32_t *L = malloc(sizeof(uint32_t) * R);
+            uint32_t nl = robust_prune(h, u, cand, m, L, &evals);
+            for (uint32_t t = 0; t < R; t++) row[t] = t < nl ? L[t] : O_INVALID;
+            h->deg[u] = nl;
+            prunes++;
+            free(L);
+            free(cand);
+        }
+        free(C);
+    }
+    h->st.prunes += prunes;
+    h->st.dist_evals += evals;
+    h->st.dirty += g->n_dirty;
+}
+
+/* ------------------------------------------------------------------------
+ * Validation (done before any state changes; a failing batch leaves the
+ * index untouched).
+ * ---------------------------------------------------------------------- */
+static int validate_ids(oindex *h, const uint32_t *ids, uint32_t n, int want_active) {
+    uint8_t *seen = calloc(h->cfg.capacity, 1);
+    int rc = O_OK;
+    for (uint32_t i = 0; i < n && rc == O_OK; i++) {
+        uint32_t id = ids[i];
+        if (id >= h->cfg.capacity) { snprintf(h->err, sizeof h->err, "id %u out of range", id); rc = O_E_ID; }
+        else if (seen[id]) { snprintf(h->err, sizeof h->err, "id %u repeated in batch", id); rc = O_E_ID; }
+        else if ((h->active[id] != 0) != (want_active != 0)) {
+            snprintf(h->err, sizeof h->err, "id %u is %s", id, want_active ? "not active" : "already active");
+            rc = O_E_ID;
+        }
+        else seen[id] = 1;
+    }
+    free(seen);
+    return rc;
+}
+
+static int validate_vectors(oindex *h, const void *vecs, uint32_t n) {
+    if (h->cfg.dtype != O_F32) return O_OK;
+    const float *x = vecs;
+    for (uint64_t i = 0; i < (uint64_t)n * h->cfg.dim; i++)
+        if (!isfinite(x[i])) { snprintf(h->err, sizeof h->err, "non-finite vector element"); return O_E_ARG; }
+    return O_OK;
+}
+
+/* ========================================================================
+ * Public entry points (ctypes).
+ * ====================================================================== */
+void *oracle_create(const ocfg *cfg) {
+    if (!cfg || cfg->dim == 0 || cfg->capacity == 0 || cfg->R == 0 || cfg->R > 4096 ||
+        cfg->L_build == 0) return NULL;
+    oindex *h = calloc(1, sizeof(oindex));
+    h->cfg = *cfg;
+    if (h->cfg.max_iters == 0) h->cfg.max_iters = 2 * h->cfg.L_build;
+    h->esize = cfg->dtype == O_U8 ? 1 : 4;
+    size_t cap = cfg->capacity;
+    h->vecs = calloc(cap * cfg->dim, h->esize);
+    h->adj = malloc(cap * cfg->R * sizeof(uint32_t));
+    h->deg = calloc(cap, sizeof(uint32_t));
+    h->active = calloc(cap, 1);
+    if (!h->vecs || !h->adj || !h->deg || !h->active) return NULL;
+    memset(h->adj, 0xFF, cap * cfg->R * sizeof(uint32_t));
+    h->medoid = O_INVALID;
+    return h;
+}
+
+void oracle_destroy(void *hv) {
+    oindex *h = hv;
+    if (!h) return;
+    free(h->vecs); free(h->adj); free(h->deg); free(h->active); free(h);
+}
+
+const char *oracle_last_error(void *hv) { return ((oindex *)hv)->err; }
+void oracle_set_threads(void *hv, int32_t t) { ((oindex *)hv)->cfg.threads = t; }
+void oracle_get_stats(void *hv, ostats *out) { *out = ((oindex *)hv)->st; }
+
+/* Stage (Alg. 5 first loop / Alg. 7 first loop): write the vector into its
+ * slot, empty its list, mark it active. */
+static void stage(oindex *h, const void *vecs, const uint32_t *ids, uint32_t n) {
+    size_t row = (size_t)h->cfg.dim * h->esize;
+    for (uint32_t i = 0; i < n; i++) {
+        memcpy(h->vecs + (size_t)ids[i] * row, (const uint8_t *)vecs + (size_t)i * row, row);
+        for (uint32_t t = 0; t < h->cfg.R; t++) h->adj[(size_t)ids[i] * h->cfg.R + t] = O_INVALID;
+        h->deg[ids[i]] = 0;
+        h->active[ids[i]] = 1;
+    }
+    h->n_active += n;
+}
+
+/* Bootstrap for an index that is empty at the start of the batch (the
+ * paper starts from seed graphs; reading: the candidates of each new point
+ * are its `want` nearest other points of the batch, found by brute force). */
+static void bootstrap_candidates(const oindex *h, const uint32_t *ids, uint32_t n, uint32_t want,
+                                 okey *out /* n x want */, uint32_t *nout) {
+    #pragma omp parallel for schedule(dynamic, 16) num_threads(nthreads(h))
+    for (uint32_t i = 0; i < n; i++) {
+        okey *all = malloc(sizeof(okey) * (n + 1));
+        uint32_t m = 0;
+        for (uint32_t j = 0; j < n; j++) {
+            if (j == i) continue;
+            all[m].id = ids[j];
+            all[m].d = dist_ids(h, ids[i], ids[j]);
+            m++;
+        }
+        qsort(all, m, sizeof(okey), key_cmp);
+        uint32_t k = m < want ? m : want;
+        memcpy(out + (size_t)i * want, all, sizeof(okey) * k);
+        nout[i] = k;
+        free(all);
+    }
+}
+
+/* GrAND-Vamana BatchInsert (Alg. 5). */
+static int vamana_insert(oindex *h, const void *vecs, const uint32_t *ids, uint32_t n) {
+    const uint32_t R = h->cfg.R, ell = h->cfg.L_build, mi = h->cfg.max_iters;
+    uint64_t n_active0 = h->n_active;
+    uint32_t m0 = h->medoid;
+    stage(h, vecs, ids, n);
+    uint32_t cmax = n_active0 == 0 ? ell : mi;
+    okey *cand = malloc(sizeof(okey) * (size_t)n * cmax);
+    uint32_t *ncand = malloc(sizeof(uint32_t) * n);
+    if (n_active0 == 0) {
+        bootstrap_candidates(h, ids, n, ell, cand, ncand);
+    } else {
+        uint64_t hops = 0, evals = 0;
+        /* forward search on the batch-start snapshot: new nodes have empty
+           lists and no in-edges, so they are unreachable from the medoid */
+        #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:hops, evals)
+        for (uint32_t i = 0; i < n; i++) {
+            osearch s;
+            search_alloc(&s, ell, R, mi);
+            beam_search(h, vec_of(h, ids[i]), m0, ell, mi, &s);
+            memcpy(cand + (size_t)i * cmax, s.V, sizeof(okey) * s.nV);   /* V_i with D_{p_i} */
+            ncand[i] = s.nV;
+            hops += s.nV; evals += s.evals;
+            search_free(&s);
+        }
+        h->st.searches += n; h->st.hops += hops; h->st.dist_evals += evals;
+    }
+    /* forward GrANDRobustPrune of V_i \ {p_i}; each item owns row p_i */
+    uint32_t *L = malloc(sizeof(uint32_t) * (size_t)n * R);
+    uint32_t *nL = malloc(sizeof(uint32_t) * n);
+    uint64_t evals = 0;
+    #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:evals)
+    for (uint32_t i = 0; i < n; i++)
+        nL[i] = robust_prune(h, ids[i], cand + (size_t)i * cmax, ncand[i], L + (size_t)i * R, &evals);
+    h->st.dist_evals += evals;
+    h->st.prunes += n;
+    uint64_t nrec = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        uint32_t *row = h->adj + (size_t)ids[i] * R;
+        for (uint32_t t = 0; t < R; t++) row[t] = t < nL[i] ? L[(size_t)i * R + t] : O_INVALID;
+        h->deg[ids[i]] = nL[i];
+        nrec += nL[i];
+    }
+    /* reverse edges (u, p_i, D_{p_i}[u]) into per-target scratch */
+    orec *rec = malloc(sizeof(orec) * (nrec + 1));
+    uint64_t r = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        const okey *ci = cand + (size_t)i * cmax;
+        for (uint32_t t = 0; t < nL[i]; t++) {
+            uint32_t u = L[(size_t)i * R + t];
+            float du = NAN;
+            for (uint32_t q = 0; q < ncand[i]; q++) if (ci[q].id == u) { du = ci[q].d; break; }
+            rec[r].t = u; rec[r].s = ids[i]; rec[r].d = du; r++;
+        }
+    }
+    ogroups g;
+    group_records(h, rec, nrec, &g);
+    h->st.records += nrec;
+    h->st.cap_dropped += g.cap_dropped;
+    rebuild_dirty(h, &g, NULL);
+    groups_free(&g);
+    free(rec); free(L); free(nL); free(cand); free(ncand);
+    if (n_active0 == 0) h->medoid = compute_medoid(h);
+    return O_OK;
+}
+
+/* GrAND-CAGRA BatchInsert (Alg. 7). */
+static int cagra_insert(oindex *h, const void *vecs, const uint32_t *ids, uint32_t n) {
+    const uint32_t R = h->cfg.R, ell = h->cfg.L_build, mi = h->cfg.max_iters;
+    uint64_t n_active0 = h->n_active;
+    uint32_t m0 = h->medoid;
+    stage(h, vecs, ids, n);
+    okey *fwd = malloc(sizeof(okey) * (size_t)n * R);   /* N_out(p_i) with distances */
+    uint32_t *nf = malloc(sizeof(uint32_t) * n);
+    if (n_active0 == 0) {
+        bootstrap_candidates(h, ids, n, R, fwd, nf);
+    } else {
+        uint64_t hops = 0, evals = 0;
+        #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:hops, evals)
+        for (uint32_t i = 0; i < n; i++) {
+            osearch s;
+            search_alloc(&s, ell, R, mi);
+            beam_search(h, vec_of(h, ids[i]), m0, ell, mi, &s);
+            uint32_t k = s.nC < R ? s.nC : R;               /* the R closest (k = R) */
+            memcpy(fwd + (size_t)i * R, s.C, sizeof(okey) * k);
+            nf[i] = k;
+            hops += s.nV; evals += s.evals;
+            search_free(&s);
+        }
+        h->st.searches += n; h->st.hops += hops; h->st.dist_evals += evals;
+    }
+    uint64_t nrec = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        uint32_t *row = h->adj + (size_t)ids[i] * R;
+        for (uint32_t t = 0; t < R; t++) row[t] = t < nf[i] ? fwd[(size_t)i * R + t].id : O_INVALID;
+        h->deg[ids[i]] = nf[i];
+        nrec += nf[i];
+    }
+    /* backward edges: records (q, p_i) grouped by q, taken in (dist, p_i) order */
+    orec *rec = malloc(sizeof(orec) * (nrec + 1));
+    uint32_t *owner = malloc(sizeof(uint32_t) * (nrec + 1));  /* batch index of src */
+    uint64_t r = 0;
+    for (uint32_t i = 0; i < n; i++)
+        for (uint32_t t = 0; t < nf[i]; t++) {
+            rec[r].t = fwd[(size_t)i * R + t].id; rec[r].s = ids[i]; rec[r].d = fwd[(size_t)i * R + t].d; r++;
+        }
+    qsort(rec, nrec, sizeof(orec), rec_cmp);
+    /* map src id -> batch index (ids are unique within the batch) */
+    uint32_t *bidx = malloc(sizeof(uint32_t) * h->cfg.capacity);
+    for (uint32_t i = 0; i < n; i++) bidx[ids[i]] = i;
+    for (uint64_t k = 0; k < nrec; k++) owner[k] = bidx[rec[k].s];
+    /* group starts */
+    uint64_t *gstart = malloc(sizeof(uint64_t) * (nrec + 1));
+    uint64_t ng = 0;
+    for (uint64_t k = 0; k < nrec; k++) if (k == 0 || rec[k].t != rec[k - 1].t) gstart[ng++] = k;
+    gstart[ng] = nrec;
+    /* one owner per target q: for each record, if q's list has a free slot
+       the new node fills the first one; otherwise pick the element of
+       N_out(q) n N_out(p_i) at the highest slot of q's list and replace it by
+       p_i (detour find-and-replace).  N_out(p_i) is read from the forward
+       lists as written above (a snapshot), never from a list being edited. */
+    #pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads(h))
+    for (uint64_t gi = 0; gi < ng; gi++) {
+        uint32_t q = rec[gstart[gi]].t;
+        uint32_t *row = h->adj + (size_t)q * R;
+        for (uint64_t k = gstart[gi]; k < gstart[gi + 1]; k++) {
+            uint32_t p = rec[k].s;
+            int has = 0, free_slot = -1;
+            for (uint32_t t = 0; t < R; t++) {
+                if (row[t] == p) has = 1;
+                if (row[t] == O_INVALID && free_slot < 0) free_slot = (int)t;
+            }
+            if (has) continue;
+            if (free_slot >= 0) { row[free_slot] = p; continue; }
+            const okey *fp = fwd + (size_t)owner[k] * R;
+            uint32_t nfp = nf[owner[k]];
+            for (int t = (int)R - 1; t >= 0; t--) {
+                int in = 0;
+                for (uint32_t j = 0; j < nfp; j++) if (fp[j].id == row[t]) { in = 1; break; }
+                if (in) { row[t] = p; break; }
+            }
+        }
+        uint32_t dg = 0;
+        for (uint32_t t = 0; t < R; t++) dg += row[t] != O_INVALID;
+        h->deg[q] = dg;
+    }
+    h->st.records += nrec;
+    h->st.dirty += ng;
+    free(gstart); free(bidx); free(owner); free(rec); free(fwd); free(nf);
+    if (n_active0 == 0) h->medoid = compute_medoid(h);
+    return O_OK;
+}
+
+int32_t oracle_insert_batch(void *hv, const void *vecs, const uint32_t *ids, uint32_t n) {
+    oindex *h = hv;
+    h->err[0] = 0;
+    if (n == 0) return O_OK;
+    if (!vecs || !ids) { snprintf(h->err, sizeof h->err, "null argument"); return O_E_ARG; }
+    int rc = validate_ids(h, ids, n, 0);
+    if (rc) return rc;
+    rc = validate_vectors(h, vecs, n);
+    if (rc) return rc;
+    return h->cfg.algo == O_CAGRA ? cagra_insert(h, vecs, ids, n) : vamana_insert(h, vecs, ids, n);
+}
+
+/* Clear the deleted rows and re-install the medoid if it was deleted
+ * (Alg. 6 last loop; Alg. 8 last loop; Section 6.2). */
+static void clear_batch(oindex *h, const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t m0) {
+    for (uint32_t i = 0; i < n; i++) {
+        for (uint32_t t = 0; t < h->cfg.R; t++) h->adj[(size_t)ids[i] * h->cfg.R + t] = O_INVALID;
+        h->deg[ids[i]] = 0;
+        h->active[ids[i]] = 0;
+    }
+    h->n_active -= n;
+    if (m0 != O_INVALID && in_batch[m0]) h->medoid = compute_medoid(h);
+}
+
+/* GrAND-Vamana BatchDelete (Alg. 6) with in-neighbours taken exactly from
+ * the on-demand reverse graph (Section 1 contribution (iii), Alg. 3). */
+static int vamana_delete(oindex *h, const uint32_t *ids, uint32_t n) {
+    const uint32_t R = h->cfg.R, ell = h->cfg.L_build, mi = h->cfg.max_iters;
+    const uint32_t cap = h->cfg.capacity, kr = h->cfg.k_repair, cc = h->cfg.c;
+    uint32_t m0 = h->medoid;
+    uint8_t *in_batch = calloc(cap, 1);
+    for (uint32_t i = 0; i < n; i++) in_batch[ids[i]] = 1;
+    /* C_i: the first k_repair of BeamSearch(x_{p_i}).C outside the batch */
+    uint32_t *Ci = malloc(sizeof(uint32_t) * (size_t)n * (kr + 1));
+    uint32_t *nCi = calloc(n, sizeof(uint32_t));
+    uint64_t hops = 0, evals = 0;
+    #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:hops, evals)
+    for (uint32_t i = 0; i < n; i++) {
+        osearch s;
+        search_alloc(&s, ell, R, mi);
+        beam_search(h, vec_of(h, ids[i]), m0, ell, mi, &s);
+        uint32_t k = 0;
+        for (uint32_t j = 0; j < s.nC && k < kr; j++)
+            if (!in_batch[s.C[j].id]) Ci[(size_t)i * (kr + 1) + k++] = s.C[j].id;
+        nCi[i] = k;
+        hops += s.nV; evals += s.evals;
+        search_free(&s);
+    }
+    h->st.searches += n; h->st.hops += hops; h->st.dist_evals += evals;
+    /* reverse graph of the batch-start graph */
+    uint32_t *offs = malloc(sizeof(uint32_t) * ((size_t)cap + 1));
+    uint64_t nnz = reverse_csr(h->adj, h->active, cap, R, offs, NULL);
+    uint32_t *srcs = malloc(sizeof(uint32_t) * (nnz + 1));
+    reverse_csr(h->adj, h->active, cap, R, offs, srcs);
+    /* record counts per deleted node: c per surviving in- and out-neighbour
+       plus one dirty marker per surviving in-neighbour */
+    uint64_t *rofs = malloc(sizeof(uint64_t) * (n + 1));
+    rofs[0] = 0;
+    for (uint32_t i = 0; i < n; i++) {
+        uint32_t p = ids[i], nin = 0, nout = 0;
+        for (uint32_t q = offs[p]; q < offs[p + 1]; q++) nin += !in_batch[srcs[q]];
+        for (uint32_t t = 0; t < R; t++) {
+            uint32_t w = h->adj[(size_t)p * R + t];
+            nout += w != O_INVALID && !in_batch[w];
+        }
+        rofs[i + 1] = rofs[i] + (uint64_t)nin * (cc + 1) + (uint64_t)nout * cc;
+    }
+    uint64_t nrec = rofs[n];
+    orec *rec = malloc(sizeof(orec) * (nrec + 1));
+    uint64_t used_total = 0;
+    evals = 0;
+    #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:evals, used_total)
+    for (uint32_t i = 0; i < n; i++) {
+        uint32_t p = ids[i];
+        const uint32_t *ci = Ci + (size_t)i * (kr + 1);
+        okey *tmp = malloc(sizeof(okey) * (nCi[i] + 1));
+        uint64_t r = rofs[i];
+        /* in-neighbour repair: z gets the c points of C_i closest to z */
+        for (uint32_t q = offs[p]; q < offs[p + 1]; q++) {
+            uint32_t z = srcs[q];
+            if (in_batch[z]) continue;
+            uint32_t m = 0;
+            for (uint32_t j = 0; j < nCi[i]; j++) {
+                if (ci[j] == z) continue;
+                tmp[m].id = ci[j]; tmp[m].d = dist_ids(h, z, ci[j]); m++;
+            }
+            evals += m;
+            qsort(tmp, m, sizeof(okey), key_cmp);
+            for (uint32_t j = 0; j < cc; j++) {
+                rec[r].t = z;
+                rec[r].s = j < m ? tmp[j].id : O_INVALID;
+                rec[r].d = j < m ? tmp[j].d : 0.0f;
+                r++;
+            }
+            rec[r].t = z; rec[r].s = O_INVALID; rec[r].d = 0.0f; r++;     /* z is dirty */
+        }
+        /* out-neighbour repair: w is added to the lists of the c points of
+           C_i closest to w */
+        for (uint32_t t = 0; t < R; t++) {
+            uint32_t w = h->adj[(size_t)p * R + t];
+            if (w == O_INVALID || in_batch[w]) continue;
+            uint32_t m = 0;
+            for (uint32_t j = 0; j < nCi[i]; j++) {
+                if (ci[j] == w) continue;
+                tmp[m].id = ci[j]; tmp[m].d = dist_ids(h, w, ci[j]); m++;
+            }
+            evals += m;
+            qsort(tmp, m, sizeof(okey), key_cmp);
+            for (uint32_t j = 0; j < cc; j++) {
+                if (j < m) { rec[r].t = tmp[j].id; rec[r].s = w; rec[r].d = tmp[j].d; }
+                else { rec[r].t = O_INVALID; rec[r].s = O_INVALID; rec[r].d = 0.0f; }
+                r++;
+            }
+        }
+        used_total += r - rofs[i];
+        free(tmp);
+    }
+    h->st.dist_evals += evals;
+    /* drop empty records (target INVALID) before grouping */
+    uint64_t w = 0;
+    for (uint64_t k = 0; k < nrec; k++) if (rec[k].t != O_INVALID) rec[w++] = rec[k];
+    ogroups g;
+    group_records(h, rec, w, &g);
+    h->st.records += w;
+    h->st.cap_dropped += g.cap_dropped;
+    rebuild_dirty(h, &g, in_batch);
+    groups_free(&g);
+    clear_batch(h, ids, n, in_batch, m0);
+    free(rec); free(rofs); free(srcs); free(offs); free(Ci); free(nCi); free(in_batch);
+    return O_OK;
+}
+
+/* GrAND-CAGRA BatchDelete (Alg. 8).  Reading of PickOne's round-robin: the
+ * in-neighbour u of a deleted p starts its cyclic scan of N_out(p) (valid
+ * entries in slot order) at (rank of u in N_in(p)) mod |N_out(p)| and takes
+ * the first r outside the batch, different from u and not already in
+ * N_out(u); with no such r the slot becomes INVALID.  Each affected u owns
+ * its list and handles its deleted out-neighbours in slot order. */
+static int cagra_delete(oindex *h, const uint32_t *ids, uint32_t n) {
+    const uint32_t R = h->cfg.R, cap = h->cfg.capacity;
+    uint32_t m0 = h->medoid;
+    uint8_t *in_batch = calloc(cap, 1);
+    for (uint32_t i = 0; i < n; i++) in_batch[ids[i]] = 1;
+    uint32_t *offs = malloc(sizeof(uint32_t) * ((size_t)cap + 1));
+    uint64_t nnz = reverse_csr(h->adj, h->active, cap, R, offs, NULL);
+    uint32_t *srcs = malloc(sizeof(uint32_t) * (nnz + 1));
+    reverse_csr(h->adj, h->active, cap, R, offs, srcs);
+    uint8_t *affected = calloc(cap, 1);
+    for (uint32_t i = 0; i < n; i++)
+        for (uint32_t q = offs[ids[i]]; q < offs[ids[i] + 1]; q++)
+            if (!in_batch[srcs[q]]) affected[srcs[q]] = 1;
+    uint64_t n_aff = 0;
+    #pragma omp parallel for schedule(dynamic, 256) num_threads(nthreads(h)) reduction(+:n_aff)
+    for (uint32_t u = 0; u < cap; u++) {
+        if (!affected[u]) continue;
+        n_aff++;
+        uint32_t *row = h->adj + (size_t)u * R;
+        for (uint32_t s = 0; s < R; s++) {
+            uint32_t p = row[s];
+            if (p == O_INVALID || !in_batch[p]) continue;
+            uint32_t L[4096];
+            uint32_t nl = 0;
+            for (uint32_t t = 0; t < R; t++) {
+                uint32_t v = h->adj[(size_t)p * R + t];   /* p's list is never edited here */
+                if (v != O_INVALID) L[nl++] = v;
+            }
+            uint32_t rank = 0;
+            for (uint32_t q = offs[p]; q < offs[p + 1]; q++) if (srcs[q] == u) { rank = q - offs[p]; break; }
+            uint32_t chosen = O_INVALID;
+            for (uint32_t j = 0; j < nl; j++) {
+                uint32_t r = L[(rank + j) % nl];
+                if (in_batch[r] || r == u) continue;
+                int in = 0;
+                for (uint32_t t = 0; t < R; t++) if (row[t] == r) { in = 1; break; }
+                if (in) continue;
+                chosen = r;
+                break;
+            }
+            row[s] = chosen;
+        }
+        uint32_t dg = 0;
+        for (uint32_t t = 0; t < R; t++) dg += row[t] != O_INVALID;
+        h->deg[u] = dg;
+    }
+    h->st.dirty += n_aff;
+    clear_batch(h, ids, n, in_batch, m0);
+    free(affected); free(srcs); free(offs); free(in_batch);
+    return O_OK;
+}
+
+int32_t oracle_delete_batch(void *hv, const uint32_t *ids, uint32_t n) {
+    oindex *h = hv;
+    h->err[0] = 0;
+    if (n == 0) return O_OK;
+    if (!ids) { snprintf(h->err, sizeof h->err, "null argument"); return O_E_ARG; }
+    int rc = validate_ids(h, ids, n, 1);
+    if (rc) return rc;
+    return h->cfg.algo == O_CAGRA ? cagra_delete(h, ids, n) : vamana_delete(h, ids, n);
+}
+
+/* Search: BeamSearch from the medoid with l = beam and a cap of 2 * beam
+ * expansions; the first k of C, padded with INVALID / +inf. */
+int32_t oracle_search(void *hv, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                      uint32_t *out_ids, float *out_d) {
+    oindex *h = hv;
+    h->err[0] = 0;
+    if (k == 0 || beam == 0 || k > beam) { snprintf(h->err, sizeof h->err, "need 1 <= k <= beam"); return O_E_ARG; }
+    if (nq == 0) return O_OK;
+    if (validate_vectors(h, queries, nq)) return O_E_ARG;
+    size_t row = (size_t)h->cfg.dim * h->esize;
+    uint64_t hops = 0, evals = 0;
+    #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:hops, evals)
+    for (uint32_t i = 0; i < nq; i++) {
+        uint32_t got = 0;
+        if (h->n_active > 0) {
+            osearch s;
+            search_alloc(&s, beam, h->cfg.R, 2 * beam);
+            beam_search(h, (const uint8_t *)queries + (size_t)i * row, h->medoid, beam, 2 * beam, &s);
+            for (; got < k && got < s.nC; got++) {
+                out_ids[(size_t)i * k + got] = s.C[got].id;
+                out_d[(size_t)i * k + got] = s.C[got].d;
+            }
+            hops += s.nV; evals += s.evals;
+            search_free(&s);
+        }
+        for (; got < k; got++) { out_ids[(size_t)i * k + got] = O_INVALID; out_d[(size_t)i * k + got] = INFINITY; }
+    }
+    h->st.searches += nq; h->st.hops += hops; h->st.dist_evals += evals;
+    return O_OK;
+}
+
+/* Export: lists as stored (slot order), degrees, active map, medoid, and
+ * optionally the reverse CSR (offsets: capacity + 1 entries). */
+int32_t oracle_export_graph(void *hv, uint32_t *adj, uint32_t *deg, uint8_t *active, uint32_t *medoid,
+                            uint32_t *rev_offsets, uint32_t *rev_srcs, uint64_t *nnz) {
+    oindex *h = hv;
+    size_t cap = h->cfg.capacity;
+    if (adj) memcpy(adj, h->adj, cap * h->cfg.R * sizeof(uint32_t));
+    if (deg) memcpy(deg, h->deg, cap * sizeof(uint32_t));
+    if (active) memcpy(active, h->active, cap);
+    if (medoid) *medoid = h->medoid;
+    if (rev_offsets) {
+        uint64_t z = reverse_csr(h->adj, h->active, h->cfg.capacity, h->cfg.R, rev_offsets, rev_srcs);
+        if (nnz) *nnz = z;
+    }
+    return O_OK;
+}
+
+/* Import a full state (vectors for every slot, lists, degrees, active map,
+ * medoid).  Used by tests to set up hand-made graphs. */
+int32_t oracle_import_graph(void *hv, const void *vecs, const uint32_t *adj, const uint32_t *deg,
+                            const uint8_t *active, uint32_t medoid) {
+    oindex *h = hv;
+    size_t cap = h->cfg.capacity;
+    memcpy(h->vecs, vecs, cap * h->cfg.dim * h->esize);
+    memcpy(h->adj, adj, cap * h->cfg.R * sizeof(uint32_t));
+    memcpy(h->deg, deg, cap * sizeof(uint32_t));
+    memcpy(h->active, active, cap);
+    h->medoid = medoid;
+    h->n_active = 0;
+    for (size_t i = 0; i < cap; i++) h->n_active += active[i] ? 1 : 0;
+    return O_OK;
+}
+
+/* ---- pieces exposed for the pin tests ---------------------------------- */
+float oracle_dist(void *hv, const void *a, const void *b) { return dist_raw(hv, a, b); }
+
+/* BeamSearch on the current state from start s; writes C (ids, dists) and V
+ * (ids, dists); returns |C| and stores |V| in *nV. */
+uint32_t oracle_beam_search(void *hv, const void *q, uint32_t s, uint32_t ell, uint32_t max_iters,
+                            uint32_t *C_ids, float *C_d, uint32_t *V_ids, float *V_d, uint32_t *nV) {
+    oindex *h = hv;
+    osearch st;
+    search_alloc(&st, ell, h->cfg.R, max_iters);
+    beam_search(h, q, s, ell, max_iters, &st);
+    for (uint32_t i = 0; i < st.nC; i++) { C_ids[i] = st.C[i].id; C_d[i] = st.C[i].d; }
+    for (uint32_t i = 0; i < st.nV; i++) { V_ids[i] = st.V[i].id; V_d[i] = st.V[i].d; }
+    *nV = st.nV;
+    uint32_t nc = st.nC;
+    search_free(&st);
+    return nc;
+}
+
+/* GrANDRobustPrune of node p over explicit candidates with their D_p. */
+uint32_t oracle_robust_prune(void *hv, uint32_t p, const uint32_t *ids, const float *D, uint32_t n,
+                             uint32_t *L) {
+    okey *cand = malloc(sizeof(okey) * (n + 1));
+    for (uint32_t i = 0; i < n; i++) { cand[i].id = ids[i]; cand[i].d = D[i]; }
+    uint64_t ev = 0;
+    uint32_t nl = robust_prune(hv, p, cand, n, L, &ev);
+    free(cand);
+    return nl;
+}
+
+uint32_t oracle_medoid(void *hv) { return compute_medoid(hv); }
+
+uint64_t oracle_reverse_csr(const uint32_t *adj, const uint8_t *active, uint32_t cap, uint32_t R,
+                            uint32_t *offsets, uint32_t *srcs) {
+    return reverse_csr(adj, active, cap, R, offsets, srcs);
+}
+
+/* Exact k nearest active neighbours by brute force (ground truth, the
+ * recall@k definition of Section 5.5). */
+int32_t oracle_bruteforce_knn(void *hv, const void *queries, uint32_t nq, uint32_t k,
+                              uint32_t *out_ids, float *out_d) {
+    oindex *h = hv;
+    size_t row = (size_t)h->cfg.dim * h->esize;
+    const uint32_t cap = h->cfg.capacity;
+    #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads(h))
+    for (uint32_t i = 0; i < nq; i++) {
+        const void *q = (const uint8_t *)queries + (size_t)i * row;
+        okey *best = malloc(sizeof(okey) * (k + 1));
+        uint32_t nb = 0;
+        for (uint32_t v = 0; v < cap; v++) {
+            if (!h->active[v]) continue;
+            okey key = { dist_raw(h, q, vec_of(h, v)), v };
+            if (nb == k && !key_less(key, best[k - 1])) continue;
+            uint32_t pos = nb < k ? nb++ : k - 1;
+            while (pos > 0 && key_less(key, best[pos - 1])) { best[pos] = best[pos - 1]; pos--; }
+            best[pos] = key;
+        }
+        for (uint32_t j = 0; j < k; j++) {
+            out_ids[(size_t)i * k + j] = j < nb ? best[j].id : O_INVALID;
+            out_d[(size_t)i * k + j] = j < nb ? best[j].d : INFINITY;
+        }
+        free(best);
+    }
+    return O_OK;
+}

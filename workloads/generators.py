@@ -1,0 +1,303 @@
+"""Seeded synthetic workloads shaped like the paper's streaming experiments.
+
+The paper evaluates on real datasets (Section 5.1, Table 2) under streaming
+patterns (Section 5.2).  None of those datasets is available here, so every
+workload below is synthetic: a seeded Gaussian (or Student-t) mixture with
+the dimensionality, element type and metric of the dataset it stands in for,
+driven through an operation stream of uniform single-type batches as in
+Section 5.2.
+
+Everything is drawn from ``numpy.random.Generator(PCG64)`` seeded by
+``SeedSequence([seed, purpose, index])`` so that every batch can be
+regenerated independently of the others.  Id bookkeeping (which ids are
+active, which are free) follows only the operation stream: fresh ids are the
+smallest free ids in ascending order, and deleted ids become free again
+(the pool of Section 4 reuses deleted ids).
+
+This module contains no distance computation, search or pruning.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+from typing import Iterator, List, Optional, Tuple
+
+import numpy as np
+
+INVALID = 0xFFFFFFFF
+
+# purpose codes for SeedSequence entropy
+_P_MODEL, _P_BASE, _P_INS, _P_DEL, _P_QRY = 1, 2, 3, 4, 5
+
+
+def _rng(seed: int, purpose: int, index: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, purpose, index])))
+
+
+@dataclass(frozen=True)
+class IndexConfig:
+    """Index parameters (Section 5.4 names l, alpha, P, k, c; R per workload)."""
+    algo: str            # "vamana" | "cagra"
+    dtype: str           # "f32" | "u8"
+    metric: str          # "l2" | "ip"
+    dim: int
+    capacity: int
+    R: int
+    L_build: int         # beam width of insert/delete searches (CAGRA: internal top-k)
+    alpha: float = 1.2
+    P: int = 64          # scratch capacity per node
+    c: int = 2           # replacement edges per repaired neighbour
+    k_repair: int = 50   # top-k of the delete search used for repair
+    max_iters: int = 0   # expansion cap of build searches; 0 means 2 * L_build
+    prune_rule: str = "alpha_on_sq"   # or "alpha_on_l2"
+    cas_mode: str = "grouped"         # or "racing" (CAGRA insert only)
+
+    @property
+    def iters(self) -> int:
+        return self.max_iters if self.max_iters > 0 else 2 * self.L_build
+
+    def replace(self, **kw) -> "IndexConfig":
+        return dataclasses.replace(self, **kw)
+
+
+@dataclass(frozen=True)
+class StreamSpec:
+    base_n: int
+    build_batch: int
+    n_rounds: int
+    n_insert: int
+    n_delete: int
+    n_query: int
+    k: int
+    beam: int
+    order: Tuple[str, ...] = ("insert", "delete", "search")
+    delete_policy: str = "uniform"    # "uniform" | "oldest"
+
+
+@dataclass(frozen=True)
+class WorkloadDef:
+    name: str
+    description: str
+    index: IndexConfig
+    stream: StreamSpec
+    sampler: str
+    sampler_args: Tuple = ()
+
+
+CONFIGS = {
+    # 10,000 x 32 fp32 N(0,1), built by 10 batches of 1,000, then one round of
+    # +1,000 inserts, -500 uniform deletes, 100 queries (k=10, beam 64).
+    "tiny": WorkloadDef(
+        "tiny", "10K x 32 fp32 N(0,1), Vamana R=32 L=64",
+        IndexConfig("vamana", "f32", "l2", 32, 11_000, 32, 64, max_iters=128),
+        StreamSpec(10_000, 1_000, 1, 1_000, 500, 100, 10, 64),
+        "gauss"),
+    # 1M x 128 uint8 from a 256-component Gaussian mixture, centres U[0,255],
+    # sigma 20, rounded and clipped; 20 rounds of +10K / -10K / 10K queries.
+    "sift1m_u8": WorkloadDef(
+        "sift1m_u8", "1M x 128 uint8 256-component mixture, Vamana R=64 L=128",
+        IndexConfig("vamana", "u8", "l2", 128, 1_010_000, 64, 128),
+        StreamSpec(1_000_000, 10_000, 20, 10_000, 10_000, 10_000, 10, 64),
+        "mix_u8", (256, 20.0)),
+    # 1M x 96 fp32 sliding window, 512-component mixture, L2-normalised,
+    # drifting mixture weights; 50 steps of +10K / -10K oldest / 10K queries.
+    "deep1m_window": WorkloadDef(
+        "deep1m_window", "1M x 96 fp32 sliding window, Vamana R=64 L=128",
+        IndexConfig("vamana", "f32", "l2", 96, 1_010_000, 64, 128),
+        StreamSpec(1_000_000, 10_000, 50, 10_000, 10_000, 10_000, 10, 64,
+                   delete_policy="oldest"),
+        "mix_norm_drift", (512, 0.5, 50)),
+    # 1M x 100 fp32 unit vectors, inner product, Student-t(3) mixture of 1,000
+    # components; CAGRA fixed degree 64; 10 batches of -30K / +10K.
+    "glove1m_cagra": WorkloadDef(
+        "glove1m_cagra", "1M x 100 fp32 IP, CAGRA fixed degree 64",
+        IndexConfig("cagra", "f32", "ip", 100, 1_000_000, 64, 64),
+        StreamSpec(1_000_000, 10_000, 10, 10_000, 30_000, 10_000, 10, 64,
+                   order=("delete", "insert", "search")),
+        "mix_t_norm", (1000, 0.3, 3.0)),
+    # 500K x 960 fp32, 128-component mixture, per-dimension scale U[0.1,1],
+    # clipped at zero; 10 rounds of +5K / -5K / 5K queries (beam 128).
+    "gist500k": WorkloadDef(
+        "gist500k", "500K x 960 fp32 scaled clipped mixture, Vamana R=64 L=128",
+        IndexConfig("vamana", "f32", "l2", 960, 505_000, 64, 128),
+        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128),
+        "mix_relu_scaled", (128, 0.5)),
+}
+
+
+class _Sampler:
+    """Draws vectors; also returns the mixture component of each vector."""
+
+    def __init__(self, kind: str, args: Tuple, dim: int, seed: int):
+        self.kind, self.args, self.dim = kind, args, dim
+        g = _rng(seed, _P_MODEL)
+        d = dim
+        if kind == "gauss":
+            self.n_comp = 1
+        elif kind == "mix_u8":
+            self.n_comp, self.sigma = args
+            self.centres = g.uniform(0.0, 255.0, size=(self.n_comp, d))
+        elif kind == "mix_norm_drift":
+            self.n_comp, self.sigma, self.horizon = args
+            self.centres = g.standard_normal((self.n_comp, d))
+            self.w0 = g.dirichlet(np.ones(self.n_comp))
+            self.w1 = g.dirichlet(np.ones(self.n_comp))
+        elif kind == "mix_t_norm":
+            self.n_comp, self.scale, self.nu = args
+            self.centres = g.standard_normal((self.n_comp, d))
+        elif kind == "mix_relu_scaled":
+            self.n_comp, self.sigma = args
+            self.dim_scale = g.uniform(0.1, 1.0, size=d)
+            self.centres = g.standard_normal((self.n_comp, d))
+        else:
+            raise ValueError(kind)
+
+    def weights(self, t: float) -> np.ndarray:
+        if self.kind == "mix_norm_drift":
+            a = min(max(t / float(self.horizon), 0.0), 1.0)
+            w = (1.0 - a) * self.w0 + a * self.w1
+            return w / w.sum()
+        return np.full(self.n_comp, 1.0 / self.n_comp)
+
+    def draw(self, g: np.random.Generator, n: int, t: float = 0.0,
+             comps: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+        d = self.dim
+        if self.kind == "gauss":
+            return g.standard_normal((n, d)).astype(np.float32), np.zeros(n, np.int32)
+        if comps is None:
+            comps = g.choice(self.n_comp, size=n, p=self.weights(t)).astype(np.int32)
+        mu = self.centres[comps]
+        if self.kind == "mix_u8":
+            x = np.rint(mu + self.sigma * g.standard_normal((n, d)))
+            return np.clip(x, 0, 255).astype(np.uint8), comps
+        if self.kind == "mix_norm_drift":
+            x = mu + self.sigma * g.standard_normal((n, d))
+        elif self.kind == "mix_t_norm":
+            x = mu + self.scale * g.standard_t(self.nu, size=(n, d))
+        else:  # mix_relu_scaled
+            x = np.maximum(0.0, self.dim_scale * (mu + self.sigma * g.standard_normal((n, d))))
+            return x.astype(np.float32), comps
+        nrm = np.linalg.norm(x, axis=1, keepdims=True)
+        nrm[nrm == 0] = 1.0
+        return (x / nrm).astype(np.float32), comps
+
+
+@dataclass
+class Op:
+    kind: str                        # "insert" | "delete" | "search"
+    ids: Optional[np.ndarray] = None  # uint32
+    vecs: Optional[np.ndarray] = None  # n x dim (insert vectors or queries)
+
+
+class Workload:
+    """Operation stream: base build batches, then rounds of single-type batches.
+
+    Fresh ids are the smallest free ids (ascending); deletes are uniform
+    without replacement over the currently active ids, or the oldest ids for
+    the sliding window.  The stream depends only on the seed, never on the
+    index state.
+    """
+
+    def __init__(self, wdef: WorkloadDef, seed: int = 0):
+        self.wdef = wdef
+        self.cfg = wdef.index
+        self.spec = wdef.stream
+        self.seed = seed
+        self.sampler = _Sampler(wdef.sampler, wdef.sampler_args, self.cfg.dim, seed)
+        cap = self.cfg.capacity
+        self.active = np.zeros(cap, dtype=bool)
+        self.birth = np.full(cap, -1, dtype=np.int64)    # insertion counter
+        self.comp = np.full(cap, -1, dtype=np.int32)
+        self._clock = 0
+        self.vectors = None  # optional host copy of every inserted vector
+        self._np_dtype = np.uint8 if self.cfg.dtype == "u8" else np.float32
+
+    # -- bookkeeping -------------------------------------------------------
+    def keep_vectors(self) -> "Workload":
+        """Keep a host copy of the vector pool (for ground truth)."""
+        self.vectors = np.zeros((self.cfg.capacity, self.cfg.dim), self._np_dtype)
+        return self
+
+    def active_ids(self) -> np.ndarray:
+        return np.flatnonzero(self.active).astype(np.uint32)
+
+    def _alloc(self, n: int) -> np.ndarray:
+        free = np.flatnonzero(~self.active)
+        if free.size < n:
+            raise RuntimeError("workload exceeds index capacity")
+        return free[:n].astype(np.uint32)
+
+    def _apply_insert(self, ids, vecs, comps):
+        self.active[ids] = True
+        self.birth[ids] = self._clock + np.arange(ids.size)
+        self._clock += ids.size
+        self.comp[ids] = comps
+        if self.vectors is not None:
+            self.vectors[ids] = vecs
+
+    def _apply_delete(self, ids):
+        self.active[ids] = False
+        self.birth[ids] = -1
+        self.comp[ids] = -1
+
+    # -- stream ------------------------------------------------------------
+    def base_batches(self) -> Iterator[Op]:
+        s = self.spec
+        n_b = (s.base_n + s.build_batch - 1) // s.build_batch
+        for b in range(n_b):
+            n = min(s.build_batch, s.base_n - b * s.build_batch)
+            g = _rng(self.seed, _P_BASE, b)
+            vecs, comps = self.sampler.draw(g, n, t=0.0)
+            ids = self._alloc(n)
+            self._apply_insert(ids, vecs, comps)
+            yield Op("insert", ids, vecs)
+
+    def _queries(self, r: int, t: float) -> np.ndarray:
+        s = self.spec
+        g = _rng(self.seed, _P_QRY, r)
+        if self.sampler.kind == "mix_norm_drift":
+            act = np.flatnonzero(self.active)
+            comps = self.comp[act[g.integers(0, act.size, size=s.n_query)]]
+            return self.sampler.draw(g, s.n_query, t, comps=comps)[0]
+        return self.sampler.draw(g, s.n_query, t)[0]
+
+    def round_ops(self, r: int) -> Iterator[Op]:
+        """Operations of round r (0-based), in the stream's order."""
+        s = self.spec
+        t = float(r + 1)
+        for kind in s.order:
+            if kind == "insert" and s.n_insert > 0:
+                g = _rng(self.seed, _P_INS, r)
+                vecs, comps = self.sampler.draw(g, s.n_insert, t)
+                ids = self._alloc(s.n_insert)
+                self._apply_insert(ids, vecs, comps)
+                yield Op("insert", ids, vecs)
+            elif kind == "delete" and s.n_delete > 0:
+                act = np.flatnonzero(self.active)
+                n = min(s.n_delete, act.size)
+                if s.delete_policy == "oldest":
+                    order = np.argsort(self.birth[act], kind="stable")
+                    ids = np.sort(act[order[:n]]).astype(np.uint32)
+                else:
+                    g = _rng(self.seed, _P_DEL, r)
+                    ids = np.sort(g.choice(act, size=n, replace=False)).astype(np.uint32)
+                    ids = g.permutation(ids).astype(np.uint32)
+                self._apply_delete(ids)
+                yield Op("delete", ids)
+            elif kind == "search" and s.n_query > 0:
+                yield Op("search", None, self._queries(r, t))
+
+    def rounds(self, n_rounds: Optional[int] = None) -> Iterator[Tuple[int, List[Op]]]:
+        n = self.spec.n_rounds if n_rounds is None else n_rounds
+        for r in range(n):
+            yield r, list(self.round_ops(r))
+
+
+def make_workload(name: str, seed: int = 0, index: Optional[dict] = None,
+                  stream: Optional[dict] = None) -> Workload:
+    """Build a workload by name, optionally overriding index or stream fields
+    (used to make small variants of the large workloads for tests)."""
+    w = CONFIGS[name]
+    idx = dataclasses.replace(w.index, **(index or {}))
+    st = dataclasses.replace(w.stream, **(stream or {}))
+    return Workload(WorkloadDef(w.name, w.description, idx, st, w.sampler, w.sampler_args), seed)
