@@ -1,0 +1,184 @@
+/*
+ * grand.h -- C ABI of the MI355X (gfx950) library for batched dynamic
+ * updates of fixed-degree proximity-graph ANN indexes, following
+ * "GrAND: GPU-based Dynamic Graph Indexes for Approximate Nearest Neighbour
+ * Search": Vamana with GrANDRobustPrune (Alg. 4-6) and a CAGRA-style fixed
+ * out-degree variant with lock-free find-and-replace (Alg. 7-8), both
+ * searched by BeamSearch (Alg. 1).
+ *
+ * Conventions for every entry point
+ *  - Status codes are returned; nothing is thrown across the ABI.
+ *  - Pointer arguments may point to host memory or to device memory of the
+ *    index's GPU; the library detects which.  The caller owns every buffer
+ *    it passes; the library copies what it needs and keeps no pointer after
+ *    the call returns.
+ *  - All work is ordered on the index's HIP stream and every call returns
+ *    after its work has completed (one host synchronisation per call).
+ *  - Arguments are validated before any state changes: a call that fails
+ *    validation leaves the index exactly as it was, and grand_last_error()
+ *    describes the problem.  A HIP failure during a call returns
+ *    GRAND_E_DEVICE and poisons the handle; every later call on it returns
+ *    GRAND_E_STATE.
+ *  - One index must not be used by two host threads at the same time.
+ *  - Ids are the slots of the resource pool (Section 4: a pool of a fixed
+ *    peak size N, ids in [0, N-1], deleted ids reusable).
+ */
+#ifndef GRAND_H
+#define GRAND_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GRAND_INVALID 0xFFFFFFFFu
+
+typedef struct grand_index grand_index;
+
+typedef enum {
+  GRAND_OK = 0,
+  GRAND_E_ARG = -1,       /* malformed argument (sizes, k > beam, NaN/inf vector element, ...) */
+  GRAND_E_ID = -2,        /* id out of range, repeated in a batch, or in the wrong active state */
+  GRAND_E_CAPACITY = -3,  /* a size limit of the library would be exceeded */
+  GRAND_E_DEVICE = -4,    /* a HIP call failed; the handle is poisoned */
+  GRAND_E_OOM = -5,       /* device allocation failed (state unchanged) */
+  GRAND_E_STATE = -6      /* the handle was poisoned by an earlier device failure */
+} grand_status;
+
+enum { GRAND_VAMANA = 0, GRAND_CAGRA = 1 };
+enum { GRAND_F32 = 0, GRAND_U8 = 1 };
+enum { GRAND_L2 = 0, GRAND_IP = 1 };
+/* alpha test of GrANDRobustPrune (Alg. 4): alpha * Dist(p*, p') <= D_p[p']
+ * on the squared distance (default), or on the Euclidean distance. */
+enum { GRAND_ALPHA_ON_DIST = 0, GRAND_ALPHA_ON_L2 = 1 };
+/* CAGRA reverse edges (Alg. 7): grouped per target and applied in
+ * (distance, id) order by one owner (deterministic, default), or applied by
+ * independent racing compare-and-swap updates as in the paper's lock-free
+ * last-writer-wins form. */
+enum { GRAND_CAS_GROUPED = 0, GRAND_CAS_RACING = 1 };
+/* In-neighbour discovery for deletes (Alg. 8): the full reverse graph of
+ * every node in CSR form (default), or the reverse lists of the deleted
+ * nodes only, built by the same histogram / prefix-scan / scatter pass. */
+enum { GRAND_REV_FULL = 0, GRAND_REV_BATCH = 1 };
+
+typedef struct {
+  uint32_t struct_size;  /* sizeof(grand_params) */
+  int32_t algo;          /* GRAND_VAMANA | GRAND_CAGRA */
+  int32_t dtype;         /* GRAND_F32 | GRAND_U8 (U8 requires L2) */
+  int32_t metric;        /* GRAND_L2 | GRAND_IP (IP requires CAGRA and F32) */
+  uint32_t dim;          /* vector length; f32 <= 1024, u8 <= 4096 */
+  uint32_t capacity;     /* pool size N (ids in [0, N)), < 2^31 */
+  uint32_t R;            /* degree bound (Vamana) / fixed degree (CAGRA), 1..64 */
+  uint32_t L_build;      /* beam width of insert/delete searches (CAGRA: internal top-k), <= 256 */
+  uint32_t P;            /* scratch capacity per node (Alg. 5 and 6), 1..128 */
+  uint32_t c;            /* replacement edges per repaired neighbour (Alg. 6), <= 64 */
+  uint32_t k_repair;     /* top-k of the delete search used for repair (Alg. 6), <= 64 */
+  uint32_t max_iters;    /* expansion cap of insert/delete searches; 0 = 2 * L_build; <= 256 */
+  float alpha;           /* pruning factor of GrANDRobustPrune */
+  int32_t prune_rule;    /* GRAND_ALPHA_ON_DIST | GRAND_ALPHA_ON_L2 */
+  int32_t cas_mode;      /* GRAND_CAS_GROUPED | GRAND_CAS_RACING */
+  int32_t rev_mode;      /* GRAND_REV_FULL | GRAND_REV_BATCH */
+  uint32_t max_batch;    /* batch size the per-batch buffers are first sized for (grown on demand) */
+  int32_t device;        /* HIP device ordinal */
+  void *stream;          /* hipStream_t for all work; NULL = the null stream */
+} grand_params;
+
+/* Fills p with the defaults (Vamana, f32, L2, R 64, L_build 128, P 64,
+ * c 2, k_repair 50, alpha 1.2 -- the parameters of Section 5.4). */
+void grand_default_params(grand_params *p);
+
+/* Creates an index and allocates its whole resource pool on the device
+ * (Section 3.1, resource-pool reuse; Section 4, peak size N).  *out
+ * receives the handle.  Errors: GRAND_E_ARG for unsupported parameters,
+ * GRAND_E_OOM, GRAND_E_DEVICE. */
+grand_status grand_create(const grand_params *p, grand_index **out);
+
+/* Frees the index and all its device memory.  NULL is accepted. */
+grand_status grand_destroy(grand_index *h);
+
+/* Sets the HIP stream used by later calls (e.g. torch's current stream). */
+grand_status grand_set_stream(grand_index *h, void *stream);
+
+/* BatchInsert (Alg. 3; Vamana Alg. 5; CAGRA Alg. 7).
+ * vecs: n rows of dim elements of the index dtype, row-major, packed.
+ * ids:  n distinct ids in [0, capacity) that are not active.
+ * Every point is searched for on the graph as it was at the start of the
+ * batch; forward lists are pruned per point; reverse edges are grouped per
+ * target and applied once per target.  An index empty at the start of the
+ * batch is bootstrapped from the batch itself (each point's candidates are
+ * its nearest other batch points) and its medoid computed.
+ * n == 0 is a no-op.  Errors: GRAND_E_ID, GRAND_E_ARG (non-finite element). */
+grand_status grand_insert_batch(grand_index *h, const void *vecs, const uint32_t *ids, uint32_t n);
+
+/* BatchDelete (Alg. 3; Vamana Alg. 6; CAGRA Alg. 8), in place.
+ * ids: n distinct active ids.  In-neighbours of the deleted nodes are found
+ * exactly from a reverse graph built on the GPU for this batch; their lists
+ * and those of the repair targets are rebuilt so that no edge points to a
+ * deleted id; the deleted rows are cleared and their ids become free.  If
+ * the medoid is deleted a new one is installed.
+ * n == 0 is a no-op.  Errors: GRAND_E_ID. */
+grand_status grand_delete_batch(grand_index *h, const uint32_t *ids, uint32_t n);
+
+/* BeamSearch (Alg. 1) from the medoid with l = beam and at most 2*beam
+ * expansions, for nq queries (nq rows of dim elements, packed).
+ * out_ids / out_dists: nq x k, the k closest (distance, id) found, padded
+ * with GRAND_INVALID / +inf (an empty index returns only padding).
+ * Requires 1 <= k <= beam <= 256.  Errors: GRAND_E_ARG. */
+grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                          uint32_t *out_ids, float *out_dists);
+
+/* Copies the index state out.  Any output pointer may be NULL.
+ *   adj: capacity x R lists as stored (Vamana lists are sets; CAGRA slot
+ *        order is meaningful), GRAND_INVALID padding;  deg: capacity;
+ *   active: capacity bytes (0/1);  medoid: 1 id (GRAND_INVALID if empty).
+ *   rev_offsets (capacity + 1) / rev_srcs: the reverse graph of the current
+ *        graph in CSR form, rows ascending by source id (Alg. 8).  With
+ *        rev_srcs NULL only the offsets and *nnz are produced, so the caller
+ *        can size rev_srcs and call again.  nnz: number of edges. */
+grand_status grand_export_graph(grand_index *h, uint32_t *adj, uint32_t *deg, uint8_t *active, uint32_t *medoid,
+                                uint32_t *rev_offsets, uint32_t *rev_srcs, uint64_t *nnz);
+
+/* Replaces the whole state: vecs (capacity rows, packed), adj (capacity x
+ * R), deg, active (capacity bytes), medoid.  Lists must hold only active ids
+ * without repeats.  Used to resume from an exported state and by tests.
+ * Errors: GRAND_E_ARG (malformed lists). */
+grand_status grand_import_graph(grand_index *h, const void *vecs, const uint32_t *adj, const uint32_t *deg,
+                                const uint8_t *active, uint32_t medoid);
+
+/* Per-phase timing and work counters. */
+enum {
+  GRAND_PH_VALIDATE = 0, GRAND_PH_STAGE, GRAND_PH_SEARCH_INSERT, GRAND_PH_BOOTSTRAP, GRAND_PH_PRUNE_FWD,
+  GRAND_PH_GROUP, GRAND_PH_REBUILD, GRAND_PH_SEARCH_DELETE, GRAND_PH_REVERSE, GRAND_PH_REPAIR,
+  GRAND_PH_CLEAR, GRAND_PH_MEDOID, GRAND_PH_SEARCH_QUERY, GRAND_PH_CAGRA_DETOUR, GRAND_PH_CAGRA_PICKONE,
+  GRAND_NPHASE
+};
+
+typedef struct {
+  uint32_t struct_size;            /* sizeof(grand_stats_t) */
+  uint32_t timing_enabled;
+  uint64_t inserted, deleted, queried;
+  uint64_t search_hops[3];         /* [insert, delete, query] searches: nodes expanded */
+  uint64_t search_evals[3];        /* distance evaluations (row gathers) of those searches */
+  uint64_t prune_evals;            /* pairwise distance evaluations in prunes */
+  uint64_t prunes;                 /* GrANDRobustPrune invocations */
+  uint64_t dirty;                  /* dirty nodes rebuilt (or CAGRA targets / affected nodes) */
+  uint64_t records;                /* reverse-edge / repair records emitted */
+  uint64_t rev_edges;              /* edges scanned by reverse-graph builds */
+  double phase_ms[GRAND_NPHASE];   /* summed kernel time per phase (timing enabled) */
+  uint64_t phase_calls[GRAND_NPHASE];
+} grand_stats_t;
+
+/* Enables (1) or disables (0) per-phase HIP event timing on the stream. */
+grand_status grand_set_timing(grand_index *h, int enable);
+grand_status grand_get_stats(grand_index *h, grand_stats_t *out);
+grand_status grand_reset_stats(grand_index *h);
+
+/* Text of the last error on this handle ("" if none). */
+const char *grand_last_error(const grand_index *h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GRAND_H */

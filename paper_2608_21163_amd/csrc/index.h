@@ -1,0 +1,188 @@
+// index.h -- internal definitions shared by the host orchestration and the
+// kernel translation units of the library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/grand.h"
+
+namespace gr {
+
+// Device-side counters and small scalars, one struct per index.
+struct DevScalars {
+  unsigned long long hops[3];       // nodes expanded by [insert, delete, query] searches
+  unsigned long long evals[3];      // row gathers of those searches
+  unsigned long long prune_evals;
+  unsigned long long prunes;
+  unsigned long long dirty;
+  unsigned long long records;
+  unsigned long long rev_edges;
+  uint32_t err_code;                // first validation error (0 = none)
+  uint32_t err_id;
+  uint32_t n_dirty;                 // number of entries in the dirty / affected list
+  uint32_t medoid;
+  unsigned long long best_bits;     // medoid search: smallest squared distance (bit pattern)
+  uint32_t best_id;
+  uint32_t need_medoid;             // medoid kernels run only when set
+  unsigned long long n_count;       // scratch counter (active ids at import)
+};
+
+enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4 };
+
+// Vector-layout classes: lanes per row (LPV) and 16-byte chunks per lane
+// (CPL) of the distance machinery, chosen from the padded row length.
+enum { kVcA = 0, kVcB = 1, kVcC = 2 };  // <= 8 chunks, <= 32 chunks, <= 256 chunks
+
+// Pool view passed to kernels.
+struct PoolView {
+  uint8_t *vecs;
+  uint32_t *adj;
+  uint32_t *deg;
+  uint8_t *active;
+  size_t stride;   // bytes per pool row (multiple of 16)
+  int nch;         // 16-byte chunks per row
+  uint32_t R;
+  uint32_t cap;
+};
+
+struct SearchArgs {
+  PoolView pool;
+  const uint8_t *qbase;       // query rows (padded to the pool stride) ...
+  const uint32_t *qids;       // ... or pool ids used as queries (if non-null)
+  uint32_t nq;
+  uint32_t start;
+  uint32_t ell;
+  uint32_t max_iters;
+  int which;                  // 0 insert, 1 delete, 2 query (counter slot)
+  // V output: expanded nodes with their distances
+  uint32_t *v_ids;
+  float *v_d;
+  uint32_t *v_n;
+  uint32_t v_stride;
+  // C output: the first c_out entries of C whose id is not flagged in c_filter
+  uint32_t *c_ids;
+  float *c_d;
+  uint32_t c_out;
+  const uint8_t *c_filter;
+  DevScalars *ds;
+};
+
+struct BootArgs {
+  PoolView pool;
+  const uint32_t *ids;        // batch ids (already staged in the pool)
+  uint32_t n;
+  uint32_t want;              // neighbours kept per point
+  uint32_t *o_ids;            // n x o_stride, sorted by (distance, id)
+  float *o_d;
+  uint32_t *o_n;              // count per point (may be null)
+  uint32_t o_stride;
+};
+
+struct FwdPruneArgs {
+  PoolView pool;
+  const uint32_t *ids;
+  uint32_t n;
+  const uint32_t *v_ids;
+  const float *v_d;
+  const uint32_t *v_n;
+  uint32_t v_stride;
+  double coef;                // alpha (or alpha^2) in fp64
+  uint32_t *rec_t, *rec_s;    // n x R reverse-edge records
+  float *rec_d;
+  DevScalars *ds;
+};
+
+struct RebuildArgs {
+  PoolView pool;
+  const uint32_t *dirty;
+  const uint32_t *goff;       // group offsets by target id (cap + 1)
+  const uint32_t *gsrc;
+  const float *gd;
+  const uint8_t *in_batch;    // delete: ids of the batch (null for insert)
+  uint32_t P;
+  double coef;
+  DevScalars *ds;
+};
+
+struct RepairArgs {
+  PoolView pool;
+  const uint32_t *ids;
+  uint32_t n;
+  const uint8_t *in_batch;
+  const uint32_t *ci;         // n x kr repair candidates (INVALID padded)
+  uint32_t kr;
+  const uint32_t *rev_off;
+  const uint32_t *rev_src;
+  int rev_by_batch;           // reverse rows indexed by batch position (1) or by id (0)
+  uint32_t c;
+  const uint32_t *rofs;       // record offsets per deleted node (n + 1)
+  uint32_t *rec_t, *rec_s;
+  float *rec_d;
+  DevScalars *ds;
+};
+
+struct CagraArgs {
+  PoolView pool;
+  const uint32_t *list;       // dirty targets (detour) or affected nodes (pickone)
+  const uint32_t *goff;       // detour: group offsets by target
+  const uint32_t *gsrc;
+  const float *gd;
+  const uint32_t *bidx;       // batch position of each batch id
+  const uint32_t *fwd;        // n x R forward lists of the new nodes (snapshot)
+  const uint8_t *in_batch;
+  const uint32_t *rev_off;
+  const uint32_t *rev_src;
+  int rev_by_batch;
+  const uint32_t *rec_t, *rec_s;   // racing mode: raw records
+  uint32_t nrec;
+  DevScalars *ds;
+};
+
+// ---- launchers (defined in the kernel translation units) ----------------
+int vec_class(int nch);
+hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t s);
+hipError_t launch_bootstrap(int kind, int vc, const BootArgs &a, hipStream_t s);
+hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPruneArgs &a, hipStream_t s);
+hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const RebuildArgs &a, uint32_t grid,
+                          hipStream_t s);
+hipError_t launch_repair(int kind, int vc, const RepairArgs &a, hipStream_t s);
+hipError_t launch_repair_count(const RepairArgs &a, uint32_t *counts, hipStream_t s);
+
+hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s);
+hipError_t launch_fill_u8(uint8_t *p, uint8_t v, size_t n, hipStream_t s);
+hipError_t launch_validate_ids(const uint32_t *ids, uint32_t n, uint32_t cap, const uint8_t *active,
+                               uint32_t *mark, uint32_t epoch, int want_active, DevScalars *ds, hipStream_t s);
+hipError_t launch_check_finite(const uint8_t *rows, uint32_t n, size_t stride, uint32_t dim, DevScalars *ds,
+                               hipStream_t s);
+hipError_t launch_stage(PoolView p, const uint8_t *rows, const uint32_t *ids, uint32_t n, uint32_t *bidx,
+                        hipStream_t s);
+hipError_t launch_mark_batch(const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t *bidx, uint8_t v,
+                             hipStream_t s);
+hipError_t launch_clear_rows(PoolView p, const uint32_t *ids, uint32_t n, hipStream_t s);
+hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec,
+                        uint32_t cap, uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc,
+                        float *gd, uint32_t *dirty, DevScalars *ds, hipStream_t s);
+hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s);
+size_t scan_tmp_words(size_t n);
+hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
+                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, DevScalars *ds,
+                          hipStream_t s);
+hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst,
+                            hipStream_t s);
+hipError_t launch_medoid(PoolView p, int kind, uint32_t dim, uint64_t n_active, void *tmp, DevScalars *ds,
+                         hipStream_t s);
+size_t medoid_tmp_bytes(uint32_t cap, uint32_t dim);
+hipError_t launch_medoid_need(DevScalars *ds, const uint8_t *in_batch, int force, hipStream_t s);
+hipError_t launch_cagra_fwd(PoolView p, const uint32_t *ids, uint32_t n, const uint32_t *c_ids, const float *c_d,
+                            uint32_t *rec_t, uint32_t *rec_s, float *rec_d, hipStream_t s);
+hipError_t launch_cagra_detour(const CagraArgs &a, uint32_t grid, hipStream_t s);
+hipError_t launch_cagra_racing(const CagraArgs &a, hipStream_t s);
+hipError_t launch_cagra_affected(const uint32_t *ids, uint32_t n, const uint8_t *in_batch, const uint32_t *rev_off,
+                                 const uint32_t *rev_src, int by_batch, uint32_t *mark, uint32_t epoch,
+                                 uint32_t *list, DevScalars *ds, hipStream_t s);
+hipError_t launch_cagra_pickone(const CagraArgs &a, uint32_t grid, hipStream_t s);
+
+}  // namespace gr

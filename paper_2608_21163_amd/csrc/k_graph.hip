@@ -1,0 +1,457 @@
+// k_graph.hip -- integer graph kernels: validation, staging of new rows,
+// grouping of reverse-edge records by target (counting sort: histogram,
+// prefix scan, scatter), the on-demand reverse graph in CSR form (Alg. 8,
+// first two loops), clearing deleted rows, and the medoid.
+#include "dispatch.h"
+
+namespace gr {
+
+static inline uint32_t blocks_for(size_t n, uint32_t per) {
+  size_t b = (n + per - 1) / per;
+  if (b > 1u << 30) b = 1u << 30;
+  return (uint32_t)(b == 0 ? 1 : b);
+}
+
+// ---------------------------------------------------------------- fills
+__global__ void k_fill_u32(uint32_t *p, uint32_t v, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+__global__ void k_fill_u8(uint8_t *p, uint8_t v, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  uint32_t g = blocks_for(n, 256);
+  if (g > 65536) g = 65536;
+  hipLaunchKernelGGL(k_fill_u32, dim3(g), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+hipError_t launch_fill_u8(uint8_t *p, uint8_t v, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  uint32_t g = blocks_for(n, 256);
+  if (g > 65536) g = 65536;
+  hipLaunchKernelGGL(k_fill_u8, dim3(g), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+static __device__ void set_error(DevScalars *ds, uint32_t code, uint32_t id) {
+  if (atomicCAS(&ds->err_code, 0u, code) == 0u) ds->err_id = id;
+}
+
+// ---------------------------------------------------------------- validation
+// ids in range, not repeated within the batch (epoch-stamped marks), and
+// in the expected active state.
+__global__ void k_validate_ids(const uint32_t *ids, uint32_t n, uint32_t cap, const uint8_t *active, uint32_t *mark,
+                               uint32_t epoch, int want_active, DevScalars *ds) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t id = ids[i];
+  if (id >= cap) { set_error(ds, kErrRange, id); return; }
+  if (atomicExch(&mark[id], epoch) == epoch) { set_error(ds, kErrRepeat, id); return; }
+  if ((active[id] != 0) != (want_active != 0)) set_error(ds, kErrState, id);
+}
+hipError_t launch_validate_ids(const uint32_t *ids, uint32_t n, uint32_t cap, const uint8_t *active, uint32_t *mark,
+                               uint32_t epoch, int want_active, DevScalars *ds, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_validate_ids, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, n, cap, active, mark, epoch,
+                     want_active, ds);
+  return hipGetLastError();
+}
+
+__global__ void k_check_finite(const uint8_t *rows, uint32_t n, size_t stride, uint32_t dim, DevScalars *ds) {
+  const size_t total = (size_t)n * dim;
+  for (size_t t = blockIdx.x * (size_t)blockDim.x + threadIdx.x; t < total; t += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = t / dim, c = t % dim;
+    const float x = reinterpret_cast<const float *>(rows + r * stride)[c];
+    if (!isfinite(x)) set_error(ds, kErrNonFinite, (uint32_t)r);
+  }
+}
+hipError_t launch_check_finite(const uint8_t *rows, uint32_t n, size_t stride, uint32_t dim, DevScalars *ds,
+                               hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  uint32_t g = blocks_for((size_t)n * dim, 256);
+  if (g > 16384) g = 16384;
+  hipLaunchKernelGGL(k_check_finite, dim3(g), dim3(256), 0, s, rows, n, stride, dim, ds);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- staging
+// Alg. 5 / Alg. 7 first loop: write x_i into slot p_i, empty its list, mark
+// it active; remember each id's batch position.  One wave per new point.
+__global__ void k_stage(PoolView P, const uint8_t *rows, const uint32_t *ids, uint32_t n, uint32_t *bidx) {
+  const uint32_t i = blockIdx.x;
+  if (i >= n) return;
+  const int ln = threadIdx.x;
+  const uint32_t id = ids[i];
+  const uint4 *src = reinterpret_cast<const uint4 *>(rows + (size_t)i * P.stride);
+  uint4 *dst = reinterpret_cast<uint4 *>(P.vecs + (size_t)id * P.stride);
+  for (int c = ln; c < P.nch; c += 64) dst[c] = src[c];
+  if (ln < (int)P.R) P.adj[(size_t)id * P.R + ln] = kInvalid;
+  if (ln == 0) {
+    P.deg[id] = 0;
+    P.active[id] = 1;
+    bidx[id] = i;
+  }
+}
+hipError_t launch_stage(PoolView p, const uint8_t *rows, const uint32_t *ids, uint32_t n, uint32_t *bidx,
+                        hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_stage, dim3(n), dim3(64), 0, s, p, rows, ids, n, bidx);
+  return hipGetLastError();
+}
+
+__global__ void k_mark_batch(const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t *bidx, uint8_t v) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  in_batch[ids[i]] = v;
+  if (bidx) bidx[ids[i]] = i;
+}
+hipError_t launch_mark_batch(const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t *bidx, uint8_t v,
+                             hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_mark_batch, dim3(blocks_for(n, 256)), dim3(256), 0, s, ids, n, in_batch, bidx, v);
+  return hipGetLastError();
+}
+
+// Alg. 6 / Alg. 8 last loop: N_out(p_i) <- empty; the slot becomes free.
+__global__ void k_clear_rows(PoolView P, const uint32_t *ids, uint32_t n) {
+  const uint32_t i = blockIdx.x;
+  if (i >= n) return;
+  const int ln = threadIdx.x;
+  const uint32_t id = ids[i];
+  if (ln < (int)P.R) P.adj[(size_t)id * P.R + ln] = kInvalid;
+  if (ln == 0) {
+    P.deg[id] = 0;
+    P.active[id] = 0;
+  }
+}
+hipError_t launch_clear_rows(PoolView p, const uint32_t *ids, uint32_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_clear_rows, dim3(n), dim3(64), 0, s, p, ids, n);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- scan
+// Exclusive prefix sum of n u32 values into out[0..n], out[n] = total, in
+// three passes over tiles of 4096 (tile sums, scan of tile sums, apply).
+constexpr int kScanThreads = 256;
+constexpr int kScanPer = 16;
+constexpr int kScanTile = kScanThreads * kScanPer;
+
+size_t scan_tmp_words(size_t n) { return (n + kScanTile - 1) / kScanTile + 2; }
+
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *wsum, uint32_t &total) {
+  const int ln = lane(), w = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (ln >= o) x += y;
+  }
+  if (ln == 63) wsum[w] = x;
+  __syncthreads();
+  uint32_t off = 0, tot = 0;
+  for (int k = 0; k < (int)(blockDim.x >> 6); k++) {
+    if (k < w) off += wsum[k];
+    tot += wsum[k];
+  }
+  __syncthreads();
+  total = tot;
+  return off + x - v;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_tiles(const uint32_t *in, size_t n, uint32_t *tsum) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t base = (size_t)blockIdx.x * kScanTile + (size_t)threadIdx.x * kScanPer;
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) s += base + k < n ? in[base + k] : 0u;
+  uint32_t total;
+  block_excl_scan(s, wsum, total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_tsum(uint32_t *tsum, uint32_t nt) {
+  __shared__ uint32_t wsum[16];
+  uint32_t carry = 0;
+  for (uint32_t b0 = 0; b0 < nt; b0 += 1024) {
+    const uint32_t i = b0 + threadIdx.x;
+    const uint32_t v = i < nt ? tsum[i] : 0u;
+    uint32_t total;
+    const uint32_t ex = block_excl_scan(v, wsum, total);
+    if (i < nt) tsum[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) tsum[nt] = carry;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(const uint32_t *in, size_t n, const uint32_t *tsum,
+                                                             uint32_t nt, uint32_t *out) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t base = (size_t)blockIdx.x * kScanTile + (size_t)threadIdx.x * kScanPer;
+  uint32_t v[kScanPer];
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    v[k] = base + k < n ? in[base + k] : 0u;
+    s += v[k];
+  }
+  uint32_t total;
+  uint32_t run = tsum[blockIdx.x] + block_excl_scan(s, wsum, total);
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    if (base + k < n) out[base + k] = run;
+    run += v[k];
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = tsum[nt];
+}
+
+hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s) {
+  const uint32_t nt = (uint32_t)((n + kScanTile - 1) / kScanTile);
+  if (nt == 0) return launch_fill_u32(out, 0u, 1, s);
+  hipLaunchKernelGGL(k_scan_tiles, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp);
+  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(1024), 0, s, tmp, nt);
+  hipLaunchKernelGGL(k_scan_apply, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp, nt, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- grouping
+// Reverse-edge records (target, src, dist) grouped by target: counts per
+// target (the first record of a target appends it to the dirty list),
+// exclusive scan, scatter.  The scatter counts back down, so `cnt` is all
+// zero again afterwards.  Order inside a group is arbitrary; consumers
+// order records by (dist, src).
+__global__ void k_group_hist(const uint32_t *rec_t, size_t nrec, uint32_t *cnt, uint32_t *dirty, DevScalars *ds) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nrec; i += (size_t)gridDim.x * blockDim.x) {
+    const uint32_t t = rec_t[i];
+    if (t == kInvalid) continue;
+    if (atomicAdd(&cnt[t], 1u) == 0u) dirty[atomicAdd(&ds->n_dirty, 1u)] = t;
+  }
+}
+__global__ void k_group_scatter(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec,
+                                uint32_t *cnt, const uint32_t *off, uint32_t *gsrc, float *gd) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nrec; i += (size_t)gridDim.x * blockDim.x) {
+    const uint32_t t = rec_t[i];
+    if (t == kInvalid) continue;
+    const uint32_t pos = off[t] + atomicSub(&cnt[t], 1u) - 1u;
+    gsrc[pos] = rec_s[i];
+    gd[pos] = rec_d[i];
+  }
+}
+__global__ void k_zero_ndirty(DevScalars *ds) { ds->n_dirty = 0; }
+
+hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec, uint32_t cap,
+                        uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc, float *gd,
+                        uint32_t *dirty, DevScalars *ds, hipStream_t s) {
+  hipLaunchKernelGGL(k_zero_ndirty, dim3(1), dim3(1), 0, s, ds);
+  uint32_t g = blocks_for(nrec, 256);
+  if (g > 8192) g = 8192;
+  if (nrec) hipLaunchKernelGGL(k_group_hist, dim3(g), dim3(256), 0, s, rec_t, nrec, cnt, dirty, ds);
+  hipError_t e = launch_scan(cnt, off, cap, scan_tmp, s);
+  if (e != hipSuccess) return e;
+  if (nrec) hipLaunchKernelGGL(k_group_scatter, dim3(g), dim3(256), 0, s, rec_t, rec_s, rec_d, nrec, cnt, off, gsrc, gd);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- reverse graph
+// N_in as CSR (Alg. 8): every edge u -> v of an active row u is counted
+// into v's row (by_batch: only edges into the delete batch, counted into
+// the batch position of v), the counts are scanned, and sources are
+// scattered.  Rows are in arbitrary order here; consumers that need an
+// order derive it from the ids (rank of u = number of sources below u).
+__global__ void k_rev_hist(PoolView P, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t *cnt) {
+  const size_t total = (size_t)P.cap * P.R;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const uint32_t v = P.adj[i];
+    if (v == kInvalid) continue;
+    const uint32_t u = (uint32_t)(i / P.R);
+    if (!P.active[u]) continue;
+    if (by_batch) {
+      if (in_batch[v]) atomicAdd(&cnt[bidx[v]], 1u);
+    } else {
+      atomicAdd(&cnt[v], 1u);
+    }
+  }
+}
+__global__ void k_rev_scatter(PoolView P, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t *cnt,
+                              const uint32_t *off, uint32_t *src) {
+  const size_t total = (size_t)P.cap * P.R;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const uint32_t v = P.adj[i];
+    if (v == kInvalid) continue;
+    const uint32_t u = (uint32_t)(i / P.R);
+    if (!P.active[u]) continue;
+    uint32_t row;
+    if (by_batch) {
+      if (!in_batch[v]) continue;
+      row = bidx[v];
+    } else {
+      row = v;
+    }
+    const uint32_t pos = off[row] + atomicSub(&cnt[row], 1u) - 1u;
+    src[pos] = u;
+  }
+}
+__global__ void k_count_edges(const uint32_t *off, uint32_t nrows, DevScalars *ds) {
+  if (threadIdx.x == 0) atomicAdd(&ds->rev_edges, (unsigned long long)off[nrows]);
+}
+
+hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
+                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, DevScalars *ds,
+                          hipStream_t s) {
+  const size_t total = (size_t)p.cap * p.R;
+  uint32_t g = blocks_for(total, 256);
+  if (g > 16384) g = 16384;
+  hipLaunchKernelGGL(k_rev_hist, dim3(g), dim3(256), 0, s, p, by_batch, in_batch, bidx, cnt);
+  hipError_t e = launch_scan(cnt, off, nrows, scan_tmp, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rev_scatter, dim3(g), dim3(256), 0, s, p, by_batch, in_batch, bidx, cnt, off, src);
+  hipLaunchKernelGGL(k_count_edges, dim3(1), dim3(64), 0, s, off, nrows, ds);
+  return hipGetLastError();
+}
+
+// Rows of a CSR sorted ascending into dst (one wave per row; sources in a
+// row are distinct).  Rows up to 64 use a register bitonic sort, longer rows
+// a rank count.
+__global__ __launch_bounds__(64) void k_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src,
+                                                  uint32_t *dst) {
+  const int ln = lane();
+  for (uint32_t r = blockIdx.x; r < nrows; r += gridDim.x) {
+    const uint32_t b = off[r], e = off[r + 1], len = e - b;
+    if (len == 0) continue;
+    if (len <= 64) {
+      float d[1] = {0.0f};
+      uint32_t v[1] = {ln < (int)len ? src[b + ln] : kInvalid};
+      wave_sort<1>(d, v);
+      if (ln < (int)len) dst[b + ln] = v[0];
+    } else {
+      for (uint32_t i = ln; i < len; i += 64) {
+        const uint32_t x = src[b + i];
+        uint32_t rank = 0;
+        for (uint32_t j = 0; j < len; j++) rank += src[b + j] < x ? 1u : 0u;
+        dst[b + rank] = x;
+      }
+    }
+  }
+}
+hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst, hipStream_t s) {
+  if (nrows == 0) return hipSuccess;
+  uint32_t g = nrows < 65536 ? nrows : 65536;
+  hipLaunchKernelGGL(k_sort_rows, dim3(g), dim3(64), 0, s, off, nrows, src, dst);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- medoid
+// The active id minimising (fp64 squared distance to the centroid, id).
+// Centroid: exact integer sums for uint8; for fp32, blocks of 1024
+// consecutive ids summed in id order, block sums added in block order;
+// divided by the active count.  Distance: fused multiply-add chain in
+// dimension order.  The smallest distance is found with a 64-bit atomic min
+// on its bit pattern (non-negative doubles order like their bits), then the
+// smallest id with exactly that distance.
+constexpr uint32_t kCentroidBlock = 1024;
+
+size_t medoid_tmp_bytes(uint32_t cap, uint32_t dim) {
+  const size_t nb = (cap + kCentroidBlock - 1) / kCentroidBlock;
+  return (nb * dim + dim) * sizeof(double) + 64;
+}
+
+__global__ void k_centroid_part(PoolView P, int kind, uint32_t dim, double *part, const DevScalars *ds) {
+  if (!ds->need_medoid) return;
+  const uint32_t j = blockIdx.y * blockDim.x + threadIdx.x;
+  const uint32_t b = blockIdx.x;
+  if (j >= dim) return;
+  const uint32_t i0 = b * kCentroidBlock;
+  const uint32_t i1 = i0 + kCentroidBlock < P.cap ? i0 + kCentroidBlock : P.cap;
+  if (kind == kU8L2) {
+    unsigned long long s = 0;
+    for (uint32_t i = i0; i < i1; i++)
+      if (P.active[i]) s += P.vecs[(size_t)i * P.stride + j];
+    part[(size_t)b * dim + j] = (double)s;  // < 2^53: exact
+  } else {
+    double s = 0.0;
+    for (uint32_t i = i0; i < i1; i++)
+      if (P.active[i]) s = s + (double)reinterpret_cast<const float *>(P.vecs + (size_t)i * P.stride)[j];
+    part[(size_t)b * dim + j] = s;
+  }
+}
+__global__ void k_centroid_sum(int kind, uint32_t dim, uint32_t nb, const double *part, double *cent,
+                               unsigned long long n, DevScalars *ds) {
+  if (!ds->need_medoid) return;
+  const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j == 0) {
+    ds->best_bits = ~0ull;
+    ds->best_id = kInvalid;
+  }
+  if (j >= dim) return;
+  if (kind == kU8L2) {
+    unsigned long long s = 0;
+    for (uint32_t b = 0; b < nb; b++) s += (unsigned long long)part[(size_t)b * dim + j];
+    cent[j] = (double)s / (double)n;
+  } else {
+    double t = 0.0;
+    for (uint32_t b = 0; b < nb; b++) t = t + part[(size_t)b * dim + j];
+    cent[j] = t / (double)n;
+  }
+}
+__device__ __forceinline__ double dist_to_centroid(const PoolView &P, int kind, uint32_t dim, uint32_t i,
+                                                   const double *cent) {
+  double s = 0.0;
+  const uint8_t *row = P.vecs + (size_t)i * P.stride;
+  for (uint32_t j = 0; j < dim; j++) {
+    const double x = kind == kU8L2 ? (double)row[j] : (double)reinterpret_cast<const float *>(row)[j];
+    const double t = x - cent[j];
+    s = __builtin_fma(t, t, s);
+  }
+  return s;
+}
+__global__ void k_medoid_min(PoolView P, int kind, uint32_t dim, const double *cent, DevScalars *ds) {
+  if (!ds->need_medoid) return;
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= P.cap || !P.active[i]) return;
+  const double s = dist_to_centroid(P, kind, dim, i, cent);
+  atomicMin(&ds->best_bits, (unsigned long long)__double_as_longlong(s));
+}
+__global__ void k_medoid_arg(PoolView P, int kind, uint32_t dim, const double *cent, DevScalars *ds) {
+  if (!ds->need_medoid) return;
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= P.cap || !P.active[i]) return;
+  const double s = dist_to_centroid(P, kind, dim, i, cent);
+  if ((unsigned long long)__double_as_longlong(s) == ds->best_bits) atomicMin(&ds->best_id, i);
+}
+__global__ void k_medoid_store(DevScalars *ds) {
+  if (ds->need_medoid) ds->medoid = ds->best_id;
+  ds->need_medoid = 0;
+}
+// A new medoid is needed when the current one is in the delete batch.
+__global__ void k_medoid_need(DevScalars *ds, const uint8_t *in_batch, int force) {
+  const uint32_t m = ds->medoid;
+  ds->need_medoid = force ? 1u : ((m != kInvalid && in_batch && in_batch[m]) ? 1u : 0u);
+}
+hipError_t launch_medoid_need(DevScalars *ds, const uint8_t *in_batch, int force, hipStream_t s) {
+  hipLaunchKernelGGL(k_medoid_need, dim3(1), dim3(1), 0, s, ds, in_batch, force);
+  return hipGetLastError();
+}
+
+hipError_t launch_medoid(PoolView p, int kind, uint32_t dim, uint64_t n_active, void *tmp, DevScalars *ds,
+                         hipStream_t s) {
+  if (n_active == 0) {
+    hipLaunchKernelGGL(k_centroid_sum, dim3(1), dim3(64), 0, s, kind, 0u, 0u, (const double *)nullptr,
+                       (double *)nullptr, 1ull, ds);
+    hipLaunchKernelGGL(k_medoid_store, dim3(1), dim3(1), 0, s, ds);
+    return hipGetLastError();
+  }
+  const uint32_t nb = (p.cap + kCentroidBlock - 1) / kCentroidBlock;
+  double *part = reinterpret_cast<double *>(tmp);
+  double *cent = part + (size_t)nb * dim;
+  hipLaunchKernelGGL(k_centroid_part, dim3(nb, (dim + 63) / 64), dim3(64), 0, s, p, kind, dim, part,
+                     (const DevScalars *)ds);
+  hipLaunchKernelGGL(k_centroid_sum, dim3((dim + 63) / 64), dim3(64), 0, s, kind, dim, nb, part, cent,
+                     (unsigned long long)n_active, ds);
+  hipLaunchKernelGGL(k_medoid_min, dim3(blocks_for(p.cap, 256)), dim3(256), 0, s, p, kind, dim, cent, ds);
+  hipLaunchKernelGGL(k_medoid_arg, dim3(blocks_for(p.cap, 256)), dim3(256), 0, s, p, kind, dim, cent, ds);
+  hipLaunchKernelGGL(k_medoid_store, dim3(1), dim3(1), 0, s, ds);
+  return hipGetLastError();
+}
+
+}  // namespace gr

@@ -1,0 +1,193 @@
+// k_search.hip -- BeamSearch (Alg. 1), one wavefront per query, and the
+// brute-force candidate search that bootstraps an empty index.
+//
+// Search state of one wave:
+//   C : the l closest (distance, id) keys seen so far, ascending, held in
+//       registers as NR rows of 64 keys (element e = row*64 + lane); the top
+//       id bit marks keys already expanded (the set V).
+//   a lossy hash of ids whose distance was already evaluated, in LDS.  An
+//       evaluated id either is in C or can never enter it again (the l-th
+//       key only decreases once C is full), so skipping it is exact; the
+//       hash may forget ids (they are then evaluated again and dropped by
+//       the exact repeat check of the merge), but never reports an id that
+//       was not evaluated.
+// Each hop expands the smallest unexpanded key u, reads u's list (one slot
+// per lane), drops ids found in the hash, gathers the remaining rows
+// LPV lanes per row, and merges the new keys into C keeping the l smallest.
+#include "dispatch.h"
+
+namespace gr {
+
+constexpr int kHashBits = 11;
+constexpr int kHashSize = 1 << kHashBits;
+
+__device__ __forceinline__ uint32_t hslot(uint32_t v) { return (v * 0x9E3779B1u) >> (32 - kHashBits); }
+
+template <int KIND, int LPV, int CPL, int NR>
+__global__ __launch_bounds__(64) void k_search(SearchArgs a) {
+  __shared__ uint32_t hsh[kHashSize];
+  __shared__ uint32_t nid[64];
+  __shared__ float nkey[64];
+  const int ln = lane();
+  const uint32_t qi = blockIdx.x;
+  if (qi >= a.nq) return;
+  const PoolView &P = a.pool;
+  const uint8_t *qrow = a.qids ? P.vecs + (size_t)a.qids[qi] * P.stride : a.qbase + (size_t)qi * P.stride;
+  Slice<KIND, LPV, CPL> s;
+  load_slice<KIND, LPV, CPL>(s, qrow, P.nch);
+  for (int i = ln; i < kHashSize; i += 64) hsh[i] = kInvalid;
+
+  float cd[NR];
+  uint32_t ci[NR];
+#pragma unroll
+  for (int r = 0; r < NR; r++) { cd[r] = finf(); ci[r] = kInvalid; }
+  if (a.start < P.cap) {  // an invalid start leaves C empty: no expansion
+    const float d0 = wave_dist1<KIND, LPV, CPL>(s, P.vecs + (size_t)a.start * P.stride, P.nch);
+    if (ln == 0) { cd[0] = d0; ci[0] = a.start; }
+  }
+  __syncthreads();
+  if (ln == 0) hsh[hslot(a.start)] = a.start;
+  __syncthreads();
+  uint32_t nv = 0, evals = 1;
+
+  while (nv < a.max_iters) {
+    // u = argmin over C \ V
+    int e = -1;
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      const uint64_t m = ballot(kvalid(ci[r]) && !(ci[r] & kVisit));
+      if (e < 0 && m) e = r * 64 + ffs64(m);
+    }
+    if (e < 0) break;
+    const int er = e >> 6, el = e & 63;
+    uint32_t u = 0;
+    float du = 0.0f;
+#pragma unroll
+    for (int r = 0; r < NR; r++)
+      if (r == er) {
+        u = rdlane(ci[r], el) & kIdMask;
+        du = rdlane(cd[r], el);
+        if (ln == el) ci[r] |= kVisit;
+      }
+    if (a.v_ids && ln == 0) {
+      a.v_ids[(size_t)qi * a.v_stride + nv] = u;
+      a.v_d[(size_t)qi * a.v_stride + nv] = du;
+    }
+    nv++;
+    // C <- C u N_out(u), skipping ids already evaluated
+    const uint32_t v = ln < (int)P.R ? P.adj[(size_t)u * P.R + ln] : kInvalid;
+    const uint32_t hs = hslot(v);
+    bool need = v != kInvalid && hsh[hs] != v;
+    __syncthreads();
+    if (need) hsh[hs] = v;
+    const uint64_t m = ballot(need);
+    const int cnt = popc(m);
+    if (cnt == 0) continue;
+    if (need) nid[mbcnt(m)] = v;
+    __syncthreads();
+    wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, nid, nkey, cnt);
+    __syncthreads();
+    evals += cnt;
+    const float nd = ln < cnt ? nkey[ln] : finf();
+    const uint32_t ni = ln < cnt ? nid[ln] : kInvalid;
+    wave_merge_new<NR>(cd, ci, nd, ni, (int)a.ell);
+    __syncthreads();
+  }
+
+  if (a.v_n && ln == 0) a.v_n[qi] = nv;
+  if (a.c_ids) {
+    int base = 0;
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      const uint32_t id = ci[r] & kIdMask;
+      const bool ok = kvalid(ci[r]) && !(a.c_filter && a.c_filter[id]);
+      const uint64_t mm = ballot(ok);
+      const int pos = base + mbcnt(mm);
+      if (ok && pos < (int)a.c_out) {
+        a.c_ids[(size_t)qi * a.c_out + pos] = id;
+        a.c_d[(size_t)qi * a.c_out + pos] = cd[r];
+      }
+      base += popc(mm);
+    }
+    for (int t = base + ln; t < (int)a.c_out; t += 64) {
+      a.c_ids[(size_t)qi * a.c_out + t] = kInvalid;
+      a.c_d[(size_t)qi * a.c_out + t] = finf();
+    }
+  }
+  if (ln == 0) {
+    atomicAdd(&a.ds->hops[a.which], (unsigned long long)nv);
+    atomicAdd(&a.ds->evals[a.which], (unsigned long long)evals);
+  }
+}
+
+// Empty index at the start of a batch: the candidates of each new point are
+// its `want` nearest other points of the batch, by brute force over the
+// batch, kept sorted by (distance, id).
+template <int KIND, int LPV, int CPL, int NR>
+__global__ __launch_bounds__(64) void k_bootstrap(BootArgs a) {
+  __shared__ uint32_t nid[64];
+  __shared__ float nkey[64];
+  const int ln = lane();
+  const uint32_t i = blockIdx.x;
+  if (i >= a.n) return;
+  const PoolView &P = a.pool;
+  const uint32_t p = a.ids[i];
+  Slice<KIND, LPV, CPL> s;
+  load_slice<KIND, LPV, CPL>(s, P.vecs + (size_t)p * P.stride, P.nch);
+  float cd[NR];
+  uint32_t ci[NR];
+#pragma unroll
+  for (int r = 0; r < NR; r++) { cd[r] = finf(); ci[r] = kInvalid; }
+  for (uint32_t base = 0; base < a.n; base += 64) {
+    const uint32_t j = base + ln;
+    const bool ok = j < a.n && j != i;
+    const uint32_t v = j < a.n ? a.ids[j] : kInvalid;
+    const uint64_t m = ballot(ok);
+    const int cnt = popc(m);
+    if (ok) nid[mbcnt(m)] = v;
+    __syncthreads();
+    wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, nid, nkey, cnt);
+    __syncthreads();
+    const float nd = ln < cnt ? nkey[ln] : finf();
+    const uint32_t ni = ln < cnt ? nid[ln] : kInvalid;
+    wave_merge_new<NR>(cd, ci, nd, ni, (int)a.want);
+    __syncthreads();
+  }
+  const uint32_t got = a.n - 1 < a.want ? a.n - 1 : a.want;
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    const int e = r * 64 + ln;
+    if (e < (int)a.o_stride) {
+      a.o_ids[(size_t)i * a.o_stride + e] = (uint32_t)e < got ? (ci[r] & kIdMask) : kInvalid;
+      a.o_d[(size_t)i * a.o_stride + e] = (uint32_t)e < got ? cd[r] : finf();
+    }
+  }
+  if (a.o_n && ln == 0) a.o_n[i] = got;
+}
+
+int vec_class(int nch) {
+  if (nch <= 8) return kVcA;
+  if (nch <= 32) return kVcB;
+  if (nch <= 256) return kVcC;
+  return -1;
+}
+
+hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t st) {
+  if (a.nq == 0) return hipSuccess;
+  GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.ell, {
+    hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR>), dim3(a.nq), dim3(64), 0, st, a);
+    return hipGetLastError();
+  }));
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_bootstrap(int kind, int vc, const BootArgs &a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.want, {
+    hipLaunchKernelGGL((k_bootstrap<KIND, LPV, CPL, NR>), dim3(a.n), dim3(64), 0, st, a);
+    return hipGetLastError();
+  }));
+  return hipErrorInvalidValue;
+}
+
+}  // namespace gr

@@ -1,0 +1,219 @@
+// wave.h -- wavefront-level building blocks for gfx950 (wave64).
+//
+// Everything here is executed by one 64-lane wavefront cooperating through
+// cross-lane shuffles, ballots and a little LDS; nothing synchronises across
+// waves.  Keys are (distance, id) pairs ordered lexicographically; the top
+// bit of an id is used as a per-entry "expanded" flag by the search, so key
+// comparisons mask it.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gr {
+
+constexpr uint32_t kInvalid = 0xFFFFFFFFu;
+constexpr uint32_t kVisit = 0x80000000u;
+constexpr uint32_t kIdMask = 0x7FFFFFFFu;
+
+__device__ __forceinline__ float finf() { return __builtin_inff(); }
+__device__ __forceinline__ int lane() { return (int)__lane_id(); }
+
+__device__ __forceinline__ bool kless(float a, uint32_t ia, float b, uint32_t ib) {
+  return a < b || (a == b && (ia & kIdMask) < (ib & kIdMask));
+}
+__device__ __forceinline__ bool kequal(float a, uint32_t ia, float b, uint32_t ib) {
+  return a == b && (ia & kIdMask) == (ib & kIdMask);
+}
+__device__ __forceinline__ bool kvalid(uint32_t id) { return (id & kIdMask) != kIdMask; }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return (uint64_t)__ballot(p); }
+__device__ __forceinline__ int popc(uint64_t m) { return __popcll(m); }
+// number of set bits of m strictly below this lane
+__device__ __forceinline__ int mbcnt(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+__device__ __forceinline__ int ffs64(uint64_t m) { return __ffsll((unsigned long long)m) - 1; }
+__device__ __forceinline__ int fls64(uint64_t m) { return 63 - __clzll((unsigned long long)m); }
+
+template <class T> __device__ __forceinline__ T rdlane(T v, int l);
+template <> __device__ __forceinline__ uint32_t rdlane(uint32_t v, int l) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+template <> __device__ __forceinline__ float rdlane(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// Compare-exchange of this lane's element with the element j lanes away.
+// keep_min: this lane ends with the smaller key of the pair.
+__device__ __forceinline__ void cx_lane(float& d, uint32_t& id, int j, bool keep_min) {
+  float od = __shfl_xor(d, j, 64);
+  uint32_t oi = __shfl_xor(id, j, 64);
+  bool take = keep_min ? kless(od, oi, d, id) : kless(d, id, od, oi);
+  if (take) { d = od; id = oi; }
+}
+
+// Compare-exchange of register rows a (lower index) and b (higher index).
+__device__ __forceinline__ void cx_reg(float& da, uint32_t& ia, float& db, uint32_t& ib, bool up) {
+  bool sw = up ? kless(db, ib, da, ia) : kless(da, ia, db, ib);
+  if (sw) {
+    float t = da; da = db; db = t;
+    uint32_t u = ia; ia = ib; ib = u;
+  }
+}
+
+// Bitonic sort, ascending, of N*64 keys held as element e = r*64 + lane.
+template <int N>
+__device__ __forceinline__ void wave_sort(float (&d)[N], uint32_t (&id)[N]) {
+  const int ln = lane();
+#pragma unroll
+  for (int k = 2; k <= 64 * N; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j >= 64) {
+        const int jr = j >> 6;
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const int p = r ^ jr;
+          if (p > r) cx_reg(d[r], id[r], d[p], id[p], ((r * 64 + ln) & k) == 0);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const bool up = ((r * 64 + ln) & k) == 0;
+          const bool lower = (ln & j) == 0;
+          cx_lane(d[r], id[r], j, lower == up);
+        }
+      }
+    }
+  }
+}
+
+// Bitonic merge (input bitonic) to ascending order.
+template <int N>
+__device__ __forceinline__ void wave_merge_up(float (&d)[N], uint32_t (&id)[N]) {
+  const int ln = lane();
+#pragma unroll
+  for (int j = 32 * N; j > 0; j >>= 1) {
+    if (j >= 64) {
+      const int jr = j >> 6;
+#pragma unroll
+      for (int r = 0; r < N; r++) {
+        const int p = r ^ jr;
+        if (p > r) cx_reg(d[r], id[r], d[p], id[p], true);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < N; r++) cx_lane(d[r], id[r], j, (ln & j) == 0);
+    }
+  }
+}
+
+// Marks (in dup[]) every element of an ascending list whose key equals the
+// key of the element just before it; returns the ballot of all marks.
+template <int N>
+__device__ __forceinline__ uint64_t wave_find_repeats(const float (&d)[N], const uint32_t (&id)[N],
+                                                      uint64_t (&dm)[N]) {
+  const int ln = lane();
+  uint64_t any = 0;
+#pragma unroll
+  for (int r = 0; r < N; r++) {
+    float pd = __shfl_up(d[r], 1, 64);
+    uint32_t pi = __shfl_up(id[r], 1, 64);
+    if (r > 0) {
+      float qd = rdlane(d[r - 1], 63);
+      uint32_t qi = rdlane(id[r - 1], 63);
+      if (ln == 0) { pd = qd; pi = qi; }
+    }
+    const bool has_prev = (r > 0) || (ln > 0);
+    const bool dup = has_prev && kvalid(id[r]) && kequal(d[r], id[r], pd, pi);
+    dm[r] = ballot(dup);
+    any |= dm[r];
+  }
+  return any;
+}
+
+// Sorts 64 keys (one per lane) ascending and removes repeated keys.
+__device__ __forceinline__ void wave_sort_unique1(float& nd, uint32_t& ni) {
+  float t1[1] = {nd};
+  uint32_t t2[1] = {ni};
+  wave_sort<1>(t1, t2);
+  uint64_t dm[1];
+  if (wave_find_repeats<1>(t1, t2, dm)) {
+    if ((dm[0] >> lane()) & 1) { t1[0] = finf(); t2[0] = kInvalid; }
+    wave_sort<1>(t1, t2);
+  }
+  nd = t1[0];
+  ni = t2[0];
+}
+
+// min(C[i], B[N*64-1-i]) for ascending C and ascending B (64 keys, padded
+// with +inf) is bitonic and holds the N*64 smallest keys of C and B; a
+// bitonic merge then sorts it.
+template <int N>
+__device__ __forceinline__ void wave_merge_sorted64(float (&cd)[N], uint32_t (&ci)[N], float bd, uint32_t bi) {
+  const int ln = lane();
+  float rd = __shfl(bd, 63 - ln, 64);
+  uint32_t ri = __shfl(bi, 63 - ln, 64);
+  if (kless(rd, ri, cd[N - 1], ci[N - 1])) { cd[N - 1] = rd; ci[N - 1] = ri; }
+  wave_merge_up<N>(cd, ci);
+}
+
+// Merges up to 64 new keys (one per lane, any order, invalid = (+inf,
+// kInvalid)) into the ascending, repeat-free list C of N*64 keys, keeping
+// the smallest `keep` distinct keys.  A new key equal to a key already in C
+// is dropped (the entry in C, with its expanded flag, stays).  Repeats are
+// rare, so they are found after merging: every new key equal to a repeated
+// key is removed and the merge is redone from the saved C.  Removing repeats
+// can expose others that the first merge had cut off, so this repeats until
+// a merge has no repeat (each round removes at least one new key).  A merge
+// without repeats holds the N*64 smallest distinct keys.
+template <int N>
+__device__ __forceinline__ void wave_merge_new(float (&cd)[N], uint32_t (&ci)[N], float nd, uint32_t ni,
+                                               int keep) {
+  const int ln = lane();
+  wave_sort_unique1(nd, ni);
+  float sd[N];
+  uint32_t si[N];
+#pragma unroll
+  for (int r = 0; r < N; r++) { sd[r] = cd[r]; si[r] = ci[r]; }
+  for (int round = 0; round <= 64; round++) {
+    wave_merge_sorted64<N>(cd, ci, nd, ni);
+    uint64_t dm[N];
+    if (!wave_find_repeats<N>(cd, ci, dm)) break;
+#pragma unroll
+    for (int r = 0; r < N; r++) {
+      uint64_t m = dm[r];
+      while (m) {
+        const int l = ffs64(m);
+        m &= m - 1;
+        const float kd = rdlane(cd[r], l);
+        const uint32_t ki = rdlane(ci[r], l);
+        if (kequal(nd, ni, kd, ki)) { nd = finf(); ni = kInvalid; }
+      }
+    }
+    float t1[1] = {nd};
+    uint32_t t2[1] = {ni};
+    wave_sort<1>(t1, t2);
+    nd = t1[0];
+    ni = t2[0];
+#pragma unroll
+    for (int r = 0; r < N; r++) { cd[r] = sd[r]; ci[r] = si[r]; }
+  }
+#pragma unroll
+  for (int r = 0; r < N; r++)
+    if (r * 64 + ln >= keep) { cd[r] = finf(); ci[r] = kInvalid; }
+}
+
+// Exclusive wave prefix sum of small non-negative ints.
+__device__ __forceinline__ int wave_excl_scan(int v, int& total) {
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane() >= o) x += y;
+  }
+  total = __shfl(x, 63, 64);
+  return x - v;
+}
+
+}  // namespace gr

@@ -1,0 +1,254 @@
+"""Thin ctypes binding of libgrand.so (the C ABI in include/grand.h).
+
+Argument marshalling only: every step of the update and search path runs in
+the library's HIP kernels.  Arrays may be numpy arrays (host memory) or
+torch tensors (host or device memory); device tensors are passed by their
+data pointer, and the library runs on torch's current HIP stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgrand.so")
+INVALID = 0xFFFFFFFF
+
+OK, E_ARG, E_ID, E_CAPACITY, E_DEVICE, E_OOM, E_STATE = 0, -1, -2, -3, -4, -5, -6
+VAMANA, CAGRA = 0, 1
+F32, U8 = 0, 1
+L2, IP = 0, 1
+ALPHA_ON_DIST, ALPHA_ON_L2 = 0, 1
+CAS_GROUPED, CAS_RACING = 0, 1
+REV_FULL, REV_BATCH = 0, 1
+
+PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group", "rebuild", "search_delete",
+          "reverse", "repair", "clear", "medoid", "search_query", "cagra_detour", "cagra_pickone"]
+
+EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
+            "grand_delete_batch", "grand_search", "grand_export_graph", "grand_import_graph", "grand_set_timing",
+            "grand_get_stats", "grand_reset_stats", "grand_last_error"]
+
+
+class GrandError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"grand status {code}: {msg}")
+        self.code = code
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("algo", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("metric", ctypes.c_int32), ("dim", ctypes.c_uint32), ("capacity", ctypes.c_uint32),
+                ("R", ctypes.c_uint32), ("L_build", ctypes.c_uint32), ("P", ctypes.c_uint32),
+                ("c", ctypes.c_uint32), ("k_repair", ctypes.c_uint32), ("max_iters", ctypes.c_uint32),
+                ("alpha", ctypes.c_float), ("prune_rule", ctypes.c_int32), ("cas_mode", ctypes.c_int32),
+                ("rev_mode", ctypes.c_int32), ("max_batch", ctypes.c_uint32), ("device", ctypes.c_int32),
+                ("stream", ctypes.c_void_p)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("timing_enabled", ctypes.c_uint32),
+                ("inserted", ctypes.c_uint64), ("deleted", ctypes.c_uint64), ("queried", ctypes.c_uint64),
+                ("search_hops", ctypes.c_uint64 * 3), ("search_evals", ctypes.c_uint64 * 3),
+                ("prune_evals", ctypes.c_uint64), ("prunes", ctypes.c_uint64), ("dirty", ctypes.c_uint64),
+                ("records", ctypes.c_uint64), ("rev_edges", ctypes.c_uint64),
+                ("phase_ms", ctypes.c_double * len(PHASES)), ("phase_calls", ctypes.c_uint64 * len(PHASES))]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads libgrand.so; raises if it has not been built (there is no
+    fallback implementation)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2608_21163_amd/build.py")
+    lib = ctypes.CDLL(path)
+    P, U32, I32, U64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64
+    lib.grand_default_params.argtypes = [P]
+    lib.grand_create.argtypes = [P, P]
+    lib.grand_destroy.argtypes = [P]
+    lib.grand_set_stream.argtypes = [P, P]
+    lib.grand_insert_batch.argtypes = [P, P, P, U32]
+    lib.grand_delete_batch.argtypes = [P, P, U32]
+    lib.grand_search.argtypes = [P, P, U32, U32, U32, P, P]
+    lib.grand_export_graph.argtypes = [P, P, P, P, P, P, P, P]
+    lib.grand_import_graph.argtypes = [P, P, P, P, P, U32]
+    lib.grand_set_timing.argtypes = [P, I32]
+    lib.grand_get_stats.argtypes = [P, P]
+    lib.grand_reset_stats.argtypes = [P]
+    lib.grand_last_error.argtypes = [P]
+    lib.grand_last_error.restype = ctypes.c_char_p
+    for name in EXPORTED:
+        if name not in ("grand_default_params", "grand_last_error"):
+            getattr(lib, name).restype = I32
+    _lib = lib
+    return lib
+
+
+def _is_torch(x) -> bool:
+    return type(x).__module__.startswith("torch")
+
+
+def _ptr(x):
+    """Data pointer of a numpy array or torch tensor (must be contiguous)."""
+    if x is None:
+        return None
+    if _is_torch(x):
+        assert x.is_contiguous()
+        return x.data_ptr()
+    assert x.flags["C_CONTIGUOUS"]
+    return x.ctypes.data
+
+
+def _np(x, dtype):
+    return np.ascontiguousarray(x, dtype=dtype)
+
+
+def params_from_config(cfg, device: int = 0, max_batch: int = 10000, rev_mode: int = REV_FULL) -> Params:
+    """grand_params from a workloads.IndexConfig."""
+    p = Params()
+    load_library().grand_default_params(ctypes.byref(p))
+    p.algo = CAGRA if cfg.algo == "cagra" else VAMANA
+    p.dtype = U8 if cfg.dtype == "u8" else F32
+    p.metric = IP if cfg.metric == "ip" else L2
+    p.dim, p.capacity, p.R, p.L_build = cfg.dim, cfg.capacity, cfg.R, cfg.L_build
+    p.P, p.c, p.k_repair, p.max_iters = cfg.P, cfg.c, cfg.k_repair, cfg.max_iters
+    p.alpha = cfg.alpha
+    p.prune_rule = ALPHA_ON_L2 if cfg.prune_rule == "alpha_on_l2" else ALPHA_ON_DIST
+    p.cas_mode = CAS_RACING if cfg.cas_mode == "racing" else CAS_GROUPED
+    p.rev_mode = rev_mode
+    p.max_batch = max_batch
+    p.device = device
+    return p
+
+
+class GrandIndex:
+    """One index on one GPU (grand_create ... grand_destroy)."""
+
+    def __init__(self, params: Params, stream: Optional[int] = None):
+        self.lib = load_library()
+        self.params = params
+        if stream is not None:
+            params.stream = stream
+        h = ctypes.c_void_p()
+        rc = self.lib.grand_create(ctypes.byref(params), ctypes.byref(h))
+        if rc != OK:
+            raise GrandError(rc, "grand_create failed")
+        self.h = h
+        self.np_dtype = np.uint8 if params.dtype == U8 else np.float32
+
+    @classmethod
+    def from_config(cls, cfg, **kw):
+        stream = kw.pop("stream", None)
+        return cls(params_from_config(cfg, **kw), stream=stream)
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.grand_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc: int) -> int:
+        if rc != OK:
+            raise GrandError(rc, self.last_error())
+        return rc
+
+    def last_error(self) -> str:
+        return self.lib.grand_last_error(self.h).decode()
+
+    def set_stream(self, stream: int):
+        self._check(self.lib.grand_set_stream(self.h, ctypes.c_void_p(stream)))
+
+    def insert(self, ids, vecs, check: bool = True) -> int:
+        if not _is_torch(ids):
+            ids = _np(ids, np.uint32)
+        if not _is_torch(vecs):
+            vecs = _np(vecs, self.np_dtype)
+        n = int(ids.shape[0])
+        rc = self.lib.grand_insert_batch(self.h, _ptr(vecs), _ptr(ids), n)
+        return self._check(rc) if check else rc
+
+    def delete(self, ids, check: bool = True) -> int:
+        if not _is_torch(ids):
+            ids = _np(ids, np.uint32)
+        rc = self.lib.grand_delete_batch(self.h, _ptr(ids), int(ids.shape[0]))
+        return self._check(rc) if check else rc
+
+    def search(self, queries, k: int, beam: int, out_ids=None, out_dists=None):
+        """Returns (ids, dists); with out_* given (e.g. device tensors) the
+        results are written there."""
+        if not _is_torch(queries):
+            queries = _np(queries, self.np_dtype)
+        nq = int(queries.shape[0])
+        if out_ids is None:
+            out_ids = np.zeros((nq, k), np.uint32)
+            out_dists = np.zeros((nq, k), np.float32)
+        self._check(self.lib.grand_search(self.h, _ptr(queries), nq, k, beam, _ptr(out_ids), _ptr(out_dists)))
+        return out_ids, out_dists
+
+    def search_rc(self, queries, k: int, beam: int) -> int:
+        q = _np(queries, self.np_dtype)
+        ids = np.zeros((max(q.shape[0], 1), max(k, 1)), np.uint32)
+        d = np.zeros_like(ids, dtype=np.float32)
+        return self.lib.grand_search(self.h, _ptr(q), q.shape[0], k, beam, _ptr(ids), _ptr(d))
+
+    def export(self, with_reverse: bool = False) -> dict:
+        p = self.params
+        cap, R = p.capacity, p.R
+        adj = np.zeros((cap, R), np.uint32)
+        deg = np.zeros(cap, np.uint32)
+        act = np.zeros(cap, np.uint8)
+        med = np.zeros(1, np.uint32)
+        out = dict(adj=adj, deg=deg, active=act)
+        if with_reverse:
+            offs = np.zeros(cap + 1, np.uint32)
+            nnz = np.zeros(1, np.uint64)
+            self._check(self.lib.grand_export_graph(self.h, _ptr(adj), _ptr(deg), _ptr(act), _ptr(med), _ptr(offs),
+                                                    None, _ptr(nnz)))
+            srcs = np.zeros(max(int(nnz[0]), 1), np.uint32)
+            self._check(self.lib.grand_export_graph(self.h, None, None, None, None, _ptr(offs), _ptr(srcs),
+                                                    _ptr(nnz)))
+            out["rev_offsets"] = offs
+            out["rev_srcs"] = srcs[: int(nnz[0])]
+        else:
+            self._check(self.lib.grand_export_graph(self.h, _ptr(adj), _ptr(deg), _ptr(act), _ptr(med), None, None,
+                                                    None))
+        out["medoid"] = int(med[0])
+        return out
+
+    def import_graph(self, vecs, adj, deg, active, medoid: int):
+        vecs = _np(vecs, self.np_dtype)
+        self._check(self.lib.grand_import_graph(self.h, _ptr(vecs), _ptr(_np(adj, np.uint32)),
+                                                _ptr(_np(deg, np.uint32)), _ptr(_np(active, np.uint8)),
+                                                int(medoid)))
+
+    def set_timing(self, on: bool = True):
+        self._check(self.lib.grand_set_timing(self.h, 1 if on else 0))
+
+    def reset_stats(self):
+        self._check(self.lib.grand_reset_stats(self.h))
+
+    def stats(self) -> dict:
+        s = Stats()
+        s.struct_size = ctypes.sizeof(Stats)
+        self._check(self.lib.grand_get_stats(self.h, ctypes.byref(s)))
+        out = {n: getattr(s, n) for n, _ in Stats._fields_ if n not in
+               ("search_hops", "search_evals", "phase_ms", "phase_calls")}
+        for i, w in enumerate(("insert", "delete", "query")):
+            out[f"hops_{w}"] = s.search_hops[i]
+            out[f"evals_{w}"] = s.search_evals[i]
+        out["phase_ms"] = {n: s.phase_ms[i] for i, n in enumerate(PHASES)}
+        out["phase_calls"] = {n: s.phase_calls[i] for i, n in enumerate(PHASES)}
+        return out

@@ -1,0 +1,257 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle on the
+same seeded inputs.  Lockstep tests import the oracle's state into the GPU,
+apply one batch on both and compare the resulting states; free-running
+tests run whole workloads on both independently."""
+import numpy as np
+import pytest
+
+from helpers import INVALID, brute_knn, check_graph_invariants
+from oracle.oracle import Oracle, reverse_csr
+from parity import compare_search, compare_states, recall, say, to_gpu
+from workloads import make_workload
+
+pytestmark = pytest.mark.gpu
+
+# (workload, index overrides, stream overrides, allowed fraction of differing lists)
+CASES = {
+    "tiny_f32_d32": ("tiny", dict(capacity=12_000), {}, 0.001),
+    "u8_d128": ("sift1m_u8", dict(capacity=12_000),
+                dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    "f32_d96": ("deep1m_window", dict(capacity=9_000),
+                dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.001),
+    "cagra_ip_d100": ("glove1m_cagra", dict(capacity=9_000),
+                      dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=2_000, n_query=200), 0.001),
+    "f32_d960": ("gist500k", dict(capacity=3_500),
+                 dict(base_n=2_500, build_batch=1_250, n_insert=500, n_delete=500, n_query=100), 0.001),
+}
+
+_BASE = {}
+
+
+def _workload(case):
+    name, idx, st, _ = CASES[case]
+    return make_workload(name, seed=7, index=idx or None, stream=st or None).keep_vectors()
+
+
+def base_state(case):
+    """(workload positioned after its base batches, oracle with the base
+    graph).  The oracle's base graph is built once per case and re-imported."""
+    w = _workload(case)
+    ops = list(w.base_batches())
+    if case not in _BASE:
+        o = Oracle(w.cfg)
+        for op in ops:
+            assert o.insert(op.ids, op.vecs) == 0
+        _BASE[case] = o.export()
+    st = _BASE[case]
+    o = Oracle(w.cfg)
+    o.import_graph(w.vectors, st["adj"], st["deg"], st["active"], st["medoid"])
+    return w, o
+
+
+def gpu_index(cfg, **kw):
+    from paper_2608_21163_amd import GrandIndex
+    return GrandIndex.from_config(cfg, max_batch=2_000, **kw)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_bootstrap_batch_matches_oracle(case):
+    say(f"[bootstrap] {case}")
+    w = _workload(case)
+    op = next(w.base_batches())
+    o = Oracle(w.cfg)
+    g = gpu_index(w.cfg)
+    assert o.insert(op.ids, op.vecs) == 0
+    g.insert(op.ids, op.vecs)
+    gst, ost = g.export(), o.export()
+    check_graph_invariants(gst, w.cfg.R)
+    compare_states(gst, ost, w.cfg.algo, CASES[case][3])
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_search_matches_oracle(case):
+    say(f"[search] {case}")
+    w, o = base_state(case)
+    g = gpu_index(w.cfg)
+    to_gpu(o, g, w)
+    q = next(op for _, ops in w.rounds(1) for op in ops if op.kind == "search").vecs
+    k, beam = w.spec.k, w.spec.beam
+    gi, gd = g.search(q, k, beam)
+    oi, od = o.search(q, k, beam)
+    compare_search(gi, gd, oi, od, allow_frac=0.01 if w.cfg.dtype == "f32" else 0.0)
+    # the k = beam edge and a small beam
+    gi, gd = g.search(q[:20], 16, 16)
+    oi, od = o.search(q[:20], 16, 16)
+    compare_search(gi, gd, oi, od, allow_frac=0.05 if w.cfg.dtype == "f32" else 0.0)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_reverse_graph_is_bit_exact(case):
+    say(f"[reverse csr] {case}")
+    w, o = base_state(case)
+    g = gpu_index(w.cfg)
+    ost = to_gpu(o, g, w)
+    gst = g.export(with_reverse=True)
+    offs, srcs = reverse_csr(ost["adj"], ost["active"])
+    assert np.array_equal(gst["rev_offsets"], offs)
+    assert np.array_equal(gst["rev_srcs"], srcs)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_insert_lockstep(case):
+    say(f"[insert lockstep] {case}")
+    w, o = base_state(case)
+    g = gpu_index(w.cfg)
+    for r, ops in w.rounds(2):
+        for op in ops:
+            if op.kind != "insert":
+                if op.kind == "delete":
+                    assert o.delete(op.ids) == 0
+                continue
+            to_gpu(o, g, w)
+            assert o.insert(op.ids, op.vecs) == 0
+            g.insert(op.ids, op.vecs)
+            gst, ost = g.export(), o.export()
+            check_graph_invariants(gst, w.cfg.R)
+            n = compare_states(gst, ost, w.cfg.algo, CASES[case][3])
+            say(f"  round {r}: {n} differing lists")
+
+
+@pytest.mark.parametrize("rev_mode", [0, 1])
+@pytest.mark.parametrize("case", list(CASES))
+def test_delete_lockstep(case, rev_mode):
+    say(f"[delete lockstep] {case} rev_mode={rev_mode}")
+    w, o = base_state(case)
+    g = gpu_index(w.cfg, rev_mode=rev_mode)
+    for r, ops in w.rounds(2):
+        for op in ops:
+            if op.kind == "insert":
+                assert o.insert(op.ids, op.vecs) == 0
+            elif op.kind == "delete":
+                to_gpu(o, g, w)
+                assert o.delete(op.ids) == 0
+                g.delete(op.ids)
+                gst, ost = g.export(), o.export()
+                check_graph_invariants(gst, w.cfg.R)
+                n = compare_states(gst, ost, w.cfg.algo, CASES[case][3])
+                say(f"  round {r}: {n} differing lists")
+
+
+def test_delete_medoid_installs_the_same_medoid():
+    say("[medoid delete] u8_d128")
+    w, o = base_state("u8_d128")
+    g = gpu_index(w.cfg)
+    st = to_gpu(o, g, w)
+    med = np.array([st["medoid"]], np.uint32)
+    assert o.delete(med) == 0
+    g.delete(med)
+    gst, ost = g.export(), o.export()
+    assert gst["medoid"] == ost["medoid"] != st["medoid"]
+    compare_states(gst, ost, "vamana", 0.0)
+
+
+def test_free_running_tiny_workload():
+    """The whole tiny workload on both sides independently: 10 bootstrap and
+    insert batches, one round of inserts and deletes, 100 queries."""
+    say("[free running] tiny")
+    w = make_workload("tiny").keep_vectors()
+    o = Oracle(w.cfg)
+    g = gpu_index(w.cfg)
+    for op in w.base_batches():
+        assert o.insert(op.ids, op.vecs) == 0
+        g.insert(op.ids, op.vecs)
+    for r, ops in w.rounds():
+        for op in ops:
+            if op.kind == "insert":
+                assert o.insert(op.ids, op.vecs) == 0
+                g.insert(op.ids, op.vecs)
+            elif op.kind == "delete":
+                assert o.delete(op.ids) == 0
+                g.delete(op.ids)
+            else:
+                gi, gd = g.search(op.vecs, 10, 64)
+                oi, od = o.search(op.vecs, 10, 64)
+                gt = brute_knn(w.vectors, w.active, op.vecs, 10)
+                rg, ro = recall(gi, gt), recall(oi, gt)
+                say(f"  recall@10 gpu {rg:.4f} oracle {ro:.4f}")
+                assert abs(rg - ro) <= 0.005
+                assert rg >= 0.9
+    gst, ost = g.export(), o.export()
+    check_graph_invariants(gst, w.cfg.R)
+    assert np.array_equal(gst["active"], ost["active"])
+    from helpers import canonical_rows
+    same = np.all(canonical_rows(gst["adj"]) == canonical_rows(ost["adj"]), axis=1)
+    frac = 1.0 - same[ost["active"] > 0].mean()
+    say(f"  differing lists after the whole workload: {frac:.5f}")
+    assert frac <= 0.01
+
+
+def test_validation_errors_leave_the_gpu_state_untouched():
+    say("[validation]")
+    from paper_2608_21163_amd import grand
+    w, o = base_state("tiny_f32_d32")
+    g = gpu_index(w.cfg)
+    to_gpu(o, g, w)
+    st0 = g.export()
+    act = np.flatnonzero(st0["active"]).astype(np.uint32)
+    free = np.flatnonzero(st0["active"] == 0).astype(np.uint32)
+    x = np.zeros((2, w.cfg.dim), np.float32)
+    assert g.insert(np.array([free[0], free[0]], np.uint32), x, check=False) == grand.E_ID
+    assert g.insert(act[:1], x[:1], check=False) == grand.E_ID
+    assert g.insert(np.array([w.cfg.capacity], np.uint32), x[:1], check=False) == grand.E_ID
+    bad = x[:1].copy()
+    bad[0, 3] = np.inf
+    assert g.insert(free[:1], bad, check=False) == grand.E_ARG
+    assert g.delete(free[:1], check=False) == grand.E_ID
+    assert g.delete(np.array([act[0], act[0]], np.uint32), check=False) == grand.E_ID
+    assert g.search_rc(x[:1], 5, 4) == grand.E_ARG
+    assert g.insert(np.zeros(0, np.uint32), x[:0], check=False) == 0
+    st1 = g.export()
+    for k in ("adj", "deg", "active"):
+        assert np.array_equal(st0[k], st1[k])
+    assert st0["medoid"] == st1["medoid"]
+
+
+def test_empty_index_search_and_delete_everything():
+    say("[empty index]")
+    w = make_workload("tiny", index=dict(capacity=300), stream=dict(base_n=200, build_batch=200)).keep_vectors()
+    g = gpu_index(w.cfg)
+    q = np.zeros((3, w.cfg.dim), np.float32)
+    ids, d = g.search(q, 5, 8)
+    assert (ids == INVALID).all() and np.isinf(d).all()
+    op = next(w.base_batches())
+    g.insert(op.ids, op.vecs)
+    g.delete(op.ids[::-1].copy())
+    st = g.export()
+    check_graph_invariants(st, w.cfg.R)
+    assert not st["active"].any() and st["medoid"] == INVALID
+    ids, d = g.search(q, 5, 8)
+    assert (ids == INVALID).all()
+
+
+def test_cagra_racing_mode_keeps_invariants():
+    """The racing (paper-literal, last writer wins) compare-and-swap mode is
+    order dependent; it is checked by invariants only: valid lists, and every
+    replaced entry was reachable through the new node (detour)."""
+    say("[cagra racing]")
+    w, o = base_state("cagra_ip_d100")
+    cfg = w.cfg.replace(cas_mode="racing")
+    g = gpu_index(cfg)
+    to_gpu(o, g, w)
+    for op in next(w.rounds(1))[1]:
+        if op.kind == "delete":
+            g.delete(op.ids)           # this stream deletes first, then inserts
+        elif op.kind == "insert":
+            break
+    st0 = g.export()
+    g.insert(op.ids, op.vecs)
+    st1 = g.export()
+    check_graph_invariants(st1, cfg.R)
+    new = set(op.ids.tolist())
+    changed = (st0["adj"] != st1["adj"]) & (st0["adj"] != INVALID)
+    assert changed.any()
+    for u, s in zip(*np.nonzero(changed)):
+        if u in new:
+            continue
+        p, r_old = int(st1["adj"][u, s]), int(st0["adj"][u, s])
+        assert p in new and r_old in set(st1["adj"][p].tolist())
