@@ -1,0 +1,344 @@
+#!/usr/bin/env python3
+"""Throughput of batched dynamic updates and search of a GrAND-Vamana index
+on one MI355X.
+
+Workload (default): 1,000,000 x 128 uint8 vectors from a 256-component
+Gaussian mixture (centres U[0,255], sigma 20, rounded and clipped), L2,
+Vamana R=64, L=128, alpha=1.2.  The base index is built by 100 batched
+inserts of 10,000 (untimed).  A step is one round of the streaming
+workload: +10,000 inserts (smallest free ids), -10,000 uniformly random
+deletes, 10,000 queries (k=10, beam 64).  Inputs of every round are staged
+in device memory before timing.  One JSON line is printed:
+  value       = updates/s (inserts + deletes over the time of the insert
+                and delete calls), with search QPS and recall@10 alongside;
+  roofline    = achieved algorithmic bandwidth of the dominant kernel,
+                from HIP events on the library's stream (per-phase timing);
+  cpu_baseline= the CPU oracle timed on a bounded sample of the workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "updates/sec and search QPS at recall@10≥0.95, 1M×128, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="sift1m_u8")
+    ap.add_argument("--base", type=int, default=0, help="override the base size (quick runs)")
+    ap.add_argument("--rev-mode", choices=["full", "batch"], default="full")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=100_000, help="base size of the oracle's sample index")
+    ap.add_argument("--no-recall", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
+    return ap.parse_args()
+
+
+def copy_probe():
+    """A plain copy of known size: 1 GiB read + 1 GiB written per launch."""
+    import torch
+    n = 1 << 30
+    x = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 5}), flush=True)
+
+
+# ------------------------------------------------------------------ ground truth
+class Mirror:
+    """Device copy of the pool and active map that follows the operation
+    stream, for exact ground truth (measurement only; not the index)."""
+
+    def __init__(self, torch, cfg, dev):
+        self.t = torch
+        dt = torch.uint8 if cfg.dtype == "u8" else torch.float32
+        self.pool = torch.zeros((cfg.capacity, cfg.dim), dtype=dt, device=dev)
+        self.active = torch.zeros(cfg.capacity, dtype=torch.bool, device=dev)
+        self.metric = cfg.metric
+        self.u8 = cfg.dtype == "u8"
+
+    def insert(self, ids, vecs):
+        self.pool[ids.long()] = vecs
+        self.active[ids.long()] = True
+
+    def delete(self, ids):
+        self.active[ids.long()] = False
+
+    def knn(self, q, k, chunk=1024):
+        t = self.t
+        act = t.nonzero(self.active).squeeze(1)
+        # uint8 L2 in fp32 is exact (integer partial sums < 2^24); fp32
+        # data in fp64
+        ct = t.float32 if self.u8 else t.float64
+        X = self.pool[act].to(ct)
+        xn = (X * X).sum(1)
+        out = []
+        for s in range(0, q.shape[0], chunk):
+            Q = q[s:s + chunk].to(ct)
+            if self.metric == "l2":
+                d = (Q * Q).sum(1, keepdim=True) + xn[None, :] - 2.0 * (Q @ X.T)
+            else:
+                d = -(Q @ X.T)
+            idx = t.topk(d, k, dim=1, largest=False).indices
+            out.append(act[idx])
+        return t.cat(out).to(t.int64)
+
+
+# ------------------------------------------------------------------ algorithmic bytes
+def algorithmic_bytes(st, phase, cfg, stride):
+    """Bytes each phase must move over the timed region, from the kernels'
+    own work counters (a vector row is `stride` bytes, an adjacency row 4R):
+      search : per query one query row; per expanded node one adjacency row;
+               per distance evaluation one vector row; outputs;
+      rebuild: per dirty node its degree, adjacency row read and written,
+               8 B per scratch record; per pruning rebuild the |C| candidate
+               rows and u's row (pairwise distances reuse those rows);
+      repair : per deleted node its C_i rows and one row per repaired
+               neighbour; 12 B per record written."""
+    R = cfg.R
+    if phase.startswith("search_"):
+        w = phase.split("_")[1]
+        hops, evals = st[f"hops_{w}"], st[f"evals_{w}"]
+        n = {"insert": st["inserted"], "delete": st["deleted"], "query": st["queried"]}[w]
+        outb = {"insert": 8 * hops, "delete": 4 * n * cfg.k_repair, "query": 8 * n * 10}[w]
+        return n * stride + hops * 4 * R + evals * stride + outb
+    if phase == "rebuild":
+        return st["dirty"] * (8 * R + 4) + 8 * st["rebuild_records"] + st["rebuild_rows"] * stride
+    if phase == "repair":
+        return st["repair_rows"] * stride + 12 * st["repair_records"]
+    return None
+
+
+# ------------------------------------------------------------------ cpu baseline
+def cpu_baseline(args, threads):
+    """The oracle (plain C, OpenMP over batch items) on a bounded sample of the
+    same workload: an index of `cpu_sample` points of the same mixture and
+    parameters built untimed, then one round of the same batch sizes timed."""
+    from oracle.oracle import Oracle
+    from workloads import make_workload
+    base = make_workload(args.workload)
+    n_ops = base.spec.n_insert
+    w = make_workload(args.workload, seed=args.seed + 1,
+                      index=dict(capacity=args.cpu_sample + n_ops),
+                      stream=dict(base_n=args.cpu_sample, n_rounds=1))
+    o = Oracle(w.cfg, threads=threads)
+    t0 = time.perf_counter()
+    for op in w.base_batches():
+        o.insert(op.ids, op.vecs)
+    build_s = time.perf_counter() - t0
+    t_upd = t_q = 0.0
+    n_upd = n_q = 0
+    for _, ops in w.rounds(1):
+        for op in ops:
+            t0 = time.perf_counter()
+            if op.kind == "insert":
+                o.insert(op.ids, op.vecs)
+                t_upd += time.perf_counter() - t0
+                n_upd += len(op.ids)
+            elif op.kind == "delete":
+                o.delete(op.ids)
+                t_upd += time.perf_counter() - t0
+                n_upd += len(op.ids)
+            else:
+                o.search(op.vecs, w.spec.k, w.spec.beam)
+                t_q += time.perf_counter() - t0
+                n_q += len(op.vecs)
+    return {"value": n_upd / t_upd, "unit": "updates/s", "cores": threads, "kind": "oracle",
+            "search_qps": n_q / t_q,
+            "sample": (f"oracle on a {args.cpu_sample:,}-point index of the same mixture and parameters "
+                       f"(built untimed in {build_s:.1f} s), one round of {n_ops:,} inserts + "
+                       f"{w.spec.n_delete:,} deletes + {w.spec.n_query:,} queries")}
+
+
+# ------------------------------------------------------------------ main
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs the update path on one GPU only; "
+              "a multi-GPU run (sharding by id, one index per GPU) is not part of it", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
+    import numpy as np
+    import torch
+
+    from paper_2608_21163_amd import GrandIndex
+    from paper_2608_21163_amd.grand import REV_BATCH, REV_FULL
+    from workloads import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.backends.cuda.matmul.allow_tf32 = False
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    W, K = args.warmup, args.steps
+    st_over = dict(n_rounds=W + K)
+    if args.base:
+        st_over["base_n"] = args.base
+    w = make_workload(args.workload, seed=args.seed, stream=st_over)
+    cfg, spec = w.cfg, w.spec
+    stride = ((cfg.dim * (1 if cfg.dtype == "u8" else 4)) + 15) // 16 * 16
+    g = GrandIndex.from_config(cfg, max_batch=max(spec.build_batch, spec.n_insert, spec.n_delete),
+                               stream=stream.cuda_stream,
+                               rev_mode=REV_BATCH if args.rev_mode == "batch" else REV_FULL)
+    mirror = Mirror(torch, cfg, dev)
+
+    def dev_ids(a):
+        return torch.from_numpy(a.astype(np.int32)).to(dev)
+
+    def dev_vecs(a):
+        return torch.from_numpy(a).to(dev)
+
+    # ---- build (untimed)
+    t0 = time.perf_counter()
+    nb = 0
+    for op in w.base_batches():
+        ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
+        g.insert(ids, vecs)
+        mirror.insert(ids, vecs)
+        nb += 1
+        if nb % 20 == 0:
+            log(f"build: {nb * spec.build_batch:,} points, {time.perf_counter() - t0:.1f} s")
+    torch.cuda.synchronize()
+    build_s = time.perf_counter() - t0
+    log(f"build done: {spec.base_n:,} points in {build_s:.1f} s")
+
+    # ---- stage every round's inputs on the device, with exact ground truth
+    rounds = []
+    for r in range(W + K):
+        ops = []
+        for op in w.round_ops(r):
+            if op.kind == "insert":
+                ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
+                mirror.insert(ids, vecs)
+                ops.append(("insert", ids, vecs, None))
+            elif op.kind == "delete":
+                ids = dev_ids(op.ids)
+                mirror.delete(ids)
+                ops.append(("delete", ids, None, None))
+            else:
+                q = dev_vecs(op.vecs)
+                gt = None if args.no_recall else mirror.knn(q, spec.k)
+                out_i = torch.empty((q.shape[0], spec.k), dtype=torch.int32, device=dev)
+                out_d = torch.empty((q.shape[0], spec.k), dtype=torch.float32, device=dev)
+                ops.append(("search", q, (out_i, out_d), gt))
+        rounds.append(ops)
+    torch.cuda.synchronize()
+    log(f"staged {W + K} rounds")
+
+    def run_round(ops, events):
+        for kind, a, b, _ in ops:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if kind == "insert":
+                g.insert(a, b)
+            elif kind == "delete":
+                g.delete(a)
+            else:
+                g.search(a, spec.k, spec.beam, out_ids=b[0], out_dists=b[1])
+            e1.record(stream)
+            events.append((kind, int(a.shape[0]), e0, e1))
+
+    for r in range(W):
+        run_round(rounds[r], [])
+    g.reset_stats()
+    g.set_timing(True)
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for r in range(W, W + K):
+        run_round(rounds[r], events)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = g.stats()
+
+    upd_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in events if k != "search")
+    upd_n = sum(n for k, n, e0, e1 in events if k != "search")
+    q_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in events if k == "search")
+    q_n = sum(n for k, n, e0, e1 in events if k == "search")
+    ins_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in events if k == "insert")
+    del_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in events if k == "delete")
+
+    recalls = []
+    if not args.no_recall:
+        for r in range(W + K):
+            for kind, q, outs, gt in rounds[r]:
+                if kind != "search":
+                    continue
+                got = outs[0].to(torch.int64)
+                hit = (got[:, :, None] == gt[:, None, :]).any(2).sum(1).float()
+                recalls.append(float(hit.mean() / spec.k))
+
+    # ---- roofline of the dominant kernel (largest share of the timed region)
+    phases = {}
+    for ph, ms in st["phase_ms"].items():
+        calls = st["phase_calls"][ph]
+        if calls == 0:
+            continue
+        b = algorithmic_bytes(st, ph, cfg, stride)
+        phases[ph] = {"ms_total": round(ms, 3), "launches": int(calls), "ms_per_launch": round(ms / calls, 4)}
+        if b is not None:
+            phases[ph]["alg_GB_per_launch"] = round(b / calls / 1e9, 5)
+            phases[ph]["achieved_GBps"] = round(b / (ms / 1e3) / 1e9, 1)
+    cand = [p for p in phases if "achieved_GBps" in phases[p]]
+    dom = max(cand, key=lambda p: phases[p]["ms_total"]) if cand else None
+    roofline = None
+    if dom:
+        ach = phases[dom]["achieved_GBps"]
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                    "ms_per_launch": phases[dom]["ms_per_launch"],
+                    "alg_GB_per_launch": phases[dom]["alg_GB_per_launch"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = min(16, os.cpu_count() or 1)
+        log(f"cpu baseline: oracle on {threads} threads ...")
+        cpu = cpu_baseline(args, threads)
+
+    value = upd_n / (upd_ms / 1e3)
+    res = {
+        "metric": METRIC, "value": round(value, 1), "unit": "updates/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(wall * 1e3 / K, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8" if cfg.dtype == "u8" else "f32",
+        "data": "synthetic (seeded mixture; stands in for the paper's SIFT-like 128-d dataset)",
+        "config": {"workload": w.wdef.description, "base_points": spec.base_n, "insert_batch": spec.n_insert,
+                   "delete_batch": spec.n_delete, "queries": spec.n_query, "k": spec.k, "beam": spec.beam,
+                   "R": cfg.R, "L": cfg.L_build, "alpha": cfg.alpha, "P": cfg.P, "c": cfg.c,
+                   "k_repair": cfg.k_repair, "reverse_graph": args.rev_mode, "parallelism": "single GPU"},
+        "search_qps": round(q_n / (q_ms / 1e3), 1),
+        "insert_per_s": round(spec.n_insert * K / (ins_ms / 1e3), 1),
+        "delete_per_s": round(spec.n_delete * K / (del_ms / 1e3), 1),
+        "recall_at_10_min": round(min(recalls), 4) if recalls else None,
+        "recall_at_10_mean": round(float(np.mean(recalls)), 4) if recalls else None,
+        "recall_at_10_per_round": [round(x, 4) for x in recalls],
+        "build_s": round(build_s, 2),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "phases": phases,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -161,11 +161,18 @@ typedef struct {
   uint64_t inserted, deleted, queried;
   uint64_t search_hops[3];         /* [insert, delete, query] searches: nodes expanded */
   uint64_t search_evals[3];        /* distance evaluations (row gathers) of those searches */
-  uint64_t prune_evals;            /* pairwise distance evaluations in prunes */
-  uint64_t prunes;                 /* GrANDRobustPrune invocations */
+  uint64_t fwd_evals;              /* pairwise distance evaluations in forward prunes */
+  uint64_t fwd_prunes;             /* forward GrANDRobustPrune invocations */
+  uint64_t rebuild_evals;          /* distance evaluations in dirty rebuilds (D_u and pairwise) */
+  uint64_t rebuild_prunes;         /* dirty rebuilds that ran GrANDRobustPrune */
   uint64_t dirty;                  /* dirty nodes rebuilt (or CAGRA targets / affected nodes) */
+  uint64_t rebuild_records;        /* scratch records read by dirty rebuilds */
   uint64_t records;                /* reverse-edge / repair records emitted */
-  uint64_t rev_edges;              /* edges scanned by reverse-graph builds */
+  uint64_t rev_edges;              /* edges found by reverse-graph builds */
+  uint64_t repair_evals;           /* distance evaluations in delete repair */
+  uint64_t rebuild_rows;           /* vector rows pruning rebuilds need (|C| + 1 each) */
+  uint64_t repair_rows;            /* vector rows repairs need (neighbours + |C_i|) */
+  uint64_t repair_records;         /* records written by repairs */
   double phase_ms[GRAND_NPHASE];   /* summed kernel time per phase (timing enabled) */
   uint64_t phase_calls[GRAND_NPHASE];
 } grand_stats_t;

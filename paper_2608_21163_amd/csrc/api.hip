@@ -428,7 +428,6 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   r.ds = h->ds;
   size_t total = 0;
   {
-    Phase ph(h, GRAND_PH_REPAIR);
     HCHK(h, launch_repair_count(r, h->rcount, h->stream));
     HCHK(h, launch_scan(h->rcount, h->rofs, n, h->scan_tmp, h->stream));
     HCHK(h, hipMemcpyAsync(&h->hs->n_dirty, h->rofs + n, sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream));
@@ -871,11 +870,18 @@ grand_status grand_get_stats(grand_index *h, grand_stats_t *out) {
     r.search_hops[i] = h->hs->hops[i];
     r.search_evals[i] = h->hs->evals[i];
   }
-  r.prune_evals = h->hs->prune_evals;
-  r.prunes = h->hs->prunes;
+  r.fwd_evals = h->hs->fwd_evals;
+  r.fwd_prunes = h->hs->fwd_prunes;
+  r.rebuild_evals = h->hs->rb_evals;
+  r.rebuild_prunes = h->hs->rb_prunes;
   r.dirty = h->hs->dirty;
+  r.rebuild_records = h->hs->rb_recs;
   r.records = h->hs->records;
   r.rev_edges = h->hs->rev_edges;
+  r.repair_evals = h->hs->rep_evals;
+  r.rebuild_rows = h->hs->rb_cand;
+  r.repair_rows = h->hs->rep_rows;
+  r.repair_records = h->hs->rep_recs;
   *out = r;
   return GRAND_OK;
 }

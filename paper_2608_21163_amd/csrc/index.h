@@ -15,11 +15,18 @@ namespace gr {
 struct DevScalars {
   unsigned long long hops[3];       // nodes expanded by [insert, delete, query] searches
   unsigned long long evals[3];      // row gathers of those searches
-  unsigned long long prune_evals;
-  unsigned long long prunes;
-  unsigned long long dirty;
-  unsigned long long records;
+  unsigned long long fwd_evals;      // pairwise distances in forward prunes
+  unsigned long long fwd_prunes;
+  unsigned long long rb_evals;       // distances in dirty rebuilds (D_u and pairwise)
+  unsigned long long rb_prunes;      // rebuilds that pruned
+  unsigned long long dirty;          // dirty nodes rebuilt / CAGRA targets / affected nodes
+  unsigned long long rb_recs;        // scratch records read by rebuilds
+  unsigned long long records;        // reverse-edge and repair records emitted
   unsigned long long rev_edges;
+  unsigned long long rep_evals;      // distances in delete repair
+  unsigned long long rb_cand;        // vector rows a pruning rebuild needs: |C| + 1
+  unsigned long long rep_rows;       // vector rows a repair needs: neighbours + |C_i|
+  unsigned long long rep_recs;       // records written by repairs
   uint32_t err_code;                // first validation error (0 = none)
   uint32_t err_id;
   uint32_t n_dirty;                 // number of entries in the dirty / affected list

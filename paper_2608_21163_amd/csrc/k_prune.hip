@@ -117,8 +117,8 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
   }
   if (ln == 0) {
     P.deg[p] = (uint32_t)nsel;
-    atomicAdd(&a.ds->prunes, 1ull);
-    atomicAdd(&a.ds->prune_evals, evals);
+    atomicAdd(&a.ds->fwd_prunes, 1ull);
+    atomicAdd(&a.ds->fwd_evals, evals);
     atomicAdd(&a.ds->records, (unsigned long long)nsel);
   }
 }
@@ -139,11 +139,12 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   const PoolView &P = a.pool;
   const uint32_t R = P.R;
   const uint32_t nd_total = a.ds->n_dirty;
-  unsigned long long evals = 0, prunes = 0, nodes = 0;
+  unsigned long long evals = 0, prunes = 0, nodes = 0, recs = 0, cand = 0;
   for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
     const uint32_t u = a.dirty[it];
     nodes++;
     const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
+    recs += g1 - g0;
     float sd[NP];
     uint32_t si[NP];
 #pragma unroll
@@ -212,13 +213,16 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? sid : kInvalid;
       if (ln == 0) P.deg[u] = (uint32_t)nsel;
       prunes++;
+      cand += (unsigned long long)m + 1;
     }
     __syncthreads();
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->prunes, prunes);
-    atomicAdd(&a.ds->prune_evals, evals);
+    atomicAdd(&a.ds->rb_prunes, prunes);
+    atomicAdd(&a.ds->rb_evals, evals);
     atomicAdd(&a.ds->dirty, nodes);
+    atomicAdd(&a.ds->rb_recs, recs);
+    atomicAdd(&a.ds->rb_cand, cand);
   }
 }
 

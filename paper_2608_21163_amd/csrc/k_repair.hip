@@ -46,7 +46,7 @@ hipError_t launch_repair_count(const RepairArgs &a, uint32_t *counts, hipStream_
 // Lane t < c ends with the t-th one (invalid when C_i has fewer points).
 template <int KIND, int LPV, int CPL>
 __device__ __forceinline__ void closest_c(const RepairArgs &a, uint32_t cv, uint32_t x, uint32_t *lst, float *ldist,
-                                          float &od, uint32_t &oi) {
+                                          float &od, uint32_t &oi, unsigned long long &evals) {
   const int ln = lane();
   const PoolView &P = a.pool;
   const bool ok = kvalid(cv) && cv != x;
@@ -58,6 +58,7 @@ __device__ __forceinline__ void closest_c(const RepairArgs &a, uint32_t cv, uint
   __syncthreads();
   wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, lst, ldist, cnt);
   __syncthreads();
+  evals += (unsigned long long)cnt;
   float d[1] = {ln < cnt ? ldist[ln] : finf()};
   uint32_t id[1] = {ln < cnt ? lst[ln] : kInvalid};
   __syncthreads();
@@ -77,6 +78,7 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
   const uint32_t p = a.ids[i];
   const uint32_t cv = ln < (int)a.kr ? a.ci[(size_t)i * a.kr + ln] : kInvalid;
   uint32_t r = a.rofs[i];
+  unsigned long long evals = 0, rows = popc(ballot(kvalid(cv)));
   uint32_t b0, b1;
   rev_row(a, i, p, b0, b1);
   for (uint32_t j = b0; j < b1; j++) {
@@ -84,7 +86,8 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
     if (a.in_batch[z]) continue;
     float od;
     uint32_t oi;
-    closest_c<KIND, LPV, CPL>(a, cv, z, lst, ldist, od, oi);
+    closest_c<KIND, LPV, CPL>(a, cv, z, lst, ldist, od, oi, evals);
+    rows++;
     if (ln < (int)a.c) {
       a.rec_t[r + ln] = z;
       a.rec_s[r + ln] = oi;
@@ -102,7 +105,8 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
     if (w == kInvalid || a.in_batch[w]) continue;
     float od;
     uint32_t oi;
-    closest_c<KIND, LPV, CPL>(a, cv, w, lst, ldist, od, oi);
+    closest_c<KIND, LPV, CPL>(a, cv, w, lst, ldist, od, oi, evals);
+    rows++;
     if (ln < (int)a.c) {
       const bool v = kvalid(oi);
       a.rec_t[r + ln] = v ? oi : kInvalid;
@@ -111,7 +115,12 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
     }
     r += a.c;
   }
-  if (ln == 0) atomicAdd(&a.ds->records, (unsigned long long)(r - a.rofs[i]));
+  if (ln == 0) {
+    atomicAdd(&a.ds->records, (unsigned long long)(r - a.rofs[i]));
+    atomicAdd(&a.ds->rep_evals, evals);
+    atomicAdd(&a.ds->rep_rows, rows);
+    atomicAdd(&a.ds->rep_recs, (unsigned long long)(r - a.rofs[i]));
+  }
 }
 
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, hipStream_t st) {

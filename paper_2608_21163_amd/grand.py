@@ -53,8 +53,11 @@ class Stats(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("timing_enabled", ctypes.c_uint32),
                 ("inserted", ctypes.c_uint64), ("deleted", ctypes.c_uint64), ("queried", ctypes.c_uint64),
                 ("search_hops", ctypes.c_uint64 * 3), ("search_evals", ctypes.c_uint64 * 3),
-                ("prune_evals", ctypes.c_uint64), ("prunes", ctypes.c_uint64), ("dirty", ctypes.c_uint64),
-                ("records", ctypes.c_uint64), ("rev_edges", ctypes.c_uint64),
+                ("fwd_evals", ctypes.c_uint64), ("fwd_prunes", ctypes.c_uint64),
+                ("rebuild_evals", ctypes.c_uint64), ("rebuild_prunes", ctypes.c_uint64), ("dirty", ctypes.c_uint64),
+                ("rebuild_records", ctypes.c_uint64), ("records", ctypes.c_uint64), ("rev_edges", ctypes.c_uint64),
+                ("repair_evals", ctypes.c_uint64), ("rebuild_rows", ctypes.c_uint64),
+                ("repair_rows", ctypes.c_uint64), ("repair_records", ctypes.c_uint64),
                 ("phase_ms", ctypes.c_double * len(PHASES)), ("phase_calls", ctypes.c_uint64 * len(PHASES))]
 
 
