@@ -336,6 +336,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "phases": phases,
+        "counters": {k: v for k, v in st.items() if isinstance(v, int)},
     }
     print(json.dumps(res), flush=True)
 

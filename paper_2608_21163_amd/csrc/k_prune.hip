@@ -1,23 +1,30 @@
 // k_prune.hip -- GrANDRobustPrune (Alg. 4) executed by one wavefront, the
 // forward prune of new nodes (Alg. 5, second loop) and the rebuild of every
 // dirty node (Alg. 5 and Alg. 6, last loops), one wavefront per node.
+//
+// When the candidate rows fit, a node's candidates and its own row are
+// staged into LDS once (all gathers in flight together), and every distance
+// of the prune -- D_p and the pairwise distances of the selection loop -- is
+// evaluated from LDS.  LDS slots are assigned in ascending id order, so
+// ordering keys by (distance, slot) breaks ties exactly as (distance, id).
+// Rows too long for LDS are read from global memory (L2) instead.
 #include "dispatch.h"
 
 namespace gr {
 
-// GrANDRobustPrune of node p.  Candidates (any order, invalid padded) come
-// with their cached distances D_p (Section 3.1: reused, not recomputed).
-// They are sorted by (D_p, id); repeats and p itself are dropped.  The
+// GrANDRobustPrune of node p over candidates addressed as rows of `vecs`.
+// Candidates (any order, invalid padded) come with their distances D_p.
+// They are sorted by (D_p, address); repeats and p itself are dropped.  The
 // first valid candidate p* is selected; selection stops at R; otherwise the
 // distance from p* to every later valid candidate p' is evaluated by the
-// wave (pivot p* held in registers, candidate rows gathered LPV lanes per
-// row) and p' is invalidated when coef * Dist(p*, p') <= D_p[p'] (coef is
-// alpha, or alpha^2 for the Euclidean reading, compared in fp64).
-// On return lane t < nsel holds the t-th selected id and its distance.
+// wave (pivot p* held in registers, candidate rows LPV lanes per row) and p'
+// is invalidated when coef * Dist(p*, p') <= D_p[p'] (coef is alpha, or
+// alpha^2 for the Euclidean reading, compared in fp64).
+// On return lane t < nsel holds the t-th selection (address, distance).
 template <int KIND, int LPV, int CPL, int NR>
-__device__ int wave_prune(const PoolView &P, uint32_t p, uint32_t R, double coef, float (&cd)[NR],
-                          uint32_t (&ci)[NR], uint32_t *lids, float *ldist, uint32_t &sel_id, float &sel_d,
-                          unsigned long long &evals) {
+__device__ int wave_prune(const uint8_t *vecs, size_t stride, int nch, uint32_t p, uint32_t R, double coef,
+                          float (&cd)[NR], uint32_t (&ci)[NR], uint32_t *lids, float *ldist, uint32_t &sel_id,
+                          float &sel_d, unsigned long long &evals) {
   const int ln = lane();
 #pragma unroll
   for (int r = 0; r < NR; r++)
@@ -69,9 +76,9 @@ __device__ int wave_prune(const PoolView &P, uint32_t p, uint32_t R, double coef
     }
     if (cnt == 0) break;
     Slice<KIND, LPV, CPL> s;
-    load_slice<KIND, LPV, CPL>(s, P.vecs + (size_t)pid * P.stride, P.nch);
+    load_slice<KIND, LPV, CPL>(s, vecs + (size_t)pid * stride, nch);
     __syncthreads();
-    wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, lids, ldist, cnt);
+    wave_dists<KIND, LPV, CPL>(s, vecs, stride, nch, lids, ldist, cnt);
     __syncthreads();
     evals += (unsigned long long)cnt;
 #pragma unroll
@@ -82,11 +89,274 @@ __device__ int wave_prune(const PoolView &P, uint32_t p, uint32_t R, double coef
   return nsel;
 }
 
+// Bytes per LDS row: the pool stride plus one chunk, which staggers rows
+// across LDS banks.
+__host__ __device__ constexpr size_t lds_stride(size_t stride) { return stride + 16; }
+
+// Copies rows ids[0..m) and row `extra` (slot m) of the pool into LDS slots
+// 0..m, LPV lanes per row, with the gathers of RIF row groups in flight.
+template <int LPV, int CPL>
+__device__ __forceinline__ void stage_rows(const PoolView &P, const uint32_t *ids, int m, uint32_t extra,
+                                           uint8_t *vbuf) {
+  constexpr int G = 64 / LPV;
+  constexpr int RIF = CPL >= 8 ? 1 : 8 / CPL;
+  const int ln = lane(), grp = ln / LPV, sub = ln % LPV;
+  const size_t ls = lds_stride(P.stride);
+  for (int base = 0; base <= m; base += G * RIF) {
+    uint4 b[RIF][CPL];
+#pragma unroll
+    for (int rr = 0; rr < RIF; rr++) {
+      const int e = base + rr * G + grp;
+      const uint32_t id = e < m ? ids[e] : extra;
+      const uint8_t *row = P.vecs + (size_t)id * P.stride;
+#pragma unroll
+      for (int k = 0; k < CPL; k++) {
+        const int ch = sub + k * LPV;
+        b[rr][k] = (e <= m && ch < P.nch) ? ld16(row + (size_t)ch * 16) : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RIF; rr++) {
+      const int e = base + rr * G + grp;
+#pragma unroll
+      for (int k = 0; k < CPL; k++) {
+        const int ch = sub + k * LPV;
+        if (e <= m && ch < P.nch) *reinterpret_cast<uint4 *>(vbuf + (size_t)e * ls + (size_t)ch * 16) = b[rr][k];
+      }
+    }
+  }
+}
+
+// GrANDRobustPrune of node p over the m distinct candidate ids in slot_id
+// (LDS, any order), with every vector in LDS: the ids are sorted (slot =
+// rank of the id), the rows of the candidates and of p are staged, D_p is
+// evaluated from LDS (bit-identical to the distance evaluated during the
+// search or carried by the records: the arithmetic and lane layout are the
+// same), and the selection loop runs on LDS rows.  Lane t < nsel returns the
+// t-th selected id and its distance.
+template <int KIND, int LPV, int CPL, int NC>
+__device__ int prune_staged(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, uint32_t *slot_id,
+                            uint8_t *vbuf, uint32_t *lids, float *ldist, uint32_t &sel_id, float &sel_d,
+                            unsigned long long &evals) {
+  const int ln = lane();
+  const size_t ls = lds_stride(P.stride);
+  float kd[NC];
+  uint32_t kid[NC];
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    kd[r] = e < m ? 0.0f : finf();
+    kid[r] = e < m ? slot_id[e] : kInvalid;
+  }
+  wave_sort<NC>(kd, kid);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    if (e < m) {
+      slot_id[e] = kid[r];
+      lids[e] = (uint32_t)e;
+    }
+  }
+  __syncthreads();
+  stage_rows<LPV, CPL>(P, slot_id, m, p, vbuf);
+  __syncthreads();
+  Slice<KIND, LPV, CPL> su;
+  load_slice<KIND, LPV, CPL>(su, vbuf + (size_t)m * ls, P.nch);
+  wave_dists<KIND, LPV, CPL>(su, vbuf, ls, P.nch, lids, ldist, m);
+  __syncthreads();
+  evals += (unsigned long long)m;
+  float cd[NC];
+  uint32_t ci[NC];
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    cd[r] = e < m ? ldist[e] : finf();
+    ci[r] = e < m ? (uint32_t)e : kInvalid;
+  }
+  __syncthreads();
+  uint32_t ssl;
+  const int nsel = wave_prune<KIND, LPV, CPL, NC>(vbuf, ls, P.nch, kIdMask - 1, R, coef, cd, ci, lids, ldist, ssl,
+                                                  sel_d, evals);
+  sel_id = ln < nsel ? slot_id[ssl] : kInvalid;
+  __syncthreads();
+  return nsel;
+}
+
+// ---------------------------------------------------------------------------
+// uint8 GrANDRobustPrune on the matrix cores.  Rows are staged in LDS as in
+// prune_staged.  The pairwise distances of the candidates form a dense Gram
+// matrix (m x m x dim): with y = x - 128 (byte-wise x ^ 0x80, an exact int8
+// view), Dist(i, j) = |y_i|^2 + |y_j|^2 - 2 y_i.y_j exactly in int32 (L2 is
+// translation invariant), so the products run on v_mfma_i32_16x16x64_i8.
+// Candidates are ordered by (D_p, slot); the greedy selection walks them in
+// blocks of 16 pivots: a block's distance rows to every later candidate are
+// produced by MFMA into LDS (blocks without a valid pivot are skipped), then
+// the block's pivots are taken in order, each invalidating later candidates
+// with coef * Dist(p*, p') <= D_p[p'].  Requires dim to be a multiple of 64.
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+struct MfmaLds {
+  uint32_t *slot_id;   // [64*NC] candidate ids, then sorted by id (slot order)
+  int32_t *nrm;        // [64*NC + 1] |y|^2 per slot (slot m = the node)
+  float *dpos;         // [64*NC] D_p by sorted position
+  uint32_t *spos;      // [64*NC] slot by sorted position
+  float *blk;          // [16][64*NC] distance rows of the current pivot block
+  uint8_t *vbuf;       // [(64*NC + 1) * lds_stride] rows
+};
+
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+}
+
+template <int NC>
+__device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const MfmaLds &L,
+                             uint32_t &sel_id, float &sel_d, unsigned long long &evals) {
+  constexpr int MP = 64 * NC;
+  const int ln = lane();
+  const size_t ls = lds_stride(P.stride);
+  const int nk = P.nch / 4;  // 64-byte K chunks
+  sel_id = kInvalid;
+  sel_d = finf();
+  if (m <= 0) return 0;
+  // slots in ascending id order
+  {
+    float kd[NC];
+    uint32_t kid[NC];
+#pragma unroll
+    for (int r = 0; r < NC; r++) {
+      const int e = r * 64 + ln;
+      kd[r] = e < m ? 0.0f : finf();
+      kid[r] = e < m ? L.slot_id[e] : kInvalid;
+    }
+    wave_sort<NC>(kd, kid);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < NC; r++)
+      if (r * 64 + ln < m) L.slot_id[r * 64 + ln] = kid[r];
+    __syncthreads();
+  }
+  stage_rows<8, 1>(P, L.slot_id, m, p, L.vbuf);
+  __syncthreads();
+  // |y|^2 per slot and D_p = |y_p|^2 + |y_j|^2 - 2 y_p.y_j (exact)
+  const uint8_t *prow = L.vbuf + (size_t)m * ls;
+  int np = 0;
+  for (int c = 0; c < P.nch; c++) {
+    const uint4 v = ld16(prow + (size_t)c * 16);
+    const uint32_t a0 = v.x ^ 0x80808080u, a1 = v.y ^ 0x80808080u, a2 = v.z ^ 0x80808080u, a3 = v.w ^ 0x80808080u;
+    np = sdot4(a0, a0, np); np = sdot4(a1, a1, np); np = sdot4(a2, a2, np); np = sdot4(a3, a3, np);
+  }
+  float kd[NC];
+  uint32_t kid[NC];
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    kd[r] = finf();
+    kid[r] = kInvalid;
+    if (e < m) {
+      const uint8_t *row = L.vbuf + (size_t)e * ls;
+      int nn = 0, dp = 0;
+      for (int c = 0; c < P.nch; c++) {
+        const uint4 v = ld16(row + (size_t)c * 16), w = ld16(prow + (size_t)c * 16);
+        const uint32_t a0 = v.x ^ 0x80808080u, a1 = v.y ^ 0x80808080u, a2 = v.z ^ 0x80808080u, a3 = v.w ^ 0x80808080u;
+        nn = sdot4(a0, a0, nn); nn = sdot4(a1, a1, nn); nn = sdot4(a2, a2, nn); nn = sdot4(a3, a3, nn);
+        dp = sdot4(a0, w.x ^ 0x80808080u, dp); dp = sdot4(a1, w.y ^ 0x80808080u, dp);
+        dp = sdot4(a2, w.z ^ 0x80808080u, dp); dp = sdot4(a3, w.w ^ 0x80808080u, dp);
+      }
+      L.nrm[e] = nn;
+      kd[r] = canon0((float)(np + nn - 2 * dp));
+      kid[r] = (uint32_t)e;
+    }
+  }
+  evals += (unsigned long long)m;
+  wave_sort<NC>(kd, kid);
+  bool valid[NC];
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    valid[r] = e < m;
+    L.spos[e] = kid[r];
+    L.dpos[e] = kd[r];
+  }
+  __syncthreads();
+  const int nt = (m + 15) / 16;
+  int nsel = 0;
+  bool done = false;
+  for (int b = 0; b < nt && !done; b++) {
+    // valid pivots of block b: sorted positions 16b .. 16b+15 live in
+    // register row b/4, lanes 16*(b%4) ..
+    uint64_t vb = 0;
+#pragma unroll
+    for (int r = 0; r < NC; r++) {
+      const uint64_t vm = ballot(valid[r]);
+      if (r == b / 4) vb = (vm >> (16 * (b % 4))) & 0xFFFFull;
+    }
+    if (!vb) continue;
+    // distance rows of the block's candidates to every candidate of tile c >= b
+    const int arow = 16 * b + (ln & 15);
+    const uint32_t aslot = L.spos[arow < m ? arow : 0];
+    const int kb = ln >> 4;
+    for (int c = b; c < nt; c++) {
+      const int bcol = 16 * c + (ln & 15);
+      const uint32_t bslot = L.spos[bcol < m ? bcol : 0];
+      v4i acc = {0, 0, 0, 0};
+      for (int kk = 0; kk < nk; kk++) {
+        const uint4 av = ld16(L.vbuf + (size_t)aslot * ls + (size_t)kk * 64 + (size_t)kb * 16);
+        const uint4 bv = ld16(L.vbuf + (size_t)bslot * ls + (size_t)kk * 64 + (size_t)kb * 16);
+        v4i A, B;
+        A[0] = (int)(av.x ^ 0x80808080u); A[1] = (int)(av.y ^ 0x80808080u);
+        A[2] = (int)(av.z ^ 0x80808080u); A[3] = (int)(av.w ^ 0x80808080u);
+        B[0] = (int)(bv.x ^ 0x80808080u); B[1] = (int)(bv.y ^ 0x80808080u);
+        B[2] = (int)(bv.z ^ 0x80808080u); B[3] = (int)(bv.w ^ 0x80808080u);
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, B, acc, 0, 0, 0);
+      }
+      const int ncol = L.nrm[bslot];
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int rr = 4 * (ln >> 4) + i;
+        const int rpos = 16 * b + rr;
+        const int rn = L.nrm[L.spos[rpos < m ? rpos : 0]];
+        L.blk[rr * MP + bcol] = canon0((float)(rn + ncol - 2 * acc[i]));
+      }
+    }
+    evals += (unsigned long long)256 * (nt - b);
+    __syncthreads();
+    for (int t = 0; t < 16; t++) {
+      const int pos = 16 * b + t;
+      if (pos >= m) break;
+      if (!((vb >> t) & 1)) continue;
+      // recheck: earlier pivots of this block may have invalidated it
+      uint64_t still = 0;
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        const uint64_t vm = ballot(valid[r]);
+        if (r == b / 4) still = (vm >> (16 * (b % 4) + t)) & 1ull;
+      }
+      if (!still) continue;
+      if (ln == nsel) { sel_id = L.slot_id[L.spos[pos]]; sel_d = L.dpos[pos]; }
+      nsel++;
+#pragma unroll
+      for (int r = 0; r < NC; r++)
+        if (r * 64 + ln == pos) valid[r] = false;
+      if (nsel == (int)R) { done = true; break; }
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        const int j = r * 64 + ln;
+        if (valid[r] && j > pos && coef * (double)L.blk[t * MP + j] <= (double)L.dpos[j]) valid[r] = false;
+      }
+    }
+    __syncthreads();
+  }
+  return nsel;
+}
+
 // Forward lists of new nodes: GrANDRobustPrune(p_i, V_i \ {p_i}, D_{p_i}),
 // written to p_i's row (each new node owns its row), and the reverse-edge
 // records (u, p_i, D_{p_i}[u]) for every selected u.
-template <int KIND, int LPV, int CPL, int NR>
+template <int KIND, int LPV, int CPL, int NR, bool STAGED>
 __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
+  extern __shared__ __align__(16) uint8_t vbuf[];
+  __shared__ uint32_t slot_id[64 * NR];
   __shared__ uint32_t lids[64 * NR];
   __shared__ float ldist[64 * NR];
   const int ln = lane();
@@ -95,19 +365,33 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
   const PoolView &P = a.pool;
   const uint32_t p = a.ids[i];
   const uint32_t nv = a.v_n[i];
-  float cd[NR];
-  uint32_t ci[NR];
-#pragma unroll
-  for (int r = 0; r < NR; r++) {
-    const uint32_t e = r * 64 + ln;
-    const bool in = e < nv;
-    cd[r] = in ? a.v_d[(size_t)i * a.v_stride + e] : finf();
-    ci[r] = in ? a.v_ids[(size_t)i * a.v_stride + e] : kInvalid;
-  }
   unsigned long long evals = 0;
   uint32_t sid;
   float sdist;
-  const int nsel = wave_prune<KIND, LPV, CPL, NR>(P, p, P.R, a.coef, cd, ci, lids, ldist, sid, sdist, evals);
+  int nsel;
+  if (STAGED) {
+    // V_i holds distinct ids other than p_i
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      const uint32_t e = r * 64 + ln;
+      if (e < nv) slot_id[e] = a.v_ids[(size_t)i * a.v_stride + e];
+    }
+    __syncthreads();
+    nsel = prune_staged<KIND, LPV, CPL, NR>(P, p, (int)nv, P.R, a.coef, slot_id, vbuf, lids, ldist, sid, sdist,
+                                            evals);
+  } else {
+    float cd[NR];
+    uint32_t ci[NR];
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      const uint32_t e = r * 64 + ln;
+      const bool in = e < nv;
+      cd[r] = in ? a.v_d[(size_t)i * a.v_stride + e] : finf();
+      ci[r] = in ? a.v_ids[(size_t)i * a.v_stride + e] : kInvalid;
+    }
+    nsel = wave_prune<KIND, LPV, CPL, NR>(P.vecs, P.stride, P.nch, p, P.R, a.coef, cd, ci, lids, ldist, sid, sdist,
+                                          evals);
+  }
   if (ln < (int)P.R) {
     const bool in = ln < nsel;
     P.adj[(size_t)p * P.R + ln] = in ? sid : kInvalid;
@@ -126,13 +410,14 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
 // Rebuild of dirty nodes.  For dirty u: scratch_u = the P smallest distinct
 // (distance, source) records addressed to u; C = (N_out(u) u scratch_u)
 // minus u (and minus the delete batch); if |C| <= R, C is installed (kept
-// entries in slot order, then new sources in record order); otherwise D_u
-// is computed for the kept entries (records carry the distance of new
-// sources) and GrANDRobustPrune(u, C, D_u) is installed.  One owner per
-// dirty node, so rows are written without locks.
-template <int KIND, int LPV, int CPL, int NP, int NC>
+// entries in slot order, then new sources in record order); otherwise
+// GrANDRobustPrune(u, C, D_u) is installed.  One owner per dirty node, so
+// rows are written without locks.
+template <int KIND, int LPV, int CPL, int NP, int NC, bool STAGED>
 __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
+  extern __shared__ __align__(16) uint8_t vbuf[];
   __shared__ uint32_t rowL[64];
+  __shared__ uint32_t slot_id[64 * NC];
   __shared__ uint32_t lids[64 * NC];
   __shared__ float ldist[64 * NC];
   const int ln = lane();
@@ -179,37 +464,43 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       kn += popc(mm);
     }
     const int m = kr + kn;
-    if (keep) lids[mbcnt(km)] = rv;
-    if (m <= (int)R) {
+    uint32_t *cl = STAGED ? slot_id : lids;
+    if (keep) cl[mbcnt(km)] = rv;
 #pragma unroll
-      for (int r = 0; r < NP; r++)
-        if (isnew[r]) lids[kr + npos[r]] = si[r];
-      __syncthreads();
-      if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? lids[ln] : kInvalid;
+    for (int r = 0; r < NP; r++)
+      if (isnew[r]) {
+        cl[kr + npos[r]] = si[r];
+        if (!STAGED) ldist[kr + npos[r]] = sd[r];
+      }
+    __syncthreads();
+    if (m <= (int)R) {
+      if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? cl[ln] : kInvalid;
       if (ln == 0) P.deg[u] = (uint32_t)m;
     } else {
-      __syncthreads();
-      Slice<KIND, LPV, CPL> s;
-      load_slice<KIND, LPV, CPL>(s, P.vecs + (size_t)u * P.stride, P.nch);
-      wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, lids, ldist, kr);
-      evals += (unsigned long long)kr;
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < NP; r++)
-        if (isnew[r]) { lids[kr + npos[r]] = si[r]; ldist[kr + npos[r]] = sd[r]; }
-      __syncthreads();
-      float cd[NC];
-      uint32_t ci[NC];
-#pragma unroll
-      for (int r = 0; r < NC; r++) {
-        const int e = r * 64 + ln;
-        cd[r] = e < m ? ldist[e] : finf();
-        ci[r] = e < m ? lids[e] : kInvalid;
-      }
-      __syncthreads();
       uint32_t sid;
       float sdist;
-      const int nsel = wave_prune<KIND, LPV, CPL, NC>(P, u, R, a.coef, cd, ci, lids, ldist, sid, sdist, evals);
+      int nsel;
+      if (STAGED) {
+        nsel = prune_staged<KIND, LPV, CPL, NC>(P, u, m, R, a.coef, slot_id, vbuf, lids, ldist, sid, sdist, evals);
+      } else {
+        // D_u of kept entries from global rows; new entries carry theirs
+        Slice<KIND, LPV, CPL> s;
+        load_slice<KIND, LPV, CPL>(s, P.vecs + (size_t)u * P.stride, P.nch);
+        wave_dists<KIND, LPV, CPL>(s, P.vecs, P.stride, P.nch, lids, ldist, kr);
+        evals += (unsigned long long)kr;
+        __syncthreads();
+        float cd[NC];
+        uint32_t ci[NC];
+#pragma unroll
+        for (int r = 0; r < NC; r++) {
+          const int e = r * 64 + ln;
+          cd[r] = e < m ? ldist[e] : finf();
+          ci[r] = e < m ? lids[e] : kInvalid;
+        }
+        __syncthreads();
+        nsel = wave_prune<KIND, LPV, CPL, NC>(P.vecs, P.stride, P.nch, u, R, a.coef, cd, ci, lids, ldist, sid, sdist,
+                                              evals);
+      }
       if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? sid : kInvalid;
       if (ln == 0) P.deg[u] = (uint32_t)nsel;
       prunes++;
@@ -226,13 +517,32 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   }
 }
 
+// LDS bytes for staging `rows` candidate rows plus the node's own row.
+static size_t staged_bytes(size_t stride, uint32_t rows) { return (size_t)(rows + 1) * lds_stride(stride); }
+constexpr size_t kMaxStagedLds = 64 * 1024;
+
 hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPruneArgs &a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(max_iters, {
-    hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR>), dim3(a.n), dim3(64), 0, st, a);
+    const size_t lds = staged_bytes(a.pool.stride, 64 * NR);
+    if (lds <= kMaxStagedLds) {
+      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, true>), dim3(a.n), dim3(64), lds, st, a);
+    } else {
+      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, false>), dim3(a.n), dim3(64), 0, st, a);
+    }
     return hipGetLastError();
   }));
   return hipErrorInvalidValue;
+}
+
+template <int KIND, int LPV, int CPL, int NP, int NC>
+static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {
+  const size_t lds = staged_bytes(a.pool.stride, 64 * NC);
+  if (lds <= kMaxStagedLds) {
+    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, true>), dim3(grid), dim3(64), lds, st, a);
+  } else {
+    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, false>), dim3(grid), dim3(64), 0, st, a);
+  }
 }
 
 hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const RebuildArgs &a, uint32_t grid,
@@ -241,11 +551,11 @@ hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const Rebuil
   if (P > 128 || R + P > 256) return hipErrorInvalidValue;
   GR_DISPATCH_KV(kind, vc, {
     if (P <= 64 && R + P <= 128) {
-      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, 1, 2>), dim3(grid), dim3(64), 0, st, a);
+      launch_rebuild_t<KIND, LPV, CPL, 1, 2>(a, grid, st);
     } else if (P <= 64) {
-      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, 1, 4>), dim3(grid), dim3(64), 0, st, a);
+      launch_rebuild_t<KIND, LPV, CPL, 1, 4>(a, grid, st);
     } else {
-      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, 2, 4>), dim3(grid), dim3(64), 0, st, a);
+      launch_rebuild_t<KIND, LPV, CPL, 2, 4>(a, grid, st);
     }
     return hipGetLastError();
   });

@@ -97,10 +97,20 @@ __device__ __forceinline__ typename Acc<KIND>::T partial(const Slice<KIND, LPV, 
   return acc;
 }
 
-template <int LPV, class T>
-__device__ __forceinline__ T group_sum(T v) {
+template <int LPV>
+__device__ __forceinline__ uint32_t group_sum(uint32_t v) {
 #pragma unroll
-  for (int o = 1; o < LPV; o <<= 1) v += __shfl_xor(v, o, 64);
+  for (int o = 1; o < LPV; o <<= 1) v += xshfl(v, o);
+  return v;
+}
+template <int LPV>
+__device__ __forceinline__ double group_sum(double v) {
+#pragma unroll
+  for (int o = 1; o < LPV; o <<= 1) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = xshfl((uint32_t)b, o), hi = xshfl((uint32_t)(b >> 32), o);
+    v += __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+  }
   return v;
 }
 

@@ -18,11 +18,13 @@ constexpr uint32_t kIdMask = 0x7FFFFFFFu;
 __device__ __forceinline__ float finf() { return __builtin_inff(); }
 __device__ __forceinline__ int lane() { return (int)__lane_id(); }
 
+// Key order and equality, written with non-short-circuit operators so that
+// compare-exchange steps compile to compares and selects, not branches.
 __device__ __forceinline__ bool kless(float a, uint32_t ia, float b, uint32_t ib) {
-  return a < b || (a == b && (ia & kIdMask) < (ib & kIdMask));
+  return (a < b) | ((a == b) & ((ia & kIdMask) < (ib & kIdMask)));
 }
 __device__ __forceinline__ bool kequal(float a, uint32_t ia, float b, uint32_t ib) {
-  return a == b && (ia & kIdMask) == (ib & kIdMask);
+  return (a == b) & ((ia & kIdMask) == (ib & kIdMask));
 }
 __device__ __forceinline__ bool kvalid(uint32_t id) { return (id & kIdMask) != kIdMask; }
 
@@ -43,22 +45,50 @@ template <> __device__ __forceinline__ float rdlane(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
+// The value of lane (this lane ^ j), j a power of two below 64.  Distances
+// up to 8 use DPP moves (quad permutes, half-row mirror, row rotate), 16 a
+// swizzle within 32 lanes, and 32 a permute through the LDS crossbar.  After
+// unrolling, j is a constant and the switch folds away.
+__device__ __forceinline__ uint32_t xshfl(uint32_t v, int j) {
+  switch (j) {
+    case 1: return __builtin_amdgcn_update_dpp(0u, v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    case 2: return __builtin_amdgcn_update_dpp(0u, v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    case 4: {
+      const uint32_t t = __builtin_amdgcn_update_dpp(0u, v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+      return __builtin_amdgcn_update_dpp(0u, t, 0x1B, 0xF, 0xF, false);                 // quad_perm [3,2,1,0]
+    }
+    case 8: return __builtin_amdgcn_update_dpp(0u, v, 0x128, 0xF, 0xF, false);  // row_ror:8
+    case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);       // xor 16 within 32 lanes
+    default: return (uint32_t)__shfl_xor((int)v, j, 64);
+  }
+}
+__device__ __forceinline__ float xshfl(float v, int j) { return __uint_as_float(xshfl(__float_as_uint(v), j)); }
+
+// The value of lane (this lane - 1); lane 0 gets its own value.
+__device__ __forceinline__ uint32_t shfl_up1(uint32_t v) {
+  return __builtin_amdgcn_update_dpp(v, v, 0x138, 0xF, 0xF, false);  // wave_shr:1
+}
+__device__ __forceinline__ float shfl_up1(float v) { return __uint_as_float(shfl_up1(__float_as_uint(v))); }
+
 // Compare-exchange of this lane's element with the element j lanes away.
 // keep_min: this lane ends with the smaller key of the pair.
 __device__ __forceinline__ void cx_lane(float& d, uint32_t& id, int j, bool keep_min) {
-  float od = __shfl_xor(d, j, 64);
-  uint32_t oi = __shfl_xor(id, j, 64);
-  bool take = keep_min ? kless(od, oi, d, id) : kless(d, id, od, oi);
-  if (take) { d = od; id = oi; }
+  const float od = xshfl(d, j);
+  const uint32_t oi = xshfl(id, j);
+  const bool take = (keep_min & kless(od, oi, d, id)) | (!keep_min & kless(d, id, od, oi));
+  d = take ? od : d;
+  id = take ? oi : id;
 }
 
 // Compare-exchange of register rows a (lower index) and b (higher index).
 __device__ __forceinline__ void cx_reg(float& da, uint32_t& ia, float& db, uint32_t& ib, bool up) {
-  bool sw = up ? kless(db, ib, da, ia) : kless(da, ia, db, ib);
-  if (sw) {
-    float t = da; da = db; db = t;
-    uint32_t u = ia; ia = ib; ib = u;
-  }
+  const bool sw = (up & kless(db, ib, da, ia)) | (!up & kless(da, ia, db, ib));
+  const float td = da;
+  const uint32_t ti = ia;
+  da = sw ? db : da;
+  ia = sw ? ib : ia;
+  db = sw ? td : db;
+  ib = sw ? ti : ib;
 }
 
 // Bitonic sort, ascending, of N*64 keys held as element e = r*64 + lane.
@@ -117,8 +147,8 @@ __device__ __forceinline__ uint64_t wave_find_repeats(const float (&d)[N], const
   uint64_t any = 0;
 #pragma unroll
   for (int r = 0; r < N; r++) {
-    float pd = __shfl_up(d[r], 1, 64);
-    uint32_t pi = __shfl_up(id[r], 1, 64);
+    float pd = shfl_up1(d[r]);
+    uint32_t pi = shfl_up1(id[r]);
     if (r > 0) {
       float qd = rdlane(d[r - 1], 63);
       uint32_t qi = rdlane(id[r - 1], 63);
