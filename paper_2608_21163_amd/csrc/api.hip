@@ -28,6 +28,7 @@ struct grand_index {
   uint8_t *in_batch = nullptr;
   uint32_t *bidx = nullptr, *mark = nullptr, *cnt = nullptr, *off = nullptr, *dirty = nullptr;
   uint32_t *rev_off = nullptr, *rev_src = nullptr, *rev_sorted = nullptr, *scan_tmp = nullptr;
+  RevBufs rev{};  // bucketed full reverse-graph build
   size_t rev_sorted_cap = 0;
   void *med_tmp = nullptr;
   uint32_t epoch = 0;
@@ -272,7 +273,7 @@ grand_status run_reverse(grand_index *h, int by_batch, uint32_t n) {
   Phase ph(h, GRAND_PH_REVERSE);
   const uint32_t nrows = by_batch ? n : h->p.capacity;
   HCHK(h, launch_reverse(h->pool, by_batch, h->in_batch, h->bidx, nrows, h->cnt, h->rev_off, h->scan_tmp, h->rev_src,
-                         h->ds, h->stream));
+                         h->rev, h->ds, h->stream));
   return GRAND_OK;
 }
 
@@ -500,6 +501,7 @@ void release(grand_index *h) {
   dfree(h->pool.vecs); dfree(h->pool.adj); dfree(h->pool.deg); dfree(h->pool.active);
   dfree(h->in_batch); dfree(h->bidx); dfree(h->mark); dfree(h->cnt); dfree(h->off); dfree(h->dirty);
   dfree(h->rev_off); dfree(h->rev_src); dfree(h->rev_sorted); dfree(h->scan_tmp); dfree(h->med_tmp);
+  dfree(h->rev.pairs); dfree(h->rev.bh); dfree(h->rev.bo);
   dfree(h->ds);
   if (h->hs) (void)hipHostFree(h->hs);
   h->hs = nullptr;
@@ -574,6 +576,7 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
   h->coef = p->prune_rule == GRAND_ALPHA_ON_L2 ? a * a : a;
   h->c_stride = std::max(p->R, p->k_repair);
   const size_t cap = p->capacity;
+  h->rev.plan = rev_plan(p->capacity, p->R);
   PoolView &P = h->pool;
   P.stride = h->stride;
   P.nch = h->nch;
@@ -583,7 +586,11 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
              dalloc(&P.active, cap) || dalloc(&h->in_batch, cap) || dalloc(&h->bidx, cap) ||
              dalloc(&h->mark, cap) || dalloc(&h->cnt, cap + 1) || dalloc(&h->off, cap + 1) ||
              dalloc(&h->dirty, cap) || dalloc(&h->rev_off, cap + 1) || dalloc(&h->rev_src, cap * p->R) ||
-             dalloc(&h->scan_tmp, scan_tmp_words(cap + 1)) || dalloc(&h->ds, 1) ||
+             dalloc(&h->scan_tmp, scan_tmp_words(std::max(cap + 1, rev_bucket_words(h->rev.plan)))) ||
+             (h->rev.plan.ok && (dalloc(&h->rev.pairs, rev_pair_words(h->rev.plan, p->capacity, p->R)) ||
+                                 dalloc(&h->rev.bh, rev_bucket_words(h->rev.plan)) ||
+                                 dalloc(&h->rev.bo, rev_bucket_words(h->rev.plan)))) ||
+             dalloc(&h->ds, 1) ||
              hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
              hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess;
   if (bad) {

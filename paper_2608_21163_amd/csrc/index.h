@@ -174,9 +174,26 @@ hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const floa
                         float *gd, uint32_t *dirty, DevScalars *ds, hipStream_t s);
 hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s);
 size_t scan_tmp_words(size_t n);
+// Plan of the bucketed full reverse-graph build: targets are split into
+// nb buckets of 2^shift ids and sources into ng chunks of ch rows.
+struct RevPlan {
+  int ok;          // the bucketed build applies (else per-edge global atomics)
+  int shift;       // log2 of the bucket width
+  int packed;      // (src << shift) | (target & (width - 1)) fits 32 bits
+  uint32_t nb, ng, ch;
+};
+RevPlan rev_plan(uint32_t cap, uint32_t R);
+size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R);  // u32 words of the pair buffer
+size_t rev_bucket_words(const RevPlan &rp);                          // u32 words of each bucket table
+struct RevBufs {
+  RevPlan plan;
+  uint32_t *pairs;  // rev_pair_words
+  uint32_t *bh;     // per (bucket, chunk) counts, rev_bucket_words
+  uint32_t *bo;     // their exclusive scan, rev_bucket_words
+};
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
-                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, DevScalars *ds,
-                          hipStream_t s);
+                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,
+                          DevScalars *ds, hipStream_t s);
 hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst,
                             hipStream_t s);
 hipError_t launch_medoid(PoolView p, int kind, uint32_t dim, uint64_t n_active, void *tmp, DevScalars *ds,

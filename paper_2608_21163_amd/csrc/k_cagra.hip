@@ -105,7 +105,7 @@ __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
         float d = j < g1 ? a.gd[j] : finf();
         uint32_t s = j < g1 ? a.gsrc[j] : kInvalid;
         if (j >= g1 || (!first && !kless(lastd, lasti, d, s))) { d = finf(); s = kInvalid; }
-        wave_merge_new<1>(cd, ci, d, s, 64);
+        wave_merge_new_fast<1>(cd, ci, d, s, 64);
       }
       const int nb = popc(ballot(kvalid(ci[0])));
       if (nb == 0) break;

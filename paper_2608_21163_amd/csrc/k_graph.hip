@@ -2,6 +2,8 @@
 // grouping of reverse-edge records by target (counting sort: histogram,
 // prefix scan, scatter), the on-demand reverse graph in CSR form (Alg. 8,
 // first two loops), clearing deleted rows, and the medoid.
+#include <algorithm>
+
 #include "dispatch.h"
 
 namespace gr {
@@ -296,9 +298,141 @@ __global__ void k_count_edges(const uint32_t *off, uint32_t nrows, DevScalars *d
   if (threadIdx.x == 0) atomicAdd(&ds->rev_edges, (unsigned long long)off[nrows]);
 }
 
+// Full reverse graph without global atomics, as a two-level counting sort:
+//  1. every source chunk counts its edges per target bucket (LDS atomics);
+//  2. the (bucket, chunk) counts are scanned bucket-major;
+//  3. every chunk writes its edges as (src, target) pairs into its slice of
+//     each bucket's segment (LDS atomics hand out the positions);
+//  4. one workgroup per bucket counts its targets' in-degrees in LDS, scans
+//     them into the CSR offsets and scatters the sources into the rows.
+// HBM traffic: adj read twice, pairs written and read twice, sources
+// written once; no global atomic operations.
+constexpr int kRevThreads = 256;
+constexpr uint32_t kRevMaxBuckets = 16384;  // LDS counters of steps 1 and 3 (64 KB)
+constexpr int kRevMinShift = 8, kRevMaxShift = 13;  // bucket width 256 .. 8192 targets
+
+RevPlan rev_plan(uint32_t cap, uint32_t R) {
+  RevPlan p{};
+  int s = kRevMinShift;
+  while (s < kRevMaxShift && (((size_t)cap + (1u << s) - 1) >> s) > 1024) s++;
+  p.shift = s;
+  p.nb = (uint32_t)(((size_t)cap + (1u << s) - 1) >> s);
+  p.ng = std::max<uint32_t>(1, std::min<uint32_t>(1024, cap / 64));
+  p.ch = (cap + p.ng - 1) / p.ng;
+  const int idbits = cap > 1 ? 32 - __builtin_clz(cap - 1) : 1;
+  p.packed = idbits + s <= 32;
+  p.ok = cap > 0 && p.nb <= kRevMaxBuckets && (uint64_t)cap * R < (1ull << 32);
+  return p;
+}
+size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R) {
+  return rp.ok ? (size_t)cap * R * (rp.packed ? 1 : 2) : 0;
+}
+size_t rev_bucket_words(const RevPlan &rp) { return rp.ok ? (size_t)rp.nb * rp.ng + 1 : 0; }
+
+// Edges of chunk blockIdx.x, four loads in flight per thread; f(u, v) for
+// every edge u -> v of an active row.
+template <class F>
+__device__ __forceinline__ void for_chunk_edges(const PoolView &P, const RevPlan &rp, F f) {
+  const size_t r0 = (size_t)blockIdx.x * rp.ch;
+  const size_t r1 = std::min<size_t>(P.cap, r0 + rp.ch);
+  if (r0 >= r1) return;
+  const size_t e0 = r0 * P.R, e1 = r1 * P.R;
+  const size_t step = (size_t)blockDim.x;
+  for (size_t i = e0 + threadIdx.x; i < e1; i += 4 * step) {
+    uint32_t v[4];
+#pragma unroll
+    for (int k = 0; k < 4; k++) v[k] = i + k * step < e1 ? P.adj[i + k * step] : kInvalid;
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      if (v[k] == kInvalid) continue;
+      const uint32_t u = (uint32_t)((i + k * step) / P.R);
+      if (P.active[u]) f(u, v[k]);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_revb_count(PoolView P, RevPlan rp, uint32_t *bh) {
+  extern __shared__ uint32_t lh[];
+  for (uint32_t b = threadIdx.x; b < rp.nb; b += blockDim.x) lh[b] = 0;
+  __syncthreads();
+  for_chunk_edges(P, rp, [&](uint32_t, uint32_t v) { atomicAdd(&lh[v >> rp.shift], 1u); });
+  __syncthreads();
+  for (uint32_t b = threadIdx.x; b < rp.nb; b += blockDim.x) bh[(size_t)b * rp.ng + blockIdx.x] = lh[b];
+}
+
+template <bool PACKED>
+__global__ __launch_bounds__(kRevThreads) void k_revb_part(PoolView P, RevPlan rp, const uint32_t *bo,
+                                                           uint32_t *pairs) {
+  extern __shared__ uint32_t lo[];
+  for (uint32_t b = threadIdx.x; b < rp.nb; b += blockDim.x) lo[b] = bo[(size_t)b * rp.ng + blockIdx.x];
+  __syncthreads();
+  const uint32_t mask = (1u << rp.shift) - 1u;
+  for_chunk_edges(P, rp, [&](uint32_t u, uint32_t v) {
+    const uint32_t pos = atomicAdd(&lo[v >> rp.shift], 1u);
+    if (PACKED) pairs[pos] = (u << rp.shift) | (v & mask);
+    else reinterpret_cast<uint2 *>(pairs)[pos] = make_uint2(u, v);
+  });
+}
+
+template <bool PACKED>
+__global__ __launch_bounds__(kRevThreads) void k_revb_fill(RevPlan rp, uint32_t cap, const uint32_t *bo,
+                                                           const uint32_t *pairs, uint32_t *off, uint32_t *src) {
+  extern __shared__ uint32_t cnt[];
+  __shared__ uint32_t wsum[kRevThreads / 64];
+  const uint32_t b = blockIdx.x, W = 1u << rp.shift, mask = W - 1u;
+  const uint32_t s0 = bo[(size_t)b * rp.ng], s1 = bo[(size_t)(b + 1) * rp.ng];
+  for (uint32_t i = threadIdx.x; i < W; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+  auto target = [&](uint32_t j) -> uint32_t {
+    return PACKED ? (pairs[j] & mask) : (reinterpret_cast<const uint2 *>(pairs)[j].y & mask);
+  };
+  auto source = [&](uint32_t j) -> uint32_t {
+    return PACKED ? (pairs[j] >> rp.shift) : reinterpret_cast<const uint2 *>(pairs)[j].x;
+  };
+  for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) atomicAdd(&cnt[target(j)], 1u);
+  __syncthreads();
+  // exclusive scan of the W counts: thread t owns W / blockDim consecutive ones
+  const uint32_t per = W / blockDim.x, base = threadIdx.x * per;
+  uint32_t sum = 0;
+  for (uint32_t k = 0; k < per; k++) sum += cnt[base + k];
+  uint32_t total;
+  uint32_t run = s0 + block_excl_scan(sum, wsum, total);
+  for (uint32_t k = 0; k < per; k++) {
+    const uint32_t c = cnt[base + k];
+    const size_t v = (size_t)b * W + base + k;
+    if (v < cap) off[v] = run;
+    cnt[base + k] = run;
+    run += c;
+  }
+  __syncthreads();
+  for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) {
+    const uint32_t pos = atomicAdd(&cnt[target(j)], 1u);
+    src[pos] = source(j);
+  }
+  if (b == rp.nb - 1 && threadIdx.x == 0) off[cap] = s1;
+}
+
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
-                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, DevScalars *ds,
-                          hipStream_t s) {
+                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,
+                          DevScalars *ds, hipStream_t s) {
+  const RevPlan &rp = rb.plan;
+  if (!by_batch && rp.ok) {
+    const size_t lds_b = (size_t)rp.nb * 4, lds_w = (size_t)4 << rp.shift;
+    hipLaunchKernelGGL(k_revb_count, dim3(rp.ng), dim3(kRevThreads), lds_b, s, p, rp, rb.bh);
+    hipError_t e = launch_scan(rb.bh, rb.bo, (size_t)rp.nb * rp.ng, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    if (rp.packed) {
+      hipLaunchKernelGGL(k_revb_part<true>, dim3(rp.ng), dim3(kRevThreads), lds_b, s, p, rp, rb.bo, rb.pairs);
+      hipLaunchKernelGGL(k_revb_fill<true>, dim3(rp.nb), dim3(kRevThreads), lds_w, s, rp, p.cap, rb.bo, rb.pairs,
+                         off, src);
+    } else {
+      hipLaunchKernelGGL(k_revb_part<false>, dim3(rp.ng), dim3(kRevThreads), lds_b, s, p, rp, rb.bo, rb.pairs);
+      hipLaunchKernelGGL(k_revb_fill<false>, dim3(rp.nb), dim3(kRevThreads), lds_w, s, rp, p.cap, rb.bo, rb.pairs,
+                         off, src);
+    }
+    hipLaunchKernelGGL(k_count_edges, dim3(1), dim3(64), 0, s, off, nrows, ds);
+    return hipGetLastError();
+  }
   const size_t total = (size_t)p.cap * p.R;
   uint32_t g = blocks_for(total, 256);
   if (g > 16384) g = 16384;

@@ -205,11 +205,29 @@ struct MfmaLds {
   uint8_t *vbuf;       // [(64*NC + 1) * lds_stride] rows
 };
 
+// Dynamic LDS of the matrix-core prune for up to MP candidates:
+// blk | nrm | rows.
+__host__ __device__ constexpr size_t mfma_blk_bytes(int MP) { return (size_t)16 * MP * 4; }
+__host__ __device__ constexpr size_t mfma_nrm_bytes(int MP) { return ((size_t)(MP + 1) * 4 + 15) / 16 * 16; }
+__host__ __device__ constexpr size_t mfma_lds_bytes(size_t stride, int MP) {
+  return mfma_blk_bytes(MP) + mfma_nrm_bytes(MP) + (size_t)(MP + 1) * lds_stride(stride);
+}
+__device__ __forceinline__ MfmaLds mfma_lds(uint8_t *dyn, uint32_t *slot_id, uint32_t *spos, float *dpos, int MP) {
+  MfmaLds L;
+  L.slot_id = slot_id;
+  L.spos = spos;
+  L.dpos = dpos;
+  L.blk = reinterpret_cast<float *>(dyn);
+  L.nrm = reinterpret_cast<int32_t *>(dyn + mfma_blk_bytes(MP));
+  L.vbuf = dyn + mfma_blk_bytes(MP) + mfma_nrm_bytes(MP);
+  return L;
+}
+
 __device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
   return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
-template <int NC>
+template <int LPV, int CPL, int NC>
 __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const MfmaLds &L,
                              uint32_t &sel_id, float &sel_d, unsigned long long &evals) {
   constexpr int MP = 64 * NC;
@@ -236,7 +254,7 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
       if (r * 64 + ln < m) L.slot_id[r * 64 + ln] = kid[r];
     __syncthreads();
   }
-  stage_rows<8, 1>(P, L.slot_id, m, p, L.vbuf);
+  stage_rows<LPV, CPL>(P, L.slot_id, m, p, L.vbuf);
   __syncthreads();
   // |y|^2 per slot and D_p = |y_p|^2 + |y_j|^2 - 2 y_p.y_j (exact)
   const uint8_t *prow = L.vbuf + (size_t)m * ls;
@@ -283,12 +301,17 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
   int nsel = 0;
   bool done = false;
   for (int b = 0; b < nt && !done; b++) {
-    // valid pivots of block b: sorted positions 16b .. 16b+15 live in
-    // register row b/4, lanes 16*(b%4) ..
+    // Sorted positions 16c .. 16c+15 (tile c) live in register row c/4,
+    // lanes 16*(c%4) ..; tmask marks the tiles that still hold a valid
+    // candidate, vb the valid pivots of block b.
     uint64_t vb = 0;
+    uint32_t tmask = 0;
 #pragma unroll
     for (int r = 0; r < NC; r++) {
       const uint64_t vm = ballot(valid[r]);
+#pragma unroll
+      for (int q = 0; q < 4; q++)
+        if ((vm >> (16 * q)) & 0xFFFFull) tmask |= 1u << (4 * r + q);
       if (r == b / 4) vb = (vm >> (16 * (b % 4))) & 0xFFFFull;
     }
     if (!vb) continue;
@@ -297,6 +320,7 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
     const uint32_t aslot = L.spos[arow < m ? arow : 0];
     const int kb = ln >> 4;
     for (int c = b; c < nt; c++) {
+      if (!((tmask >> c) & 1u)) continue;
       const int bcol = 16 * c + (ln & 15);
       const uint32_t bslot = L.spos[bcol < m ? bcol : 0];
       v4i acc = {0, 0, 0, 0};
@@ -319,7 +343,7 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
         L.blk[rr * MP + bcol] = canon0((float)(rn + ncol - 2 * acc[i]));
       }
     }
-    evals += (unsigned long long)256 * (nt - b);
+    evals += (unsigned long long)256 * __popc(tmask >> b);
     __syncthreads();
     for (int t = 0; t < 16; t++) {
       const int pos = 16 * b + t;
@@ -350,10 +374,189 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
   return nsel;
 }
 
+// ---------------------------------------------------------------------------
+// uint8 GrANDRobustPrune with the candidate rows held in registers, for
+// rows of 4*NK chunks (dim = 64*NK) and at most 64*NC candidates.  Same
+// arithmetic as prune_mfma_u8 (exact int32 distances through int8 MFMA on
+// x ^ 0x80), but nothing is staged in LDS, so many waves fit per CU:
+//  1. the rows of the candidates (list order) and of p are loaded in the
+//     MFMA operand layout (tile t = candidates 16t..16t+15; lane l holds
+//     bytes 64kk + 16(l/16) .. +15 of candidate 16t + l%16), giving |y|^2 and
+//     D_p exactly;
+//  2. candidates are sorted by (D_p, id) and the rows reloaded in that order;
+//  3. the greedy selection walks blocks of 16 pivots.  For a block b and a
+//     tile c >= b one MFMA tile gives Dist(pivot, candidate) for 16 x 16
+//     pairs; each lane turns the 4 values it holds into "kill" bits
+//     (coef * Dist <= D_p[candidate]) and the bits of one candidate column
+//     are OR-ed across the 4 lane groups into a 16-bit mask over the block's
+//     pivots.  The block's pivots are resolved in order on the diagonal
+//     tile's masks (scalar loop), and later candidates are invalidated when
+//     their mask meets the set of selected pivots.
+// cl[0..m): distinct candidate ids other than p (LDS).  spos/dpos: LDS
+// scratch of 64*NC entries.  Lane t < nsel returns the t-th selection.
+template <int NK, int NC>
+__device__ int prune_mfma_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *cl,
+                              uint32_t *spos, float *dpos, uint32_t &sel_id, float &sel_d,
+                              unsigned long long &evals) {
+  constexpr int T = 4 * NC;
+  const int ln = lane(), g = ln >> 4, col = ln & 15;
+  sel_id = kInvalid;
+  sel_d = finf();
+  if (m <= 0) return 0;
+  const int nt = (m + 15) >> 4;
+  const size_t goff = (size_t)g * 16;
+  v4i B[T][NK];
+  int nrm[T];
+  auto load_tile = [&](int t, uint32_t id) {
+    const uint8_t *row = P.vecs + (size_t)id * P.stride + goff;
+    int s = 0;
+#pragma unroll
+    for (int kk = 0; kk < NK; kk++) {
+      const uint4 v = ld16(row + (size_t)kk * 64);
+      B[t][kk][0] = (int)(v.x ^ 0x80808080u);
+      B[t][kk][1] = (int)(v.y ^ 0x80808080u);
+      B[t][kk][2] = (int)(v.z ^ 0x80808080u);
+      B[t][kk][3] = (int)(v.w ^ 0x80808080u);
+#pragma unroll
+      for (int w = 0; w < 4; w++) s = sdot4((uint32_t)B[t][kk][w], (uint32_t)B[t][kk][w], s);
+    }
+    s += (int)xshfl((uint32_t)s, 16);
+    s += (int)xshfl((uint32_t)s, 32);
+    nrm[t] = s;
+  };
+  // 1. rows in list order, the node's row, D_p
+#pragma unroll
+  for (int t = 0; t < T; t++)
+    if (t < nt) {
+      const int e = 16 * t + col;
+      load_tile(t, e < m ? cl[e] : p);
+    }
+  v4i A[NK];
+  int np = 0;
+  {
+    const uint8_t *row = P.vecs + (size_t)p * P.stride + goff;
+#pragma unroll
+    for (int kk = 0; kk < NK; kk++) {
+      const uint4 v = ld16(row + (size_t)kk * 64);
+      A[kk][0] = (int)(v.x ^ 0x80808080u);
+      A[kk][1] = (int)(v.y ^ 0x80808080u);
+      A[kk][2] = (int)(v.z ^ 0x80808080u);
+      A[kk][3] = (int)(v.w ^ 0x80808080u);
+#pragma unroll
+      for (int w = 0; w < 4; w++) np = sdot4((uint32_t)A[kk][w], (uint32_t)A[kk][w], np);
+    }
+    np += (int)xshfl((uint32_t)np, 16);
+    np += (int)xshfl((uint32_t)np, 32);
+  }
+  float dt[T];
+#pragma unroll
+  for (int t = 0; t < T; t++) {
+    dt[t] = finf();
+    if (t < nt) {
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[kk], B[t][kk], acc, 0, 0, 0);
+      dt[t] = canon0((float)(np + nrm[t] - 2 * acc[0]));
+    }
+  }
+  evals += (unsigned long long)m;
+  // 2. sort by (D_p, id): position e = 16t + col of the list sits in
+  //    register row t/4 at lane 16(t%4) + col
+  float kd[NC];
+  uint32_t kid[NC];
+  bool valid[NC];
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    float d = dt[4 * r];
+#pragma unroll
+    for (int q = 1; q < 4; q++) d = g == q ? dt[4 * r + q] : d;
+    kd[r] = e < m ? d : finf();
+    kid[r] = e < m ? cl[e] : kInvalid;
+  }
+  wave_sort<NC>(kd, kid);
+#pragma unroll
+  for (int r = 0; r < NC; r++) {
+    const int e = r * 64 + ln;
+    valid[r] = e < m;
+    spos[e] = kid[r];
+    dpos[e] = kd[r];
+  }
+  __syncthreads();
+  float dcol[T];
+#pragma unroll
+  for (int t = 0; t < T; t++) {
+    dcol[t] = finf();
+    if (t < nt) {
+      const int e = 16 * t + col;
+      load_tile(t, e < m ? spos[e] : p);
+      dcol[t] = dpos[e];
+    }
+  }
+  // 3. greedy selection over pivot blocks
+  int nsel = 0;
+  bool done = false;
+#pragma unroll
+  for (int b = 0; b < T; b++) {
+    if (done || b >= nt) continue;
+    const uint32_t vb = (uint32_t)(ballot(valid[b >> 2]) >> (16 * (b & 3))) & 0xFFFFu;
+    if (!vb) continue;
+    int rn[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) rn[i] = __shfl(nrm[b], 4 * g + i, 64);
+    auto kill_mask = [&](int c) -> uint32_t {
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[b][kk], B[c][kk], acc, 0, 0, 0);
+      uint32_t km = 0;
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const float d = canon0((float)(rn[i] + nrm[c] - 2 * acc[i]));
+        km |= (coef * (double)d <= (double)dcol[c]) ? (1u << (4 * g + i)) : 0u;
+      }
+      km |= xshfl(km, 16);
+      km |= xshfl(km, 32);
+      return km;
+    };
+    const uint32_t kmd = kill_mask(b);
+    const uint32_t bid = spos[16 * b + col];
+    const float bd = dpos[16 * b + col];
+    uint32_t S = 0, alive = vb;
+    while (alive) {
+      const int t = __ffs(alive) - 1;
+      alive &= alive - 1;
+      S |= 1u << t;
+      const uint32_t sid = rdlane(bid, t);
+      const float sd = rdlane(bd, t);
+      if (ln == nsel) { sel_id = sid; sel_d = sd; }
+      nsel++;
+      if (nsel == (int)R) { done = true; break; }
+      alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
+    }
+    evals += 256;
+    if (done) continue;
+#pragma unroll
+    for (int c = b + 1; c < T; c++) {
+      if (c >= nt) continue;
+      if (!((ballot(valid[c >> 2]) >> (16 * (c & 3))) & 0xFFFFull)) continue;
+      const uint32_t km = kill_mask(c);
+      evals += 256;
+      if (g == (c & 3) && (km & S)) valid[c >> 2] = false;
+    }
+  }
+  __syncthreads();
+  return nsel;
+}
+
 // Forward lists of new nodes: GrANDRobustPrune(p_i, V_i \ {p_i}, D_{p_i}),
 // written to p_i's row (each new node owns its row), and the reverse-edge
 // records (u, p_i, D_{p_i}[u]) for every selected u.
-template <int KIND, int LPV, int CPL, int NR, bool STAGED>
+// MODE: kGlobal (rows read from global memory), kStaged (rows staged in
+// LDS), kMfma (uint8 rows staged in LDS, pairwise distances on MFMA).
+// kMfmaReg (uint8 rows of 64*NK bytes, candidate rows in registers).
+enum { kGlobal = 0, kStaged = 1, kMfma = 2, kMfmaReg = 3 };
+
+template <int KIND, int LPV, int CPL, int NR, int MODE>
 __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
   extern __shared__ __align__(16) uint8_t vbuf[];
   __shared__ uint32_t slot_id[64 * NR];
@@ -369,7 +572,7 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
   uint32_t sid;
   float sdist;
   int nsel;
-  if (STAGED) {
+  if (MODE != kGlobal) {
     // V_i holds distinct ids other than p_i
 #pragma unroll
     for (int r = 0; r < NR; r++) {
@@ -377,8 +580,12 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
       if (e < nv) slot_id[e] = a.v_ids[(size_t)i * a.v_stride + e];
     }
     __syncthreads();
-    nsel = prune_staged<KIND, LPV, CPL, NR>(P, p, (int)nv, P.R, a.coef, slot_id, vbuf, lids, ldist, sid, sdist,
-                                            evals);
+    if constexpr (MODE == kMfma)
+      nsel = prune_mfma_u8<LPV, CPL, NR>(P, p, (int)nv, P.R, a.coef, mfma_lds(vbuf, slot_id, lids, ldist, 64 * NR),
+                                         sid, sdist, evals);
+    else
+      nsel = prune_staged<KIND, LPV, CPL, NR>(P, p, (int)nv, P.R, a.coef, slot_id, vbuf, lids, ldist, sid, sdist,
+                                              evals);
   } else {
     float cd[NR];
     uint32_t ci[NR];
@@ -413,7 +620,7 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
 // entries in slot order, then new sources in record order); otherwise
 // GrANDRobustPrune(u, C, D_u) is installed.  One owner per dirty node, so
 // rows are written without locks.
-template <int KIND, int LPV, int CPL, int NP, int NC, bool STAGED>
+template <int KIND, int LPV, int CPL, int NP, int NC, int MODE, int NK = 0>
 __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   extern __shared__ __align__(16) uint8_t vbuf[];
   __shared__ uint32_t rowL[64];
@@ -439,7 +646,7 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       uint32_t sv = j < g1 ? a.gsrc[j] : kInvalid;
       float dv = j < g1 ? a.gd[j] : finf();
       if (!kvalid(sv)) { sv = kInvalid; dv = finf(); }
-      wave_merge_new<NP>(sd, si, dv, sv, (int)a.P);
+      wave_merge_new_fast<NP>(sd, si, dv, sv, (int)a.P);
     }
     const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
     const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
@@ -464,13 +671,13 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       kn += popc(mm);
     }
     const int m = kr + kn;
-    uint32_t *cl = STAGED ? slot_id : lids;
+    uint32_t *cl = MODE != kGlobal ? slot_id : lids;
     if (keep) cl[mbcnt(km)] = rv;
 #pragma unroll
     for (int r = 0; r < NP; r++)
       if (isnew[r]) {
         cl[kr + npos[r]] = si[r];
-        if (!STAGED) ldist[kr + npos[r]] = sd[r];
+        if (MODE == kGlobal) ldist[kr + npos[r]] = sd[r];
       }
     __syncthreads();
     if (m <= (int)R) {
@@ -480,7 +687,12 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       uint32_t sid;
       float sdist;
       int nsel;
-      if (STAGED) {
+      if constexpr (MODE == kMfmaReg) {
+        nsel = prune_mfma_reg<NK, NC>(P, u, m, R, a.coef, slot_id, lids, ldist, sid, sdist, evals);
+      } else if constexpr (MODE == kMfma) {
+        nsel = prune_mfma_u8<LPV, CPL, NC>(P, u, m, R, a.coef, mfma_lds(vbuf, slot_id, lids, ldist, 64 * NC), sid,
+                                           sdist, evals);
+      } else if constexpr (MODE == kStaged) {
         nsel = prune_staged<KIND, LPV, CPL, NC>(P, u, m, R, a.coef, slot_id, vbuf, lids, ldist, sid, sdist, evals);
       } else {
         // D_u of kept entries from global rows; new entries carry theirs
@@ -521,14 +733,25 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
 static size_t staged_bytes(size_t stride, uint32_t rows) { return (size_t)(rows + 1) * lds_stride(stride); }
 constexpr size_t kMaxStagedLds = 64 * 1024;
 
+// The matrix-core prune applies to uint8 rows whose chunk count is a
+// multiple of 4 (dim a multiple of 64), i.e. whole 64-byte MFMA K steps.
+static bool mfma_ok(int kind, const PoolView &P) { return kind == kU8L2 && P.nch % 4 == 0; }
+
 hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPruneArgs &a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(max_iters, {
     const size_t lds = staged_bytes(a.pool.stride, 64 * NR);
+    const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NR);
+    if constexpr (KIND == kU8L2) {
+      if (mfma_ok(kind, a.pool) && mlds <= kMaxStagedLds) {
+        hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, kMfma>), dim3(a.n), dim3(64), mlds, st, a);
+        return hipGetLastError();
+      }
+    }
     if (lds <= kMaxStagedLds) {
-      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, true>), dim3(a.n), dim3(64), lds, st, a);
+      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, kStaged>), dim3(a.n), dim3(64), lds, st, a);
     } else {
-      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, false>), dim3(a.n), dim3(64), 0, st, a);
+      hipLaunchKernelGGL((k_fwd_prune<KIND, LPV, CPL, NR, kGlobal>), dim3(a.n), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }));
@@ -538,10 +761,27 @@ hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPrune
 template <int KIND, int LPV, int CPL, int NP, int NC>
 static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {
   const size_t lds = staged_bytes(a.pool.stride, 64 * NC);
+  const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NC);
+  if constexpr (KIND == kU8L2 && NC == 2) {
+    if (a.pool.nch == 8) {
+      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kMfmaReg, 2>), dim3(grid), dim3(64), 0, st, a);
+      return;
+    }
+    if (a.pool.nch == 4) {
+      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kMfmaReg, 1>), dim3(grid), dim3(64), 0, st, a);
+      return;
+    }
+  }
+  if constexpr (KIND == kU8L2) {
+    if (mfma_ok(KIND, a.pool) && mlds <= kMaxStagedLds) {
+      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kMfma>), dim3(grid), dim3(64), mlds, st, a);
+      return;
+    }
+  }
   if (lds <= kMaxStagedLds) {
-    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, true>), dim3(grid), dim3(64), lds, st, a);
+    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kStaged>), dim3(grid), dim3(64), lds, st, a);
   } else {
-    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, false>), dim3(grid), dim3(64), 0, st, a);
+    hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kGlobal>), dim3(grid), dim3(64), 0, st, a);
   }
 }
 

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     evals += cnt;
     const float nd = ln < cnt ? nkey[ln] : finf();
     const uint32_t ni = ln < cnt ? nid[ln] : kInvalid;
-    wave_merge_new<NR>(cd, ci, nd, ni, (int)a.ell);
+    wave_merge_new_fast<NR>(cd, ci, nd, ni, (int)a.ell);
     __syncthreads();
   }
 
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(64) void k_bootstrap(BootArgs a) {
     __syncthreads();
     const float nd = ln < cnt ? nkey[ln] : finf();
     const uint32_t ni = ln < cnt ? nid[ln] : kInvalid;
-    wave_merge_new<NR>(cd, ci, nd, ni, (int)a.want);
+    wave_merge_new_fast<NR>(cd, ci, nd, ni, (int)a.want);
     __syncthreads();
   }
   const uint32_t got = a.n - 1 < a.want ? a.n - 1 : a.want;

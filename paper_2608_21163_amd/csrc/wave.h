@@ -234,6 +234,70 @@ __device__ __forceinline__ void wave_merge_new(float (&cd)[N], uint32_t (&ci)[N]
     if (r * 64 + ln >= keep) { cd[r] = finf(); ci[r] = kInvalid; }
 }
 
+// Same result as wave_merge_new (C <- the `keep` smallest distinct keys of
+// C u new), cheaper when few new keys can enter.  C holds at most `keep`
+// valid keys, sorted.  New keys not below C's key at position keep-1 (+inf
+// while C is not full) cannot enter and are dropped first; up to kFewMax
+// survivors are then inserted one at a time (rank by ballot, shift up by one
+// element), repeats of keys already in C are skipped, and keys pushed past
+// `keep` are dropped.  More survivors take the sort-and-merge path.
+constexpr int kFewMax = 16;
+template <int N>
+__device__ __forceinline__ void wave_merge_new_fast(float (&cd)[N], uint32_t (&ci)[N], float nd, uint32_t ni,
+                                                    int keep) {
+  const int ln = lane();
+  const int wr = (keep - 1) >> 6, wl = (keep - 1) & 63;
+  float wd = 0.0f;
+  uint32_t wi = 0;
+#pragma unroll
+  for (int r = 0; r < N; r++)
+    if (r == wr) {
+      wd = rdlane(cd[r], wl);
+      wi = rdlane(ci[r], wl);
+    }
+  const bool in = kvalid(ni) && kless(nd, ni, wd, wi);
+  uint64_t m = ballot(in);
+  if (!m) return;
+  if (popc(m) > kFewMax) {
+    wave_merge_new<N>(cd, ci, in ? nd : finf(), in ? ni : kInvalid, keep);
+    return;
+  }
+  while (m) {
+    const int l = ffs64(m);
+    m &= m - 1;
+    const float xd = rdlane(nd, l);
+    const uint32_t xi = rdlane(ni, l);
+    int pos = 0;
+    bool dup = false;
+#pragma unroll
+    for (int r = 0; r < N; r++) {
+      pos += popc(ballot(kless(cd[r], ci[r], xd, xi)));
+      dup |= ballot(kequal(cd[r], ci[r], xd, xi)) != 0;
+    }
+    if (dup || pos >= keep) continue;
+    float pd = 0.0f;
+    uint32_t pi = 0;
+#pragma unroll
+    for (int r = 0; r < N; r++) {
+      const float top_d = rdlane(cd[r], 63);
+      const uint32_t top_i = rdlane(ci[r], 63);
+      float ud = shfl_up1(cd[r]);
+      uint32_t ui = shfl_up1(ci[r]);
+      ud = ln == 0 ? pd : ud;
+      ui = ln == 0 ? pi : ui;
+      const int e = r * 64 + ln;
+      const bool at = e == pos, above = e > pos;
+      cd[r] = at ? xd : (above ? ud : cd[r]);
+      ci[r] = at ? xi : (above ? ui : ci[r]);
+      pd = top_d;
+      pi = top_i;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < N; r++)
+    if (r * 64 + ln >= keep) { cd[r] = finf(); ci[r] = kInvalid; }
+}
+
 // Exclusive wave prefix sum of small non-negative ints.
 __device__ __forceinline__ int wave_excl_scan(int v, int& total) {
   int x = v;
