@@ -194,8 +194,6 @@ __device__ int prune_staged(const PoolView &P, uint32_t p, int m, uint32_t R, do
 // produced by MFMA into LDS (blocks without a valid pivot are skipped), then
 // the block's pivots are taken in order, each invalidating later candidates
 // with coef * Dist(p*, p') <= D_p[p'].  Requires dim to be a multiple of 64.
-typedef int v4i __attribute__((ext_vector_type(4)));
-
 struct MfmaLds {
   uint32_t *slot_id;   // [64*NC] candidate ids, then sorted by id (slot order)
   int32_t *nrm;        // [64*NC + 1] |y|^2 per slot (slot m = the node)
@@ -221,10 +219,6 @@ __device__ __forceinline__ MfmaLds mfma_lds(uint8_t *dyn, uint32_t *slot_id, uin
   L.nrm = reinterpret_cast<int32_t *>(dyn + mfma_blk_bytes(MP));
   L.vbuf = dyn + mfma_blk_bytes(MP) + mfma_nrm_bytes(MP);
   return L;
-}
-
-__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
-  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
 }
 
 template <int LPV, int CPL, int NC>

@@ -25,6 +25,30 @@ __device__ __forceinline__ uint32_t udot4(uint32_t a, uint32_t b, uint32_t c) {
 }
 __device__ __forceinline__ float canon0(float x) { return x == 0.0f ? 0.0f : x; }
 
+// int8 matrix-core operands: uint8 rows are used as x ^ 0x80 = x - 128
+// (signed), which leaves squared Euclidean distances unchanged, so
+// Dist(i, j) = |y_i|^2 + |y_j|^2 - 2 y_i.y_j holds exactly in int32.
+typedef int v4i __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ int sdot4(uint32_t a, uint32_t b, int c) {
+  return __builtin_amdgcn_sdot4((int)a, (int)b, c, false);
+}
+__device__ __forceinline__ v4i to_i8x16(uint4 v) {
+  v4i r;
+  r[0] = (int)(v.x ^ 0x80808080u);
+  r[1] = (int)(v.y ^ 0x80808080u);
+  r[2] = (int)(v.z ^ 0x80808080u);
+  r[3] = (int)(v.w ^ 0x80808080u);
+  return r;
+}
+__device__ __forceinline__ int sq_i8x16(v4i a, int acc) {
+#pragma unroll
+  for (int w = 0; w < 4; w++) acc = sdot4((uint32_t)a[w], (uint32_t)a[w], acc);
+  return acc;
+}
+__device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
 template <int KIND> struct Acc;
 template <> struct Acc<kU8L2> { typedef uint32_t T; };
 template <> struct Acc<kF32L2> { typedef double T; };

@@ -17,6 +17,13 @@ CASES = {
     "tiny_f32_d32": ("tiny", dict(capacity=12_000), {}, 0.001),
     "u8_d128": ("sift1m_u8", dict(capacity=12_000),
                 dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    # uint8 variants that take the other matrix-core paths: 64-byte rows with
+    # c = 4 (one K step per tile, 4-key repair lists), and P = 100 (R + P >
+    # 128 candidates: the LDS-staged prune)
+    "u8_d64_c4": ("sift1m_u8", dict(capacity=12_000, dim=64, c=4, k_repair=40),
+                  dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    "u8_d128_p100": ("sift1m_u8", dict(capacity=12_000, P=100, c=3),
+                     dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     "f32_d96": ("deep1m_window", dict(capacity=9_000),
                 dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.001),
     "cagra_ip_d100": ("glove1m_cagra", dict(capacity=9_000),
