@@ -5,7 +5,10 @@ on one MI355X.
 Workload (default): 1,000,000 x 128 uint8 vectors from a 256-component
 Gaussian mixture (centres U[0,255], sigma 20, rounded and clipped), L2,
 Vamana R=64, L=128, alpha=1.2.  The base index is built by 100 batched
-inserts of 10,000 (untimed).  A step is one round of the streaming
+inserts of 10,000, then refreshed once: each base batch is deleted and
+re-inserted with the same ids and vectors, so every list is rebuilt against
+the complete base set (the batched counterpart of a static build's second
+pass; untimed).  A step is one round of the streaming
 workload: +10,000 inserts (smallest free ids), -10,000 uniformly random
 deletes, 10,000 queries (k=10, beam 64).  Inputs of every round are staged
 in device memory before timing.  One JSON line is printed:
@@ -40,6 +43,13 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="sift1m_u8")
     ap.add_argument("--base", type=int, default=0, help="override the base size (quick runs)")
+    ap.add_argument("--build-batch", type=int, default=0, help="override the batch size of the untimed base build")
+    ap.add_argument("--build-frac", type=float, default=-1.0, help="override the growth fraction of the base build")
+    ap.add_argument("--build-min", type=int, default=0, help="override the smallest base build batch")
+    ap.add_argument("--refresh-passes", type=int, default=1,
+                    help="after the base build, delete and re-insert every base batch this many times (untimed)")
+    ap.add_argument("--prune-rule", choices=["alpha_on_sq", "alpha_on_l2"], default=None,
+                    help="override the alpha test of GrANDRobustPrune")
     ap.add_argument("--rev-mode", choices=["full", "batch"], default="full")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -194,7 +204,14 @@ def main():
     st_over = dict(n_rounds=W + K)
     if args.base:
         st_over["base_n"] = args.base
-    w = make_workload(args.workload, seed=args.seed, stream=st_over)
+    if args.build_batch:
+        st_over["build_batch"] = args.build_batch
+    if args.build_frac >= 0.0:
+        st_over["build_frac"] = args.build_frac
+    if args.build_min:
+        st_over["build_min"] = args.build_min
+    idx_over = {"prune_rule": args.prune_rule} if args.prune_rule else None
+    w = make_workload(args.workload, seed=args.seed, index=idx_over, stream=st_over)
     cfg, spec = w.cfg, w.spec
     stride = ((cfg.dim * (1 if cfg.dtype == "u8" else 4)) + 15) // 16 * 16
     g = GrandIndex.from_config(cfg, max_batch=max(spec.build_batch, spec.n_insert, spec.n_delete),
@@ -210,14 +227,24 @@ def main():
 
     # ---- build (untimed)
     t0 = time.perf_counter()
-    nb = 0
+    nb = npts = 0
+    base_ops = []
     for op in w.base_batches():
         ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
         g.insert(ids, vecs)
         mirror.insert(ids, vecs)
+        base_ops.append((ids, vecs))
         nb += 1
-        if nb % 20 == 0:
-            log(f"build: {nb * spec.build_batch:,} points, {time.perf_counter() - t0:.1f} s")
+        npts += len(op.ids)
+        if nb % 50 == 0:
+            log(f"build: {npts:,} points, {time.perf_counter() - t0:.1f} s")
+    # refresh passes: the same points leave and re-enter batch by batch, so
+    # every list is rebuilt against the complete base set
+    for _ in range(args.refresh_passes):
+        for ids, vecs in base_ops:
+            g.delete(ids)
+            g.insert(ids, vecs)
+    del base_ops
     torch.cuda.synchronize()
     build_s = time.perf_counter() - t0
     log(f"build done: {spec.base_n:,} points in {build_s:.1f} s")
@@ -325,7 +352,9 @@ def main():
         "config": {"workload": w.wdef.description, "base_points": spec.base_n, "insert_batch": spec.n_insert,
                    "delete_batch": spec.n_delete, "queries": spec.n_query, "k": spec.k, "beam": spec.beam,
                    "R": cfg.R, "L": cfg.L_build, "alpha": cfg.alpha, "P": cfg.P, "c": cfg.c,
-                   "k_repair": cfg.k_repair, "reverse_graph": args.rev_mode, "parallelism": "single GPU"},
+                   "k_repair": cfg.k_repair, "reverse_graph": args.rev_mode, "parallelism": "single GPU",
+                   "base_build": f"{len(spec.build_sizes())} insert batches, then {args.refresh_passes} refresh "
+                                 f"pass(es) deleting and re-inserting each base batch (untimed)"},
         "search_qps": round(q_n / (q_ms / 1e3), 1),
         "insert_per_s": round(spec.n_insert * K / (ins_ms / 1e3), 1),
         "delete_per_s": round(spec.n_delete * K / (del_ms / 1e3), 1),

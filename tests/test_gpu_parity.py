@@ -24,6 +24,9 @@ CASES = {
                   dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     "u8_d128_p100": ("sift1m_u8", dict(capacity=12_000, P=100, c=3),
                      dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    # the Euclidean reading of the alpha test (alpha^2 on squared distances)
+    "u8_d128_l2": ("sift1m_u8", dict(capacity=12_000, prune_rule="alpha_on_l2"),
+                   dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     "f32_d96": ("deep1m_window", dict(capacity=9_000),
                 dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.001),
     "cagra_ip_d100": ("glove1m_cagra", dict(capacity=9_000),

@@ -72,6 +72,22 @@ class StreamSpec:
     beam: int
     order: Tuple[str, ...] = ("insert", "delete", "search")
     delete_policy: str = "uniform"    # "uniform" | "oldest"
+    # growing base build: with build_frac > 0 each base batch holds
+    # build_frac x (points already built) points, at least build_min and at
+    # most build_batch (the first batch, into the empty index, is build_min)
+    build_frac: float = 0.0
+    build_min: int = 0
+
+    def build_sizes(self):
+        if self.build_frac <= 0.0:
+            n_b = (self.base_n + self.build_batch - 1) // self.build_batch
+            return [min(self.build_batch, self.base_n - b * self.build_batch) for b in range(n_b)]
+        sizes, done = [], 0
+        while done < self.base_n:
+            n = min(self.build_batch, max(self.build_min, int(self.build_frac * done)), self.base_n - done)
+            sizes.append(n)
+            done += n
+        return sizes
 
 
 @dataclass(frozen=True)
@@ -243,9 +259,7 @@ class Workload:
     # -- stream ------------------------------------------------------------
     def base_batches(self) -> Iterator[Op]:
         s = self.spec
-        n_b = (s.base_n + s.build_batch - 1) // s.build_batch
-        for b in range(n_b):
-            n = min(s.build_batch, s.base_n - b * s.build_batch)
+        for b, n in enumerate(s.build_sizes()):
             g = _rng(self.seed, _P_BASE, b)
             vecs, comps = self.sampler.draw(g, n, t=0.0)
             ids = self._alloc(n)
