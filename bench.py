@@ -67,7 +67,7 @@ def copy_probe():
     x = torch.ones(n, dtype=torch.uint8, device="cuda:0")
     y = torch.empty_like(x)
     for _ in range(5):
-        y.copy_(x)
+        torch.mul(x, 1, out=y)  # an elementwise shader kernel (a D2D memcpy may run on a DMA engine)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "launches": 5}), flush=True)
 
@@ -137,6 +137,34 @@ def algorithmic_bytes(st, phase, cfg, stride):
     return None
 
 
+def profiled_traffic(phase):
+    """HBM bytes per launch of `phase` (read + write), from the rocprofv3
+    counter summary in profiles/, or None when the kernel sources changed
+    since the counters were taken (the summary records their hash)."""
+    import hashlib
+    import glob
+    path = os.path.join(ROOT, "profiles", "traffic_sift1m_u8.md")
+    if not os.path.exists(path):
+        return None
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_21163_amd", "csrc", "*"))) + \
+            [os.path.join(ROOT, "include", "grand.h")]:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    want, val = None, None
+    with open(path) as fh:
+        for line in fh:
+            t = line.split()
+            if len(t) == 2 and t[0] == "sources-sha256":
+                want = t[1]
+            elif len(t) == 3 and t[0] == "traffic" and t[1] == phase:
+                val = float(t[2])
+    if want != h.hexdigest()[:16]:
+        return None
+    return val
+
+
 # ------------------------------------------------------------------ cpu baseline
 def cpu_baseline(args, threads):
     """The oracle (plain C, OpenMP over batch items) on a bounded sample of the
@@ -151,8 +179,9 @@ def cpu_baseline(args, threads):
                       stream=dict(base_n=args.cpu_sample, n_rounds=1))
     o = Oracle(w.cfg, threads=threads)
     t0 = time.perf_counter()
-    for op in w.base_batches():
+    for b, op in enumerate(w.base_batches()):
         o.insert(op.ids, op.vecs)
+        log(f"cpu baseline: sample build batch {b + 1}, {time.perf_counter() - t0:.1f} s")
     build_s = time.perf_counter() - t0
     t_upd = t_q = 0.0
     n_upd = n_q = 0
@@ -332,8 +361,14 @@ def main():
     roofline = None
     if dom:
         ach = phases[dom]["achieved_GBps"]
+        tb = None
+        if args.workload == "sift1m_u8" and not args.base and not args.build_batch:
+            tb = profiled_traffic(dom)
         roofline = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                    "frac": round(ach / HBM_PEAK_GBS, 4),
+                    "traffic": None if tb is None else round(tb / 1e9, 5),
+                    "traffic_unit": "GB per launch, HBM read + write (rocprofv3 FETCH_SIZE and WRITE_SIZE, "
+                                    "calibrated on a 1 GiB copy; profiles/traffic_sift1m_u8.md)",
                     "ms_per_launch": phases[dom]["ms_per_launch"],
                     "alg_GB_per_launch": phases[dom]["alg_GB_per_launch"]}
 
