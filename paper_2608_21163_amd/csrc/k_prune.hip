@@ -368,151 +368,81 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
   return nsel;
 }
 
-// ---------------------------------------------------------------------------
-// uint8 GrANDRobustPrune with the candidate rows held in registers, for
-// rows of 4*NK chunks (dim = 64*NK) and at most 64*NC candidates.  Same
-// arithmetic as prune_mfma_u8 (exact int32 distances through int8 MFMA on
-// x ^ 0x80), but nothing is staged in LDS, so many waves fit per CU:
-//  1. the rows of the candidates (list order) and of p are loaded in the
-//     MFMA operand layout (tile t = candidates 16t..16t+15; lane l holds
-//     bytes 64kk + 16(l/16) .. +15 of candidate 16t + l%16), giving |y|^2 and
-//     D_p exactly;
-//  2. candidates are sorted by (D_p, id) and the rows reloaded in that order;
-//  3. the greedy selection walks blocks of 16 pivots.  For a block b and a
-//     tile c >= b one MFMA tile gives Dist(pivot, candidate) for 16 x 16
-//     pairs; each lane turns the 4 values it holds into "kill" bits
-//     (coef * Dist <= D_p[candidate]) and the bits of one candidate column
-//     are OR-ed across the 4 lane groups into a 16-bit mask over the block's
-//     pivots.  The block's pivots are resolved in order on the diagonal
-//     tile's masks (scalar loop), and later candidates are invalidated when
-//     their mask meets the set of selected pivots.
-// cl[0..m): distinct candidate ids other than p (LDS).  spos/dpos: LDS
-// scratch of 64*NC entries.  Lane t < nsel returns the t-th selection.
-template <int NK, int NC>
-__device__ int prune_mfma_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *cl,
-                              uint32_t *spos, float *dpos, uint32_t &sel_id, float &sel_d,
-                              unsigned long long &evals) {
-  constexpr int T = 4 * NC;
+// The largest integer distance d with coef * d <= D (fp64 product, as in the
+// prune test), for an integer-valued D >= 0; every d up to it passes, since
+// rounding is monotone.
+__device__ __forceinline__ int kill_threshold(double coef, float D) {
+  if (!(coef > 0.0)) return 0x7FFFFFFF;
+  const double dd = (double)D;
+  if (!(dd < 2147483647.0)) return 0x7FFFFFFF;
+  int t = (int)floor(dd / coef);
+  t = coef * (double)(t + 1) <= dd ? t + 1 : t;
+  t = coef * (double)t <= dd ? t : t - 1;
+  return t;
+}
+
+// GrANDRobustPrune's greedy selection for uint8 rows of 64*NK bytes, over
+// up to 64*NR candidates already sorted by (D_p, id): spos/dpos (LDS) hold
+// the sorted ids and distances, valid[] marks positions < m (element
+// e = r*64 + lane).  Blocks of 16 sorted positions are taken in order: the
+// block's rows are loaded as the MFMA A operand; the diagonal tile's kill
+// masks resolve the block's own pivots in order (scalar loop), then every
+// later tile that still holds a valid candidate is loaded as the B operand
+// and its candidates are invalidated when their mask meets the selected
+// pivots.  Distances are exact int32 (x ^ 0x80 operands), and the test
+// coef * Dist <= D_p is the integer test Dist <= kill_threshold(coef, D_p).
+// Rows are read from global memory (L2) when needed; nothing is staged.
+// Lane t < nsel returns the t-th selection.
+template <int NK, int NR>
+__device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
+                         const float *dpos, bool (&valid)[NR], uint32_t &sid, float &sdist,
+                         unsigned long long &evals) {
   const int ln = lane(), g = ln >> 4, col = ln & 15;
-  sel_id = kInvalid;
-  sel_d = finf();
-  if (m <= 0) return 0;
-  const int nt = (m + 15) >> 4;
   const size_t goff = (size_t)g * 16;
-  v4i B[T][NK];
-  int nrm[T];
-  auto load_tile = [&](int t, uint32_t id) {
-    const uint8_t *row = P.vecs + (size_t)id * P.stride + goff;
-    int s = 0;
+  const int nt = (m + 15) >> 4;
+  auto load_tile = [&](v4i (&dst)[NK], int t) -> int {
+    const int e = 16 * t + col;
+    const uint8_t *row = P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride + goff;
+    int sq = 0;
 #pragma unroll
     for (int kk = 0; kk < NK; kk++) {
-      const uint4 v = ld16(row + (size_t)kk * 64);
-      B[t][kk][0] = (int)(v.x ^ 0x80808080u);
-      B[t][kk][1] = (int)(v.y ^ 0x80808080u);
-      B[t][kk][2] = (int)(v.z ^ 0x80808080u);
-      B[t][kk][3] = (int)(v.w ^ 0x80808080u);
-#pragma unroll
-      for (int w = 0; w < 4; w++) s = sdot4((uint32_t)B[t][kk][w], (uint32_t)B[t][kk][w], s);
+      dst[kk] = to_i8x16(ld16(row + (size_t)kk * 64));
+      sq = sq_i8x16(dst[kk], sq);
     }
-    s += (int)xshfl((uint32_t)s, 16);
-    s += (int)xshfl((uint32_t)s, 32);
-    nrm[t] = s;
+    sq += (int)xshfl((uint32_t)sq, 16);
+    sq += (int)xshfl((uint32_t)sq, 32);
+    return sq;
   };
-  // 1. rows in list order, the node's row, D_p
+  auto tile_valid = [&](int t) -> uint32_t {
+    bool v = valid[0];
 #pragma unroll
-  for (int t = 0; t < T; t++)
-    if (t < nt) {
-      const int e = 16 * t + col;
-      load_tile(t, e < m ? cl[e] : p);
-    }
-  v4i A[NK];
-  int np = 0;
-  {
-    const uint8_t *row = P.vecs + (size_t)p * P.stride + goff;
-#pragma unroll
-    for (int kk = 0; kk < NK; kk++) {
-      const uint4 v = ld16(row + (size_t)kk * 64);
-      A[kk][0] = (int)(v.x ^ 0x80808080u);
-      A[kk][1] = (int)(v.y ^ 0x80808080u);
-      A[kk][2] = (int)(v.z ^ 0x80808080u);
-      A[kk][3] = (int)(v.w ^ 0x80808080u);
-#pragma unroll
-      for (int w = 0; w < 4; w++) np = sdot4((uint32_t)A[kk][w], (uint32_t)A[kk][w], np);
-    }
-    np += (int)xshfl((uint32_t)np, 16);
-    np += (int)xshfl((uint32_t)np, 32);
-  }
-  float dt[T];
-#pragma unroll
-  for (int t = 0; t < T; t++) {
-    dt[t] = finf();
-    if (t < nt) {
-      v4i acc = {0, 0, 0, 0};
-#pragma unroll
-      for (int kk = 0; kk < NK; kk++) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(A[kk], B[t][kk], acc, 0, 0, 0);
-      dt[t] = canon0((float)(np + nrm[t] - 2 * acc[0]));
-    }
-  }
-  evals += (unsigned long long)m;
-  // 2. sort by (D_p, id): position e = 16t + col of the list sits in
-  //    register row t/4 at lane 16(t%4) + col
-  float kd[NC];
-  uint32_t kid[NC];
-  bool valid[NC];
-#pragma unroll
-  for (int r = 0; r < NC; r++) {
-    const int e = r * 64 + ln;
-    float d = dt[4 * r];
-#pragma unroll
-    for (int q = 1; q < 4; q++) d = g == q ? dt[4 * r + q] : d;
-    kd[r] = e < m ? d : finf();
-    kid[r] = e < m ? cl[e] : kInvalid;
-  }
-  wave_sort<NC>(kd, kid);
-#pragma unroll
-  for (int r = 0; r < NC; r++) {
-    const int e = r * 64 + ln;
-    valid[r] = e < m;
-    spos[e] = kid[r];
-    dpos[e] = kd[r];
-  }
-  __syncthreads();
-  float dcol[T];
-#pragma unroll
-  for (int t = 0; t < T; t++) {
-    dcol[t] = finf();
-    if (t < nt) {
-      const int e = 16 * t + col;
-      load_tile(t, e < m ? spos[e] : p);
-      dcol[t] = dpos[e];
-    }
-  }
-  // 3. greedy selection over pivot blocks
+    for (int r = 1; r < NR; r++) v = r == (t >> 2) ? valid[r] : v;
+    return (uint32_t)(ballot(v) >> (16 * (t & 3))) & 0xFFFFu;
+  };
+  sid = kInvalid;
+  sdist = finf();
   int nsel = 0;
   bool done = false;
-#pragma unroll
-  for (int b = 0; b < T; b++) {
-    if (done || b >= nt) continue;
-    const uint32_t vb = (uint32_t)(ballot(valid[b >> 2]) >> (16 * (b & 3))) & 0xFFFFu;
+  for (int b = 0; b < nt && !done; b++) {
+    const uint32_t vb = tile_valid(b);
     if (!vb) continue;
+    v4i A[NK];
+    const int na = load_tile(A, b);
     int rn[4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) rn[i] = __shfl(nrm[b], 4 * g + i, 64);
-    auto kill_mask = [&](int c) -> uint32_t {
+    for (int ii = 0; ii < 4; ii++) rn[ii] = __shfl(na, 4 * g + ii, 64);
+    uint32_t kmd = 0;
+    {
+      const int thr = kill_threshold(coef, dpos[16 * b + col]);
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
-      for (int kk = 0; kk < NK; kk++) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(B[b][kk], B[c][kk], acc, 0, 0, 0);
-      uint32_t km = 0;
+      for (int kk = 0; kk < NK; kk++) acc = mfma_i8(A[kk], A[kk], acc);
 #pragma unroll
-      for (int i = 0; i < 4; i++) {
-        const float d = canon0((float)(rn[i] + nrm[c] - 2 * acc[i]));
-        km |= (coef * (double)d <= (double)dcol[c]) ? (1u << (4 * g + i)) : 0u;
-      }
-      km |= xshfl(km, 16);
-      km |= xshfl(km, 32);
-      return km;
-    };
-    const uint32_t kmd = kill_mask(b);
+      for (int ii = 0; ii < 4; ii++) kmd |= (rn[ii] + na - 2 * acc[ii] <= thr) ? (1u << (4 * g + ii)) : 0u;
+      kmd |= xshfl(kmd, 16);
+      kmd |= xshfl(kmd, 32);
+    }
+    evals += 256;
     const uint32_t bid = spos[16 * b + col];
     const float bd = dpos[16 * b + col];
     uint32_t S = 0, alive = vb;
@@ -520,26 +450,101 @@ __device__ int prune_mfma_reg(const PoolView &P, uint32_t p, int m, uint32_t R, 
       const int t = __ffs(alive) - 1;
       alive &= alive - 1;
       S |= 1u << t;
-      const uint32_t sid = rdlane(bid, t);
-      const float sd = rdlane(bd, t);
-      if (ln == nsel) { sel_id = sid; sel_d = sd; }
+      const uint32_t sv = rdlane(bid, t);
+      const float sdv = rdlane(bd, t);
+      if (ln == nsel) { sid = sv; sdist = sdv; }
       nsel++;
       if (nsel == (int)R) { done = true; break; }
       alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
     }
-    evals += 256;
-    if (done) continue;
+    if (done) break;
+    for (int c = b + 1; c < nt; c++) {
+      if (!tile_valid(c)) continue;
+      v4i Bt[NK];
+      const int nb = load_tile(Bt, c);
+      const int thr = kill_threshold(coef, dpos[16 * c + col]);
+      v4i acc = {0, 0, 0, 0};
 #pragma unroll
-    for (int c = b + 1; c < T; c++) {
-      if (c >= nt) continue;
-      if (!((ballot(valid[c >> 2]) >> (16 * (c & 3))) & 0xFFFFull)) continue;
-      const uint32_t km = kill_mask(c);
+      for (int kk = 0; kk < NK; kk++) acc = mfma_i8(A[kk], Bt[kk], acc);
+      uint32_t km = 0;
+#pragma unroll
+      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nb - 2 * acc[ii] <= thr) ? (1u << (4 * g + ii)) : 0u;
+      km |= xshfl(km, 16);
+      km |= xshfl(km, 32);
       evals += 256;
-      if (g == (c & 3) && (km & S)) valid[c >> 2] = false;
+      const bool dead = g == (c & 3) && (km & S) != 0;
+#pragma unroll
+      for (int r = 0; r < NR; r++)
+        if (r == (c >> 2)) valid[r] = valid[r] && !dead;
     }
   }
-  __syncthreads();
   return nsel;
+}
+
+// ---------------------------------------------------------------------------
+// Forward GrANDRobustPrune of a new uint8 point (rows of 64*NK bytes, R <=
+// 64): V_i arrives with D_{p_i} from the search, so the keys are sorted at
+// once and the greedy selection (greedy_u8) needs no gather beforehand.
+template <int NK, int NR>
+__global__ __launch_bounds__(64) void k_fwd_prune_mr(FwdPruneArgs a) {
+  __shared__ uint32_t spos[64 * NR];
+  __shared__ float dpos[64 * NR];
+  const int ln = lane();
+  const uint32_t i = blockIdx.x;
+  if (i >= a.n) return;
+  const PoolView &P = a.pool;
+  const uint32_t p = a.ids[i];
+  const uint32_t nv = a.v_n[i];
+  const uint32_t R = P.R;
+  float kd[NR];
+  uint32_t kid[NR];
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    const uint32_t e = r * 64 + ln;
+    const bool in = e < nv;
+    uint32_t id = in ? a.v_ids[(size_t)i * a.v_stride + e] : kInvalid;
+    float d = in ? a.v_d[(size_t)i * a.v_stride + e] : finf();
+    if (id == p || !kvalid(id)) { id = kInvalid; d = finf(); }
+    kd[r] = d;
+    kid[r] = id;
+  }
+  wave_sort<NR>(kd, kid);
+  {
+    uint64_t dm[NR];
+    if (wave_find_repeats<NR>(kd, kid, dm)) {
+#pragma unroll
+      for (int r = 0; r < NR; r++)
+        if ((dm[r] >> ln) & 1) { kd[r] = finf(); kid[r] = kInvalid; }
+      wave_sort<NR>(kd, kid);
+    }
+  }
+  bool valid[NR];
+  int m = 0;
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    valid[r] = kvalid(kid[r]);
+    m += popc(ballot(valid[r]));
+    spos[r * 64 + ln] = kid[r];
+    dpos[r * 64 + ln] = kd[r];
+  }
+  __syncthreads();
+  uint32_t sid;
+  float sdist;
+  unsigned long long evals = 0;
+  const int nsel = greedy_u8<NK, NR>(P, p, m, R, a.coef, spos, dpos, valid, sid, sdist, evals);
+  if (ln < (int)R) {
+    const bool in = ln < nsel;
+    P.adj[(size_t)p * R + ln] = in ? sid : kInvalid;
+    a.rec_t[(size_t)i * R + ln] = in ? sid : kInvalid;
+    a.rec_s[(size_t)i * R + ln] = p;
+    a.rec_d[(size_t)i * R + ln] = in ? sdist : 0.0f;
+  }
+  if (ln == 0) {
+    P.deg[p] = (uint32_t)nsel;
+    atomicAdd(&a.ds->fwd_prunes, 1ull);
+    atomicAdd(&a.ds->fwd_evals, evals);
+    atomicAdd(&a.ds->records, (unsigned long long)nsel);
+  }
 }
 
 // Forward lists of new nodes: GrANDRobustPrune(p_i, V_i \ {p_i}, D_{p_i}),
@@ -547,8 +552,7 @@ __device__ int prune_mfma_reg(const PoolView &P, uint32_t p, int m, uint32_t R, 
 // records (u, p_i, D_{p_i}[u]) for every selected u.
 // MODE: kGlobal (rows read from global memory), kStaged (rows staged in
 // LDS), kMfma (uint8 rows staged in LDS, pairwise distances on MFMA).
-// kMfmaReg (uint8 rows of 64*NK bytes, candidate rows in registers).
-enum { kGlobal = 0, kStaged = 1, kMfma = 2, kMfmaReg = 3 };
+enum { kGlobal = 0, kStaged = 1, kMfma = 2 };
 
 template <int KIND, int LPV, int CPL, int NR, int MODE>
 __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
@@ -614,7 +618,7 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
 // entries in slot order, then new sources in record order); otherwise
 // GrANDRobustPrune(u, C, D_u) is installed.  One owner per dirty node, so
 // rows are written without locks.
-template <int KIND, int LPV, int CPL, int NP, int NC, int MODE, int NK = 0>
+template <int KIND, int LPV, int CPL, int NP, int NC, int MODE>
 __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   extern __shared__ __align__(16) uint8_t vbuf[];
   __shared__ uint32_t rowL[64];
@@ -681,9 +685,7 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
       uint32_t sid;
       float sdist;
       int nsel;
-      if constexpr (MODE == kMfmaReg) {
-        nsel = prune_mfma_reg<NK, NC>(P, u, m, R, a.coef, slot_id, lids, ldist, sid, sdist, evals);
-      } else if constexpr (MODE == kMfma) {
+      if constexpr (MODE == kMfma) {
         nsel = prune_mfma_u8<LPV, CPL, NC>(P, u, m, R, a.coef, mfma_lds(vbuf, slot_id, lids, ldist, 64 * NC), sid,
                                            sdist, evals);
       } else if constexpr (MODE == kStaged) {
@@ -723,6 +725,133 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   }
 }
 
+// Rebuild of dirty nodes for uint8 rows of 64*NK bytes with R <= 64 and
+// R + P <= 128 (the same steps as k_rebuild).  When a node prunes, D_u of
+// every candidate comes from int8 MFMA of u's row against the candidates,
+// 16 at a time (exact, so it equals the distances the records carry); the
+// keys are sorted and greedy_u8 selects.  Only a few registers per
+// candidate tile are live at a time, so many waves fit per SIMD to hide
+// the gathers.
+template <int NK>
+__global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
+  constexpr int NC = 2;
+  __shared__ uint32_t rowL[64];
+  __shared__ uint32_t cl[64 * NC];
+  __shared__ uint32_t spos[64 * NC];
+  __shared__ float dpos[64 * NC];
+  const int ln = lane(), g = ln >> 4, col = ln & 15;
+  const PoolView &P = a.pool;
+  const uint32_t R = P.R;
+  const uint32_t nd_total = a.ds->n_dirty;
+  const size_t goff = (size_t)g * 16;
+  unsigned long long evals = 0, prunes = 0, nodes = 0, recs = 0, cand = 0;
+  for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
+    const uint32_t u = a.dirty[it];
+    nodes++;
+    const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
+    const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
+    recs += g1 - g0;
+    const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
+    const uint64_t kmask = ballot(keep);
+    const int kr = popc(kmask);
+    rowL[ln] = keep ? rv : kInvalid;
+    if (keep) cl[mbcnt(kmask)] = rv;
+    __syncthreads();
+    // scratch_u: the P smallest distinct (distance, source) records
+    float sd[1] = {finf()};
+    uint32_t si[1] = {kInvalid};
+    for (uint32_t base = g0; base < g1; base += 64) {
+      const uint32_t j = base + ln;
+      uint32_t sv = j < g1 ? a.gsrc[j] : kInvalid;
+      float dv = j < g1 ? a.gd[j] : finf();
+      if (!kvalid(sv)) { sv = kInvalid; dv = finf(); }
+      wave_merge_new_fast<1>(sd, si, dv, sv, (int)a.P);
+    }
+    bool isnew;
+    {
+      const uint32_t sv = si[0];
+      bool ok = kvalid(sv) && sv != u && !(a.in_batch && a.in_batch[sv]);
+      for (uint32_t t = 0; t < R; t++) ok = ok && rowL[t] != sv;
+      isnew = ok;
+    }
+    const uint64_t nmask = ballot(isnew);
+    const int m = kr + popc(nmask);
+    if (isnew) cl[kr + mbcnt(nmask)] = si[0];
+    __syncthreads();
+    if (m <= (int)R) {
+      if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? cl[ln] : kInvalid;
+      if (ln == 0) P.deg[u] = (uint32_t)m;
+      __syncthreads();
+      continue;
+    }
+    // D_u of every candidate (list order), into dpos
+    {
+      v4i A[NK];
+      int np = 0;
+      const uint8_t *urow = P.vecs + (size_t)u * P.stride + goff;
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) {
+        A[kk] = to_i8x16(ld16(urow + (size_t)kk * 64));
+        np = sq_i8x16(A[kk], np);
+      }
+      np += (int)xshfl((uint32_t)np, 16);
+      np += (int)xshfl((uint32_t)np, 32);
+      const int nt = (m + 15) >> 4;
+      for (int t = 0; t < nt; t++) {
+        const int e = 16 * t + col;
+        const uint8_t *row = P.vecs + (size_t)(e < m ? cl[e] : u) * P.stride + goff;
+        int sq = 0;
+        v4i acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int kk = 0; kk < NK; kk++) {
+          const v4i b = to_i8x16(ld16(row + (size_t)kk * 64));
+          sq = sq_i8x16(b, sq);
+          acc = mfma_i8(A[kk], b, acc);
+        }
+        sq += (int)xshfl((uint32_t)sq, 16);
+        sq += (int)xshfl((uint32_t)sq, 32);
+        if (g == 0) dpos[e] = canon0((float)(np + sq - 2 * acc[0]));
+      }
+    }
+    evals += (unsigned long long)m;
+    __syncthreads();
+    float kd[NC];
+    uint32_t kid[NC];
+#pragma unroll
+    for (int r = 0; r < NC; r++) {
+      const int e = r * 64 + ln;
+      kd[r] = e < m ? dpos[e] : finf();
+      kid[r] = e < m ? cl[e] : kInvalid;
+    }
+    __syncthreads();
+    wave_sort<NC>(kd, kid);
+    bool valid[NC];
+#pragma unroll
+    for (int r = 0; r < NC; r++) {
+      valid[r] = r * 64 + ln < m;
+      spos[r * 64 + ln] = kid[r];
+      dpos[r * 64 + ln] = kd[r];
+    }
+    __syncthreads();
+    uint32_t sid;
+    float sdist;
+    const int nsel = greedy_u8<NK, NC>(P, u, m, R, a.coef, spos, dpos, valid, sid, sdist, evals);
+    (void)sdist;
+    if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? sid : kInvalid;
+    if (ln == 0) P.deg[u] = (uint32_t)nsel;
+    prunes++;
+    cand += (unsigned long long)m + 1;
+    __syncthreads();
+  }
+  if (ln == 0) {
+    atomicAdd(&a.ds->rb_prunes, prunes);
+    atomicAdd(&a.ds->rb_evals, evals);
+    atomicAdd(&a.ds->dirty, nodes);
+    atomicAdd(&a.ds->rb_recs, recs);
+    atomicAdd(&a.ds->rb_cand, cand);
+  }
+}
+
 // LDS bytes for staging `rows` candidate rows plus the node's own row.
 static size_t staged_bytes(size_t stride, uint32_t rows) { return (size_t)(rows + 1) * lds_stride(stride); }
 constexpr size_t kMaxStagedLds = 64 * 1024;
@@ -733,6 +862,13 @@ static bool mfma_ok(int kind, const PoolView &P) { return kind == kU8L2 && P.nch
 
 hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPruneArgs &a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
+  if (kind == kU8L2 && a.pool.R <= 64 && (a.pool.nch == 8 || a.pool.nch == 4)) {
+    GR_DISPATCH_N(max_iters, {
+      if (a.pool.nch == 8) hipLaunchKernelGGL((k_fwd_prune_mr<2, NR>), dim3(a.n), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_fwd_prune_mr<1, NR>), dim3(a.n), dim3(64), 0, st, a);
+      return hipGetLastError();
+    });
+  }
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(max_iters, {
     const size_t lds = staged_bytes(a.pool.stride, 64 * NR);
     const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NR);
@@ -756,13 +892,13 @@ template <int KIND, int LPV, int CPL, int NP, int NC>
 static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {
   const size_t lds = staged_bytes(a.pool.stride, 64 * NC);
   const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NC);
-  if constexpr (KIND == kU8L2 && NC == 2) {
-    if (a.pool.nch == 8) {
-      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kMfmaReg, 2>), dim3(grid), dim3(64), 0, st, a);
+  if constexpr (KIND == kU8L2 && NC == 2 && NP == 1) {
+    if (a.pool.R <= 64 && a.pool.nch == 8) {
+      hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(grid), dim3(64), 0, st, a);
       return;
     }
-    if (a.pool.nch == 4) {
-      hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kMfmaReg, 1>), dim3(grid), dim3(64), 0, st, a);
+    if (a.pool.R <= 64 && a.pool.nch == 4) {
+      hipLaunchKernelGGL(k_rebuild_mr<1>, dim3(grid), dim3(64), 0, st, a);
       return;
     }
   }

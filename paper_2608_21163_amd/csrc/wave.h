@@ -118,6 +118,54 @@ __device__ __forceinline__ void wave_sort(float (&d)[N], uint32_t (&id)[N]) {
   }
 }
 
+// The same sort carrying a payload word with every key.
+__device__ __forceinline__ void cx_lane3(float& d, uint32_t& id, uint32_t& pay, int j, bool keep_min) {
+  const float od = xshfl(d, j);
+  const uint32_t oi = xshfl(id, j);
+  const uint32_t op = xshfl(pay, j);
+  const bool take = (keep_min & kless(od, oi, d, id)) | (!keep_min & kless(d, id, od, oi));
+  d = take ? od : d;
+  id = take ? oi : id;
+  pay = take ? op : pay;
+}
+__device__ __forceinline__ void cx_reg3(float& da, uint32_t& ia, uint32_t& pa, float& db, uint32_t& ib, uint32_t& pb,
+                                        bool up) {
+  const bool sw = (up & kless(db, ib, da, ia)) | (!up & kless(da, ia, db, ib));
+  const float td = da;
+  const uint32_t ti = ia, tp = pa;
+  da = sw ? db : da;
+  ia = sw ? ib : ia;
+  pa = sw ? pb : pa;
+  db = sw ? td : db;
+  ib = sw ? ti : ib;
+  pb = sw ? tp : pb;
+}
+template <int N>
+__device__ __forceinline__ void wave_sort_pay(float (&d)[N], uint32_t (&id)[N], uint32_t (&pay)[N]) {
+  const int ln = lane();
+#pragma unroll
+  for (int k = 2; k <= 64 * N; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j >= 64) {
+        const int jr = j >> 6;
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const int p = r ^ jr;
+          if (p > r) cx_reg3(d[r], id[r], pay[r], d[p], id[p], pay[p], ((r * 64 + ln) & k) == 0);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const bool up = ((r * 64 + ln) & k) == 0;
+          const bool lower = (ln & j) == 0;
+          cx_lane3(d[r], id[r], pay[r], j, lower == up);
+        }
+      }
+    }
+  }
+}
+
 // Bitonic merge (input bitonic) to ascending order.
 template <int N>
 __device__ __forceinline__ void wave_merge_up(float (&d)[N], uint32_t (&id)[N]) {
