@@ -502,6 +502,7 @@ void release(grand_index *h) {
   dfree(h->in_batch); dfree(h->bidx); dfree(h->mark); dfree(h->cnt); dfree(h->off); dfree(h->dirty);
   dfree(h->rev_off); dfree(h->rev_src); dfree(h->rev_sorted); dfree(h->scan_tmp); dfree(h->med_tmp);
   dfree(h->rev.pairs); dfree(h->rev.bh); dfree(h->rev.bo);
+  dfree(h->rev.pairs2); dfree(h->rev.bh2); dfree(h->rev.bo2);
   dfree(h->ds);
   if (h->hs) (void)hipHostFree(h->hs);
   h->hs = nullptr;
@@ -586,10 +587,14 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
              dalloc(&P.active, cap) || dalloc(&h->in_batch, cap) || dalloc(&h->bidx, cap) ||
              dalloc(&h->mark, cap) || dalloc(&h->cnt, cap + 1) || dalloc(&h->off, cap + 1) ||
              dalloc(&h->dirty, cap) || dalloc(&h->rev_off, cap + 1) || dalloc(&h->rev_src, cap * p->R) ||
-             dalloc(&h->scan_tmp, scan_tmp_words(std::max(cap + 1, rev_bucket_words(h->rev.plan)))) ||
+             dalloc(&h->scan_tmp, scan_tmp_words(std::max(std::max(cap + 1, rev_bucket_words(h->rev.plan)),
+                                                          rev_fine_words(h->rev.plan)))) ||
              (h->rev.plan.ok && (dalloc(&h->rev.pairs, rev_pair_words(h->rev.plan, p->capacity, p->R)) ||
                                  dalloc(&h->rev.bh, rev_bucket_words(h->rev.plan)) ||
                                  dalloc(&h->rev.bo, rev_bucket_words(h->rev.plan)))) ||
+             (h->rev.plan.two && (dalloc(&h->rev.pairs2, rev_pair_words(h->rev.plan, p->capacity, p->R)) ||
+                                  dalloc(&h->rev.bh2, rev_fine_words(h->rev.plan)) ||
+                                  dalloc(&h->rev.bo2, rev_fine_words(h->rev.plan)))) ||
              dalloc(&h->ds, 1) ||
              hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
              hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess;

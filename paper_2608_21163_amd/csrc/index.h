@@ -181,15 +181,25 @@ struct RevPlan {
   int shift;       // log2 of the bucket width
   int packed;      // (src << shift) | (target & (width - 1)) fits 32 bits
   uint32_t nb, ng, ch;
+  // two-level form (ids of at most 20 bits): nb1 coarse buckets of 2^s1
+  // targets, each split into nsub sub-buckets of 2^s2 targets; the coarse
+  // partition is counted in ng source chunks, the fine one in nc2 chunks of
+  // each coarse bucket
+  int two, s1, s2;
+  uint32_t nb1, nsub, nc2;
 };
 RevPlan rev_plan(uint32_t cap, uint32_t R);
-size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R);  // u32 words of the pair buffer
-size_t rev_bucket_words(const RevPlan &rp);                          // u32 words of each bucket table
+size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R);  // u32 words of each pair buffer
+size_t rev_bucket_words(const RevPlan &rp);                          // u32 words of each coarse table
+size_t rev_fine_words(const RevPlan &rp);                            // u32 words of each fine table
 struct RevBufs {
   RevPlan plan;
-  uint32_t *pairs;  // rev_pair_words
+  uint32_t *pairs;  // rev_pair_words (one-level pairs, or the coarse partition)
   uint32_t *bh;     // per (bucket, chunk) counts, rev_bucket_words
   uint32_t *bo;     // their exclusive scan, rev_bucket_words
+  uint32_t *pairs2; // fine partition (two-level form), rev_pair_words
+  uint32_t *bh2;    // per (coarse bucket, sub-bucket, chunk) counts, rev_fine_words
+  uint32_t *bo2;    // their exclusive scan
 };
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
                           uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,

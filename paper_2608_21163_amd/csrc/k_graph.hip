@@ -310,6 +310,13 @@ __global__ void k_count_edges(const uint32_t *off, uint32_t nrows, DevScalars *d
 constexpr int kRevThreads = 256;
 constexpr uint32_t kRevMaxBuckets = 16384;  // LDS counters of steps 1 and 3 (64 KB)
 constexpr int kRevMinShift = 8, kRevMaxShift = 13;  // bucket width 256 .. 8192 targets
+constexpr uint32_t kRev2Coarse = 256;      // coarse buckets (two-level form)
+constexpr int kRev2FineShift = 7;          // fine buckets of 128 targets
+constexpr uint32_t kRev2FineChunks = 16;   // chunks per coarse bucket
+constexpr uint32_t kRev2MaxSub = 256;      // fine buckets per coarse bucket
+constexpr int kRev2Per = 16;               // edges per thread per local-sort step
+constexpr int kRev2Step = kRevThreads * kRev2Per;  // edges per local-sort step
+constexpr uint32_t kRev2Stage = 12288;     // sources a fine bucket stages in LDS (48 KB)
 
 RevPlan rev_plan(uint32_t cap, uint32_t R) {
   RevPlan p{};
@@ -322,12 +329,26 @@ RevPlan rev_plan(uint32_t cap, uint32_t R) {
   const int idbits = cap > 1 ? 32 - __builtin_clz(cap - 1) : 1;
   p.packed = idbits + s <= 32;
   p.ok = cap > 0 && p.nb <= kRevMaxBuckets && (uint64_t)cap * R < (1ull << 32);
+  // two-level form: at most kRev2Coarse coarse buckets, fine buckets of
+  // 2^kRev2FineShift targets, both partitions packed into 32 bits
+  int s1 = kRev2FineShift + 1;
+  while ((((size_t)cap + (1u << s1) - 1) >> s1) > kRev2Coarse) s1++;
+  p.s1 = s1;
+  p.s2 = kRev2FineShift;
+  p.nb1 = (uint32_t)(((size_t)cap + (1u << s1) - 1) >> s1);
+  p.nsub = 1u << (s1 - p.s2);
+  p.nc2 = kRev2FineChunks;
+  p.two = p.ok && idbits + s1 <= 32 && p.nsub <= kRev2MaxSub;
   return p;
 }
 size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R) {
-  return rp.ok ? (size_t)cap * R * (rp.packed ? 1 : 2) : 0;
+  return rp.ok ? (size_t)cap * R * (rp.packed || rp.two ? 1 : 2) : 0;
 }
-size_t rev_bucket_words(const RevPlan &rp) { return rp.ok ? (size_t)rp.nb * rp.ng + 1 : 0; }
+size_t rev_bucket_words(const RevPlan &rp) {
+  if (!rp.ok) return 0;
+  return std::max((size_t)rp.nb * rp.ng, (size_t)rp.nb1 * rp.ng) + 1;
+}
+size_t rev_fine_words(const RevPlan &rp) { return rp.two ? (size_t)rp.nb1 * rp.nsub * rp.nc2 + 1 : 0; }
 
 // Edges of chunk blockIdx.x, four loads in flight per thread; f(u, v) for
 // every edge u -> v of an active row.
@@ -412,10 +433,227 @@ __global__ __launch_bounds__(kRevThreads) void k_revb_fill(RevPlan rp, uint32_t 
   if (b == rp.nb - 1 && threadIdx.x == 0) off[cap] = s1;
 }
 
+// ---- two-level form.  Every write is a run of consecutive addresses:
+// each partition step sorts a block of kRev2Step items by bucket in LDS
+// (counting sort) and then writes the block bucket by bucket, so a bucket's
+// items leave as one contiguous run instead of scattered words.
+//  A  coarse counts per (coarse bucket, source chunk)       k_rev2_count
+//  B  coarse partition: pairs (src << s1) | (target & m1)   k_rev2_part1
+//  C  fine counts per (coarse, fine bucket, chunk)          k_rev2_count2
+//  D  fine partition: pairs (src << s2) | (target & m2)     k_rev2_part2
+//  E  one workgroup per fine bucket: in-degrees, offsets, sources staged
+//     in LDS and written contiguously                      k_rev2_fill
+
+// Local counting sort of up to kRev2Step items (key < nkey) of one block:
+// returns, for this thread's items, their position in key order; fills
+// lcnt (counts) and lstart (exclusive starts).  lcnt/lstart hold nkey
+// entries (nkey <= blockDim.x * 4).
+__device__ __forceinline__ void rev2_local_sort(const uint32_t (&key)[kRev2Per], const bool (&ok)[kRev2Per],
+                                                uint32_t nkey, uint32_t *lcnt, uint32_t *lstart, uint32_t *wsum,
+                                                uint32_t (&pos)[kRev2Per]) {
+  for (uint32_t b = threadIdx.x; b < nkey; b += blockDim.x) lcnt[b] = 0;
+  __syncthreads();
+  uint32_t rk[kRev2Per];
+#pragma unroll
+  for (int k = 0; k < kRev2Per; k++) rk[k] = ok[k] ? atomicAdd(&lcnt[key[k]], 1u) : 0u;
+  __syncthreads();
+  // exclusive scan of lcnt: thread t owns keys 4t .. 4t+3
+  uint32_t c[4], sum = 0;
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    const uint32_t b = threadIdx.x * 4 + q;
+    c[q] = b < nkey ? lcnt[b] : 0u;
+    sum += c[q];
+  }
+  uint32_t total;
+  uint32_t run = block_excl_scan(sum, wsum, total);
+#pragma unroll
+  for (int q = 0; q < 4; q++) {
+    const uint32_t b = threadIdx.x * 4 + q;
+    if (b < nkey) lstart[b] = run;
+    run += c[q];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kRev2Per; k++) pos[k] = ok[k] ? lstart[key[k]] + rk[k] : 0u;
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_rev2_count(PoolView P, RevPlan rp, uint32_t *bh) {
+  __shared__ uint32_t lh[kRev2Coarse];
+  for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) lh[b] = 0;
+  __syncthreads();
+  for_chunk_edges(P, rp, [&](uint32_t, uint32_t v) { atomicAdd(&lh[v >> rp.s1], 1u); });
+  __syncthreads();
+  for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) bh[(size_t)b * rp.ng + blockIdx.x] = lh[b];
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_rev2_part1(PoolView P, RevPlan rp, const uint32_t *bo,
+                                                            uint32_t *pairs) {
+  __shared__ uint32_t gpos[kRev2Coarse], lcnt[kRev2Coarse], lstart[kRev2Coarse];
+  __shared__ uint32_t wsum[kRevThreads / 64];
+  __shared__ uint32_t sval[kRev2Step];
+  __shared__ uint8_t skey[kRev2Step];
+  for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) gpos[b] = bo[(size_t)b * rp.ng + blockIdx.x];
+  const size_t r0 = (size_t)blockIdx.x * rp.ch;
+  const size_t r1 = std::min<size_t>(P.cap, r0 + rp.ch);
+  const size_t e0 = r0 * P.R, e1 = r1 < r0 ? e0 : r1 * P.R;
+  const uint32_t m1 = (1u << rp.s1) - 1u;
+  for (size_t base = e0; base < e1; base += kRev2Step) {
+    uint32_t key[kRev2Per], val[kRev2Per], pos[kRev2Per];
+    bool ok[kRev2Per];
+#pragma unroll
+    for (int k = 0; k < kRev2Per; k++) {
+      const size_t i = base + (size_t)k * blockDim.x + threadIdx.x;
+      const bool in = i < e1;
+      const uint32_t v = in ? P.adj[i] : kInvalid;
+      const uint32_t u = (uint32_t)((in ? i : e1 - 1) / P.R);
+      ok[k] = v != kInvalid && P.active[u] != 0;
+      key[k] = ok[k] ? v >> rp.s1 : 0u;
+      val[k] = (u << rp.s1) | (v & m1);
+    }
+    rev2_local_sort(key, ok, rp.nb1, lcnt, lstart, wsum, pos);
+#pragma unroll
+    for (int k = 0; k < kRev2Per; k++)
+      if (ok[k]) {
+        sval[pos[k]] = val[k];
+        skey[pos[k]] = (uint8_t)key[k];
+      }
+    __syncthreads();
+    const uint32_t n = lstart[rp.nb1 - 1] + lcnt[rp.nb1 - 1];
+    for (uint32_t j = threadIdx.x; j < n; j += blockDim.x) {
+      const uint32_t b = skey[j];
+      pairs[gpos[b] + (j - lstart[b])] = sval[j];
+    }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) gpos[b] += lcnt[b];
+    __syncthreads();
+  }
+}
+
+// Range of chunk c (of nc2) of coarse bucket b1 in the coarse partition.
+__device__ __forceinline__ void rev2_chunk(const RevPlan &rp, const uint32_t *bo, uint32_t b1, uint32_t c,
+                                           uint32_t &x0, uint32_t &x1) {
+  const uint32_t s0 = bo[(size_t)b1 * rp.ng], s1 = bo[(size_t)(b1 + 1) * rp.ng];
+  const uint32_t n = s1 - s0;
+  x0 = s0 + (uint32_t)((uint64_t)n * c / rp.nc2);
+  x1 = s0 + (uint32_t)((uint64_t)n * (c + 1) / rp.nc2);
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_rev2_count2(RevPlan rp, const uint32_t *bo, const uint32_t *pairs,
+                                                             uint32_t *bh2) {
+  __shared__ uint32_t lh[kRev2MaxSub];
+  const uint32_t b1 = blockIdx.x / rp.nc2, c = blockIdx.x % rp.nc2;
+  for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x) lh[b] = 0;
+  __syncthreads();
+  uint32_t x0, x1;
+  rev2_chunk(rp, bo, b1, c, x0, x1);
+  const uint32_t m1 = (1u << rp.s1) - 1u;
+  for (uint32_t j = x0 + threadIdx.x; j < x1; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
+  __syncthreads();
+  for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x) bh2[((size_t)b1 * rp.nsub + b) * rp.nc2 + c] = lh[b];
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_rev2_part2(RevPlan rp, const uint32_t *bo, const uint32_t *bo2,
+                                                            const uint32_t *pairs, uint32_t *pairs2) {
+  __shared__ uint32_t gpos[kRev2MaxSub], lcnt[kRev2MaxSub], lstart[kRev2MaxSub];
+  __shared__ uint32_t wsum[kRevThreads / 64];
+  __shared__ uint32_t sval[kRev2Step];
+  __shared__ uint8_t skey[kRev2Step];
+  const uint32_t b1 = blockIdx.x / rp.nc2, c = blockIdx.x % rp.nc2;
+  for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x)
+    gpos[b] = bo2[((size_t)b1 * rp.nsub + b) * rp.nc2 + c];
+  uint32_t x0, x1;
+  rev2_chunk(rp, bo, b1, c, x0, x1);
+  const uint32_t m1 = (1u << rp.s1) - 1u, m2 = (1u << rp.s2) - 1u;
+  for (uint32_t base = x0; base < x1; base += kRev2Step) {
+    uint32_t key[kRev2Per], val[kRev2Per], pos[kRev2Per];
+    bool ok[kRev2Per];
+#pragma unroll
+    for (int k = 0; k < kRev2Per; k++) {
+      const uint32_t j = base + (uint32_t)k * blockDim.x + threadIdx.x;
+      const uint32_t x = j < x1 ? pairs[j] : 0u;
+      ok[k] = j < x1;
+      key[k] = (x & m1) >> rp.s2;
+      val[k] = ((x >> rp.s1) << rp.s2) | (x & m2);
+    }
+    rev2_local_sort(key, ok, rp.nsub, lcnt, lstart, wsum, pos);
+#pragma unroll
+    for (int k = 0; k < kRev2Per; k++)
+      if (ok[k]) {
+        sval[pos[k]] = val[k];
+        skey[pos[k]] = (uint8_t)key[k];
+      }
+    __syncthreads();
+    const uint32_t n = lstart[rp.nsub - 1] + lcnt[rp.nsub - 1];
+    for (uint32_t j = threadIdx.x; j < n; j += blockDim.x) {
+      const uint32_t b = skey[j];
+      pairs2[gpos[b] + (j - lstart[b])] = sval[j];
+    }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x) gpos[b] += lcnt[b];
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kRevThreads) void k_rev2_fill(RevPlan rp, uint32_t cap, const uint32_t *bo2,
+                                                           const uint32_t *pairs2, uint32_t *off, uint32_t *src) {
+  constexpr uint32_t W = 1u << kRev2FineShift;
+  __shared__ uint32_t cnt[W];
+  __shared__ uint32_t wsum[kRevThreads / 64];
+  __shared__ uint32_t stage[kRev2Stage];
+  const uint32_t fb = blockIdx.x;  // fine bucket = coarse * nsub + sub
+  const size_t nfine = (size_t)rp.nb1 * rp.nsub;
+  const uint32_t s0 = bo2[(size_t)fb * rp.nc2], s1 = bo2[(size_t)(fb + 1) * rp.nc2];
+  const uint32_t m2 = W - 1u;
+  for (uint32_t i = threadIdx.x; i < W; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+  for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) atomicAdd(&cnt[pairs2[j] & m2], 1u);
+  __syncthreads();
+  // offsets: W = 128 counts, thread t < W owns count t
+  const uint32_t c = threadIdx.x < W ? cnt[threadIdx.x] : 0u;
+  uint32_t total;
+  const uint32_t ex = block_excl_scan(c, wsum, total);
+  const size_t v = (size_t)fb * W + threadIdx.x;
+  if (threadIdx.x < W && v < cap) off[v] = s0 + ex;
+  __syncthreads();
+  if (threadIdx.x < W) cnt[threadIdx.x] = ex;
+  __syncthreads();
+  const uint32_t n = s1 - s0;
+  if (n <= kRev2Stage) {
+    for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) {
+      const uint32_t x = pairs2[j];
+      stage[atomicAdd(&cnt[x & m2], 1u)] = x >> rp.s2;
+    }
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < n; j += blockDim.x) src[s0 + j] = stage[j];
+  } else {
+    for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) {
+      const uint32_t x = pairs2[j];
+      src[s0 + atomicAdd(&cnt[x & m2], 1u)] = x >> rp.s2;
+    }
+  }
+  if (fb == nfine - 1 && threadIdx.x == 0) off[cap] = s1;
+}
+
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
                           uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,
                           DevScalars *ds, hipStream_t s) {
   const RevPlan &rp = rb.plan;
+  if (!by_batch && rp.two) {
+    hipLaunchKernelGGL(k_rev2_count, dim3(rp.ng), dim3(kRevThreads), 0, s, p, rp, rb.bh);
+    hipError_t e = launch_scan(rb.bh, rb.bo, (size_t)rp.nb1 * rp.ng, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rev2_part1, dim3(rp.ng), dim3(kRevThreads), 0, s, p, rp, rb.bo, rb.pairs);
+    hipLaunchKernelGGL(k_rev2_count2, dim3(rp.nb1 * rp.nc2), dim3(kRevThreads), 0, s, rp, rb.bo, rb.pairs, rb.bh2);
+    e = launch_scan(rb.bh2, rb.bo2, (size_t)rp.nb1 * rp.nsub * rp.nc2, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rev2_part2, dim3(rp.nb1 * rp.nc2), dim3(kRevThreads), 0, s, rp, rb.bo, rb.bo2, rb.pairs,
+                       rb.pairs2);
+    hipLaunchKernelGGL(k_rev2_fill, dim3(rp.nb1 * rp.nsub), dim3(kRevThreads), 0, s, rp, p.cap, rb.bo2, rb.pairs2,
+                       off, src);
+    hipLaunchKernelGGL(k_count_edges, dim3(1), dim3(64), 0, s, off, nrows, ds);
+    return hipGetLastError();
+  }
   if (!by_batch && rp.ok) {
     const size_t lds_b = (size_t)rp.nb * 4, lds_w = (size_t)4 << rp.shift;
     hipLaunchKernelGGL(k_revb_count, dim3(rp.ng), dim3(kRevThreads), lds_b, s, p, rp, rb.bh);

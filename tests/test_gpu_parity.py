@@ -265,3 +265,43 @@ def test_cagra_racing_mode_keeps_invariants():
             continue
         p, r_old = int(st1["adj"][u, s]), int(st0["adj"][u, s])
         assert p in new and r_old in set(st1["adj"][p].tolist())
+
+def test_reverse_graph_large_random_graph_is_exact_transpose():
+    """The reverse CSR of an imported 300,000-node random graph (64 distinct
+    out-neighbours per row, a few inactive rows) against the transpose
+    computed with numpy."""
+    from paper_2608_21163_amd import GrandIndex
+    from workloads.generators import IndexConfig
+    say("[reverse large]")
+    cap, R, dim = 300_000, 64, 64
+    rng = np.random.default_rng(11)
+    active = np.ones(cap, np.uint8)
+    active[rng.choice(cap, 3_000, replace=False)] = 0
+    act_ids = np.flatnonzero(active)
+    adj = np.full((cap, R), INVALID, np.uint32)
+    deg = np.zeros(cap, np.uint32)
+    # rows: distinct random active targets other than u, random degree 0..R
+    d = rng.integers(0, R + 1, size=cap)
+    d[active == 0] = 0
+    cand = act_ids[rng.integers(0, act_ids.size, size=(cap, R + 8))]
+    for u in np.flatnonzero(d):
+        row = cand[u][cand[u] != u]
+        row = np.unique(row)[: d[u]]
+        rng.shuffle(row)
+        adj[u, : row.size] = row
+        deg[u] = row.size
+    vecs = rng.integers(0, 256, size=(cap, dim), dtype=np.uint8)
+    cfg = IndexConfig("vamana", "u8", "l2", dim, cap, R, 64)
+    g = GrandIndex.from_config(cfg, max_batch=1_000)
+    g.import_graph(vecs, adj, deg, active, int(act_ids[0]))
+    e = g.export(with_reverse=True)
+    src = np.repeat(np.arange(cap, dtype=np.int64), R)
+    tgt = adj.reshape(-1).astype(np.int64)
+    keep = tgt != INVALID
+    src, tgt = src[keep], tgt[keep]
+    order = np.lexsort((src, tgt))
+    want_off = np.zeros(cap + 1, np.int64)
+    np.add.at(want_off, tgt + 1, 1)
+    want_off = np.cumsum(want_off)
+    assert np.array_equal(e["rev_offsets"].astype(np.int64), want_off)
+    assert np.array_equal(e["rev_srcs"].astype(np.int64), src[order])
