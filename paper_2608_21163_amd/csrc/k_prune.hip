@@ -391,8 +391,11 @@ __device__ __forceinline__ int kill_threshold(double coef, float D) {
 // and its candidates are invalidated when their mask meets the selected
 // pivots.  Distances are exact int32 (x ^ 0x80 operands), and the test
 // coef * Dist <= D_p is the integer test Dist <= kill_threshold(coef, D_p).
-// Rows are read from global memory (L2) when needed; nothing is staged.
+// Rows are read from global memory (L2) when needed, the later tiles of a
+// block kGroup at a time with all their loads in flight; nothing is staged.
 // Lane t < nsel returns the t-th selection.
+constexpr int kGroup = 4;  // candidate tiles loaded together by greedy_u8
+
 template <int NK, int NR>
 __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
                          const float *dpos, bool (&valid)[NR], uint32_t &sid, float &sdist,
@@ -458,24 +461,61 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
     }
     if (done) break;
-    for (int c = b + 1; c < nt; c++) {
-      if (!tile_valid(c)) continue;
-      v4i Bt[NK];
-      const int nb = load_tile(Bt, c);
-      const int thr = kill_threshold(coef, dpos[16 * c + col]);
-      v4i acc = {0, 0, 0, 0};
+    // later tiles that still hold a valid candidate, kGroup at a time: all
+    // loads of a group are issued before any is used
+    int c = b + 1;
+    while (c < nt) {
+      int cs[kGroup];
+      int ng = 0;
 #pragma unroll
-      for (int kk = 0; kk < NK; kk++) acc = mfma_i8(A[kk], Bt[kk], acc);
-      uint32_t km = 0;
+      for (int q = 0; q < kGroup; q++) {
+        cs[q] = -1;
+        while (c < nt && cs[q] < 0) {
+          if (tile_valid(c)) cs[q] = c;
+          c++;
+        }
+        ng += cs[q] >= 0 ? 1 : 0;
+      }
+      if (ng == 0) break;
+      v4i Bt[kGroup][NK];
+      int nb[kGroup], thr[kGroup];
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nb - 2 * acc[ii] <= thr) ? (1u << (4 * g + ii)) : 0u;
-      km |= xshfl(km, 16);
-      km |= xshfl(km, 32);
-      evals += 256;
-      const bool dead = g == (c & 3) && (km & S) != 0;
+      for (int q = 0; q < kGroup; q++) {
+        nb[q] = 0;
+        thr[q] = 0;
+        if (cs[q] >= 0) {
+          const int e = 16 * cs[q] + col;
+          const uint8_t *row = P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride + goff;
 #pragma unroll
-      for (int r = 0; r < NR; r++)
-        if (r == (c >> 2)) valid[r] = valid[r] && !dead;
+          for (int kk = 0; kk < NK; kk++) Bt[q][kk] = to_i8x16(ld16(row + (size_t)kk * 64));
+          thr[q] = kill_threshold(coef, dpos[e]);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kGroup; q++) {
+        if (cs[q] < 0) continue;
+        int sq = 0;
+        v4i acc = {0, 0, 0, 0};
+#pragma unroll
+        for (int kk = 0; kk < NK; kk++) {
+          sq = sq_i8x16(Bt[q][kk], sq);
+          acc = mfma_i8(A[kk], Bt[q][kk], acc);
+        }
+        sq += (int)xshfl((uint32_t)sq, 16);
+        sq += (int)xshfl((uint32_t)sq, 32);
+        nb[q] = sq;
+        uint32_t km = 0;
+#pragma unroll
+        for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nb[q] - 2 * acc[ii] <= thr[q]) ? (1u << (4 * g + ii)) : 0u;
+        km |= xshfl(km, 16);
+        km |= xshfl(km, 32);
+        evals += 256;
+        const int cc = cs[q];
+        const bool dead = g == (cc & 3) && (km & S) != 0;
+#pragma unroll
+        for (int r = 0; r < NR; r++)
+          if (r == (cc >> 2)) valid[r] = valid[r] && !dead;
+      }
     }
   }
   return nsel;
