@@ -215,9 +215,14 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
     const uint32_t u = a.list[it];
     uint32_t rv = inrow ? P.adj[(size_t)u * P.R + ln] : kInvalid;
-    for (uint32_t s = 0; s < P.R; s++) {
+    // slots holding a deleted out-neighbour, found with one parallel lookup;
+    // they are then handled in slot order (replacements only ever put
+    // non-deleted ids into the row, so the set does not change)
+    uint64_t dels = ballot(rv != kInvalid && a.in_batch[rv] != 0);
+    while (dels) {
+      const uint32_t s = (uint32_t)ffs64(dels);
+      dels &= dels - 1;
       const uint32_t p = rdlane(rv, (int)s);
-      if (p == kInvalid || !a.in_batch[p]) continue;
       // valid entries of N_out(p) in slot order (p's row is not edited here)
       const uint32_t lv = inrow ? P.adj[(size_t)p * P.R + ln] : kInvalid;
       const uint64_t vm = ballot(lv != kInvalid);

@@ -894,7 +894,7 @@ __global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
 
 // LDS bytes for staging `rows` candidate rows plus the node's own row.
 static size_t staged_bytes(size_t stride, uint32_t rows) { return (size_t)(rows + 1) * lds_stride(stride); }
-constexpr size_t kMaxStagedLds = 64 * 1024;
+constexpr size_t kMaxStagedLds = 16 * 1024;  // larger footprints limit occupancy more than staging saves
 
 // The matrix-core prune applies to uint8 rows whose chunk count is a
 // multiple of 4 (dim a multiple of 64), i.e. whole 64-byte MFMA K steps.
