@@ -26,7 +26,7 @@ struct grand_index {
   PoolView pool{};
   // pool-sized arrays (allocated once, Section 3.1 resource pool)
   uint8_t *in_batch = nullptr;
-  uint32_t *bidx = nullptr, *mark = nullptr, *cnt = nullptr, *off = nullptr, *dirty = nullptr;
+  uint32_t *bidx = nullptr, *mark = nullptr, *cnt = nullptr, *off = nullptr, *dirty = nullptr, *queue = nullptr, *qflag = nullptr;
   uint32_t *rev_off = nullptr, *rev_src = nullptr, *rev_sorted = nullptr, *scan_tmp = nullptr;
   RevBufs rev{};  // bucketed full reverse-graph build
   size_t rev_sorted_cap = 0;
@@ -248,6 +248,11 @@ grand_status run_rebuild(grand_index *h, size_t nrec, const uint8_t *in_batch) {
   RebuildArgs a{};
   a.pool = h->pool;
   a.dirty = h->dirty;
+  a.queue = h->queue;
+  a.queue_n = &h->ds->n_queue;
+  a.qflag = h->qflag;
+  a.flag_cap = h->p.capacity;
+  a.scan_tmp = h->scan_tmp;
   a.goff = h->off;
   a.gsrc = h->gsrc;
   a.gd = h->gd;
@@ -499,7 +504,7 @@ bool params_ok(const grand_params *p, std::string &why) {
 void release(grand_index *h) {
   if (h->pool.vecs) (void)hipSetDevice(h->p.device);
   dfree(h->pool.vecs); dfree(h->pool.adj); dfree(h->pool.deg); dfree(h->pool.active);
-  dfree(h->in_batch); dfree(h->bidx); dfree(h->mark); dfree(h->cnt); dfree(h->off); dfree(h->dirty);
+  dfree(h->in_batch); dfree(h->bidx); dfree(h->mark); dfree(h->cnt); dfree(h->off); dfree(h->dirty); dfree(h->queue); dfree(h->qflag);
   dfree(h->rev_off); dfree(h->rev_src); dfree(h->rev_sorted); dfree(h->scan_tmp); dfree(h->med_tmp);
   dfree(h->rev.pairs); dfree(h->rev.bh); dfree(h->rev.bo);
   dfree(h->rev.pairs2); dfree(h->rev.bh2); dfree(h->rev.bo2);
@@ -586,7 +591,7 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
   bool bad = dalloc(&P.vecs, cap * h->stride) || dalloc(&P.adj, cap * p->R) || dalloc(&P.deg, cap) ||
              dalloc(&P.active, cap) || dalloc(&h->in_batch, cap) || dalloc(&h->bidx, cap) ||
              dalloc(&h->mark, cap) || dalloc(&h->cnt, cap + 1) || dalloc(&h->off, cap + 1) ||
-             dalloc(&h->dirty, cap) || dalloc(&h->rev_off, cap + 1) || dalloc(&h->rev_src, cap * p->R) ||
+             dalloc(&h->dirty, cap) || dalloc(&h->queue, cap) || dalloc(&h->qflag, cap) || dalloc(&h->rev_off, cap + 1) || dalloc(&h->rev_src, cap * p->R) ||
              dalloc(&h->scan_tmp, scan_tmp_words(std::max(std::max(cap + 1, rev_bucket_words(h->rev.plan)),
                                                           rev_fine_words(h->rev.plan)))) ||
              (h->rev.plan.ok && (dalloc(&h->rev.pairs, rev_pair_words(h->rev.plan, p->capacity, p->R)) ||

@@ -30,6 +30,7 @@ struct DevScalars {
   uint32_t err_code;                // first validation error (0 = none)
   uint32_t err_id;
   uint32_t n_dirty;                 // number of entries in the dirty / affected list
+  uint32_t n_queue;                 // dirty nodes left by the fast rebuild for the general one
   uint32_t medoid;
   unsigned long long best_bits;     // medoid search: smallest squared distance (bit pattern)
   uint32_t best_id;
@@ -104,7 +105,15 @@ struct FwdPruneArgs {
 
 struct RebuildArgs {
   PoolView pool;
-  const uint32_t *dirty;
+  const uint32_t *dirty;      // dirty nodes (count in ds->n_dirty)
+  const uint32_t *list;       // nodes this launch rebuilds ...
+  const uint32_t *list_n;     // ... and their number (device)
+  uint32_t *queue;            // fast rebuild: nodes left for the general kernel ...
+  uint32_t *queue_n;          // ... and their number (device)
+  uint32_t *qflag;            // per list position: 1 if left for the general kernel
+  uint32_t flag_cap;          // entries of qflag (bounds the list length)
+  uint32_t *scan_tmp;         // compaction scratch (scan_tmp_words(flag_cap))
+  int count_nodes;            // this launch counts dirty nodes and records read
   const uint32_t *goff;       // group offsets by target id (cap + 1)
   const uint32_t *gsrc;
   const float *gd;
@@ -173,6 +182,10 @@ hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const floa
                         uint32_t cap, uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc,
                         float *gd, uint32_t *dirty, DevScalars *ds, hipStream_t s);
 hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s);
+// out[0..k) = the items[i] with flags[i] != 0, i < *n (n on the device, at
+// most cap), in order; *out_n = k.
+hipError_t launch_compact_flags(const uint32_t *flags, const uint32_t *items, const uint32_t *n, uint32_t cap,
+                                uint32_t *out, uint32_t *out_n, uint32_t *tmp, hipStream_t s);
 size_t scan_tmp_words(size_t n);
 // Plan of the bucketed full reverse-graph build: targets are split into
 // nb buckets of 2^shift ids and sources into ng chunks of ch rows.

@@ -140,7 +140,9 @@ constexpr int kScanThreads = 256;
 constexpr int kScanPer = 16;
 constexpr int kScanTile = kScanThreads * kScanPer;
 
-size_t scan_tmp_words(size_t n) { return (n + kScanTile - 1) / kScanTile + 2; }
+// Scratch words of launch_scan (and of the grouping scan, which keeps two
+// tile-sum arrays).
+size_t scan_tmp_words(size_t n) { return 2 * ((n + kScanTile - 1) / kScanTile + 2); }
 
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *wsum, uint32_t &total) {
   const int ln = lane(), w = threadIdx.x >> 6;
@@ -218,18 +220,143 @@ hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tm
 }
 
 // ---------------------------------------------------------------- grouping
-// Reverse-edge records (target, src, dist) grouped by target: counts per
-// target (the first record of a target appends it to the dirty list),
-// exclusive scan, scatter.  The scatter counts back down, so `cnt` is all
-// zero again afterwards.  Order inside a group is arbitrary; consumers
-// order records by (dist, src).
-__global__ void k_group_hist(const uint32_t *rec_t, size_t nrec, uint32_t *cnt, uint32_t *dirty, DevScalars *ds) {
+// Reverse-edge records (target, src, dist) grouped by target (counting sort):
+// a histogram of targets (non-returning atomics), one scan that yields both
+// the group offsets and the dirty list (the targets with a record, compacted
+// in ascending id order), and the scatter.  The scatter counts back down,
+// so `cnt` is all zero again afterwards.  Order inside a group is arbitrary;
+// consumers order records by (dist, src).
+__global__ void k_group_hist(const uint32_t *rec_t, size_t nrec, uint32_t *cnt) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nrec; i += (size_t)gridDim.x * blockDim.x) {
     const uint32_t t = rec_t[i];
-    if (t == kInvalid) continue;
-    if (atomicAdd(&cnt[t], 1u) == 0u) dirty[atomicAdd(&ds->n_dirty, 1u)] = t;
+    if (t != kInvalid) atomicAdd(&cnt[t], 1u);
   }
 }
+
+// Pass 1: per tile of kScanTile targets, the number of records and the
+// number of targets holding at least one.  Thread t reads elements
+// t, t + 256, ... of the tile (coalesced).
+__global__ __launch_bounds__(kScanThreads) void k_gscan_tiles(const uint32_t *cnt, size_t n, uint32_t *tsum,
+                                                              uint32_t *fsum) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t base = (size_t)blockIdx.x * kScanTile + threadIdx.x;
+  uint32_t s = 0, f = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    const size_t i = base + (size_t)k * kScanThreads;
+    const uint32_t c = i < n ? cnt[i] : 0u;
+    s += c;
+    f += c != 0u;
+  }
+  uint32_t ts, tf;
+  block_excl_scan(s, wsum, ts);
+  block_excl_scan(f, wsum, tf);
+  if (threadIdx.x == 0) {
+    tsum[blockIdx.x] = ts;
+    fsum[blockIdx.x] = tf;
+  }
+}
+
+// Pass 2: exclusive scans of both tile-sum arrays (one workgroup).
+__global__ __launch_bounds__(1024) void k_gscan_tsum(uint32_t *tsum, uint32_t *fsum, uint32_t nt) {
+  __shared__ uint32_t wsum[16];
+  uint32_t carry = 0, fcarry = 0;
+  for (uint32_t b0 = 0; b0 < nt; b0 += 1024) {
+    const uint32_t i = b0 + threadIdx.x;
+    const uint32_t v = i < nt ? tsum[i] : 0u, w = i < nt ? fsum[i] : 0u;
+    uint32_t total, ftotal;
+    const uint32_t ex = block_excl_scan(v, wsum, total);
+    const uint32_t fx = block_excl_scan(w, wsum, ftotal);
+    if (i < nt) {
+      tsum[i] = carry + ex;
+      fsum[i] = fcarry + fx;
+    }
+    carry += total;
+    fcarry += ftotal;
+  }
+  if (threadIdx.x == 0) {
+    tsum[nt] = carry;
+    fsum[nt] = fcarry;
+  }
+}
+
+// Pass 3: offsets of every target and the dirty list.  Each thread owns
+// kScanPer consecutive targets of the tile.
+__global__ __launch_bounds__(kScanThreads) void k_gscan_apply(const uint32_t *cnt, size_t n, const uint32_t *tsum,
+                                                              const uint32_t *fsum, uint32_t nt, uint32_t *off,
+                                                              uint32_t *dirty, DevScalars *ds) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t base = (size_t)blockIdx.x * kScanTile + (size_t)threadIdx.x * kScanPer;
+  uint32_t v[kScanPer];
+  uint32_t s = 0, f = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    v[k] = base + k < n ? cnt[base + k] : 0u;
+    s += v[k];
+    f += v[k] != 0u;
+  }
+  uint32_t total;
+  uint32_t run = tsum[blockIdx.x] + block_excl_scan(s, wsum, total);
+  uint32_t frun = fsum[blockIdx.x] + block_excl_scan(f, wsum, total);
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    if (base + k < n) off[base + k] = run;
+    if (v[k]) dirty[frun++] = (uint32_t)(base + k);
+    run += v[k];
+  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+    off[n] = tsum[nt];
+    ds->n_dirty = fsum[nt];
+  }
+}
+
+// Stream compaction by flags, for a length known only on the device: the
+// same three passes as the scan, over tiles of kScanTile flags; tiles at or
+// beyond *n contribute nothing.
+__global__ __launch_bounds__(kScanThreads) void k_cf_tiles(const uint32_t *flags, const uint32_t *np, uint32_t *tsum) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t n = *np;
+  const size_t base = (size_t)blockIdx.x * kScanTile + threadIdx.x;
+  uint32_t f = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    const size_t i = base + (size_t)k * kScanThreads;
+    f += (i < n && flags[i] != 0u) ? 1u : 0u;
+  }
+  uint32_t total;
+  block_excl_scan(f, wsum, total);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+__global__ __launch_bounds__(kScanThreads) void k_cf_apply(const uint32_t *flags, const uint32_t *items,
+                                                           const uint32_t *np, const uint32_t *tsum, uint32_t nt,
+                                                           uint32_t *out, uint32_t *out_n) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  const size_t n = *np;
+  const size_t base = (size_t)blockIdx.x * kScanTile + (size_t)threadIdx.x * kScanPer;
+  uint32_t f[kScanPer];
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    f[k] = (base + k < n && flags[base + k] != 0u) ? 1u : 0u;
+    s += f[k];
+  }
+  uint32_t total;
+  uint32_t run = tsum[blockIdx.x] + block_excl_scan(s, wsum, total);
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++)
+    if (f[k]) out[run++] = items[base + k];
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *out_n = tsum[nt];
+}
+hipError_t launch_compact_flags(const uint32_t *flags, const uint32_t *items, const uint32_t *n, uint32_t cap,
+                                uint32_t *out, uint32_t *out_n, uint32_t *tmp, hipStream_t s) {
+  const uint32_t nt = (uint32_t)((cap + kScanTile - 1) / kScanTile);
+  if (nt == 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_cf_tiles, dim3(nt), dim3(kScanThreads), 0, s, flags, n, tmp);
+  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(1024), 0, s, tmp, nt);
+  hipLaunchKernelGGL(k_cf_apply, dim3(nt), dim3(kScanThreads), 0, s, flags, items, n, tmp, nt, out, out_n);
+  return hipGetLastError();
+}
+
 __global__ void k_group_scatter(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec,
                                 uint32_t *cnt, const uint32_t *off, uint32_t *gsrc, float *gd) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nrec; i += (size_t)gridDim.x * blockDim.x) {
@@ -240,17 +367,19 @@ __global__ void k_group_scatter(const uint32_t *rec_t, const uint32_t *rec_s, co
     gd[pos] = rec_d[i];
   }
 }
-__global__ void k_zero_ndirty(DevScalars *ds) { ds->n_dirty = 0; }
 
 hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec, uint32_t cap,
                         uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc, float *gd,
                         uint32_t *dirty, DevScalars *ds, hipStream_t s) {
-  hipLaunchKernelGGL(k_zero_ndirty, dim3(1), dim3(1), 0, s, ds);
   uint32_t g = blocks_for(nrec, 256);
   if (g > 8192) g = 8192;
-  if (nrec) hipLaunchKernelGGL(k_group_hist, dim3(g), dim3(256), 0, s, rec_t, nrec, cnt, dirty, ds);
-  hipError_t e = launch_scan(cnt, off, cap, scan_tmp, s);
-  if (e != hipSuccess) return e;
+  if (nrec) hipLaunchKernelGGL(k_group_hist, dim3(g), dim3(256), 0, s, rec_t, nrec, cnt);
+  const uint32_t nt = (uint32_t)((cap + kScanTile - 1) / kScanTile);
+  uint32_t *tsum = scan_tmp, *fsum = scan_tmp + nt + 1;
+  hipLaunchKernelGGL(k_gscan_tiles, dim3(nt), dim3(kScanThreads), 0, s, cnt, (size_t)cap, tsum, fsum);
+  hipLaunchKernelGGL(k_gscan_tsum, dim3(1), dim3(1024), 0, s, tsum, fsum, nt);
+  hipLaunchKernelGGL(k_gscan_apply, dim3(nt), dim3(kScanThreads), 0, s, cnt, (size_t)cap, tsum, fsum, nt, off, dirty,
+                     ds);
   if (nrec) hipLaunchKernelGGL(k_group_scatter, dim3(g), dim3(256), 0, s, rec_t, rec_s, rec_d, nrec, cnt, off, gsrc, gd);
   return hipGetLastError();
 }

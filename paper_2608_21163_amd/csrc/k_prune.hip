@@ -521,6 +521,114 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
   return nsel;
 }
 
+// greedy_u8 with every candidate tile resident in registers: the NT tiles
+// (16 sorted candidates each, at most 16*NT candidates) are loaded once, all
+// loads in flight together, and each tile's norms and kill thresholds are
+// computed once; the block-wise selection then touches no memory.
+template <int NK, int NR, int NT>
+__device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
+                             const float *dpos, int *thr, bool (&valid)[NR], uint32_t &sid, float &sdist,
+                             unsigned long long &evals) {
+  static_assert(NT <= 4 * NR, "tiles beyond the candidate registers");
+  const int ln = lane(), g = ln >> 4, col = ln & 15;
+  const size_t goff = (size_t)g * 16;
+  const int nt = (m + 15) >> 4;
+  v4i T[NT][NK];
+  {
+    uint4 raw[NT][NK];
+#pragma unroll
+    for (int t = 0; t < NT; t++) {
+      const int e = 16 * t + col;
+      const uint8_t *row = P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride + goff;
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) raw[t][kk] = 16 * t < m ? ld16(row + (size_t)kk * 64) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; t++)
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) T[t][kk] = to_i8x16(raw[t][kk]);
+  }
+  // kill thresholds of every sorted position (LDS), norms of the tile rows
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    const int e = r * 64 + ln;
+    thr[e] = e < m ? kill_threshold(coef, dpos[e]) : -1;
+  }
+  int nrm[NT];
+#pragma unroll
+  for (int t = 0; t < NT; t++) {
+    int sq = 0;
+#pragma unroll
+    for (int kk = 0; kk < NK; kk++) sq = sq_i8x16(T[t][kk], sq);
+    sq += (int)xshfl((uint32_t)sq, 16);
+    sq += (int)xshfl((uint32_t)sq, 32);
+    nrm[t] = sq;
+  }
+  __syncthreads();
+  auto tile_valid = [&](int t) -> uint32_t {
+    bool v = valid[0];
+#pragma unroll
+    for (int r = 1; r < NR; r++) v = r == (t >> 2) ? valid[r] : v;
+    return (uint32_t)(ballot(v) >> (16 * (t & 3))) & 0xFFFFu;
+  };
+  sid = kInvalid;
+  sdist = finf();
+  int nsel = 0;
+  bool done = false;
+#pragma unroll
+  for (int b = 0; b < NT; b++) {
+    if (b >= nt || done) break;
+    const uint32_t vb = tile_valid(b);
+    if (!vb) continue;
+    int rn[4];
+#pragma unroll
+    for (int ii = 0; ii < 4; ii++) rn[ii] = __shfl(nrm[b], 4 * g + ii, 64);
+    uint32_t kmd = 0;
+    {
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[b][kk], acc);
+#pragma unroll
+      for (int ii = 0; ii < 4; ii++) kmd |= (rn[ii] + nrm[b] - 2 * acc[ii] <= thr[16 * b + col]) ? (1u << (4 * g + ii)) : 0u;
+      kmd |= xshfl(kmd, 16);
+      kmd |= xshfl(kmd, 32);
+    }
+    evals += 256;
+    const uint32_t bid = spos[16 * b + col];
+    const float bd = dpos[16 * b + col];
+    uint32_t S = 0, alive = vb;
+    while (alive) {
+      const int t = __ffs(alive) - 1;
+      alive &= alive - 1;
+      S |= 1u << t;
+      const uint32_t sv = rdlane(bid, t);
+      const float sdv = rdlane(bd, t);
+      if (ln == nsel) { sid = sv; sdist = sdv; }
+      nsel++;
+      if (nsel == (int)R) { done = true; break; }
+      alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
+    }
+    if (done) break;
+#pragma unroll
+    for (int c = b + 1; c < NT; c++) {
+      if (c >= nt) break;
+      if (!tile_valid(c)) continue;
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[c][kk], acc);
+      uint32_t km = 0;
+#pragma unroll
+      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nrm[c] - 2 * acc[ii] <= thr[16 * c + col]) ? (1u << (4 * g + ii)) : 0u;
+      km |= xshfl(km, 16);
+      km |= xshfl(km, 32);
+      evals += 256;
+      const bool dead = g == (c & 3) && (km & S) != 0;
+      valid[c >> 2] = valid[c >> 2] && !dead;
+    }
+  }
+  return nsel;
+}
+
 // ---------------------------------------------------------------------------
 // Forward GrANDRobustPrune of a new uint8 point (rows of 64*NK bytes, R <=
 // 64): V_i arrives with D_{p_i} from the search, so the keys are sorted at
@@ -668,10 +776,10 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   const int ln = lane();
   const PoolView &P = a.pool;
   const uint32_t R = P.R;
-  const uint32_t nd_total = a.ds->n_dirty;
+  const uint32_t nd_total = *a.list_n;
   unsigned long long evals = 0, prunes = 0, nodes = 0, recs = 0, cand = 0;
   for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
-    const uint32_t u = a.dirty[it];
+    const uint32_t u = a.list[it];
     nodes++;
     const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
     recs += g1 - g0;
@@ -759,9 +867,11 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   if (ln == 0) {
     atomicAdd(&a.ds->rb_prunes, prunes);
     atomicAdd(&a.ds->rb_evals, evals);
-    atomicAdd(&a.ds->dirty, nodes);
-    atomicAdd(&a.ds->rb_recs, recs);
     atomicAdd(&a.ds->rb_cand, cand);
+    if (a.count_nodes) {
+      atomicAdd(&a.ds->dirty, nodes);
+      atomicAdd(&a.ds->rb_recs, recs);
+    }
   }
 }
 
@@ -773,20 +883,22 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
 // candidate tile are live at a time, so many waves fit per SIMD to hide
 // the gathers.
 template <int NK>
-__global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
+__global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
   constexpr int NC = 2;
   __shared__ uint32_t rowL[64];
   __shared__ uint32_t cl[64 * NC];
   __shared__ uint32_t spos[64 * NC];
   __shared__ float dpos[64 * NC];
+  __shared__ int thrL[64 * NC];
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const PoolView &P = a.pool;
   const uint32_t R = P.R;
-  const uint32_t nd_total = a.ds->n_dirty;
+  const uint32_t nd_total = *a.list_n;
   const size_t goff = (size_t)g * 16;
-  unsigned long long evals = 0, prunes = 0, nodes = 0, recs = 0, cand = 0;
+  unsigned long long evals = 0;
+  uint32_t prunes = 0, nodes = 0, recs = 0, cand = 0;
   for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
-    const uint32_t u = a.dirty[it];
+    const uint32_t u = a.list[it];
     nodes++;
     const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
     const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
@@ -836,15 +948,26 @@ __global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
       }
       np += (int)xshfl((uint32_t)np, 16);
       np += (int)xshfl((uint32_t)np, 32);
-      const int nt = (m + 15) >> 4;
-      for (int t = 0; t < nt; t++) {
+      // every candidate tile is loaded before the first is used
+      constexpr int NT = 4 * NC;
+      uint4 raw[NT][NK];
+#pragma unroll
+      for (int t = 0; t < NT; t++) {
         const int e = 16 * t + col;
         const uint8_t *row = P.vecs + (size_t)(e < m ? cl[e] : u) * P.stride + goff;
+#pragma unroll
+        for (int kk = 0; kk < NK; kk++)
+          raw[t][kk] = 16 * t < m ? ld16(row + (size_t)kk * 64) : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int t = 0; t < NT; t++) {
+        if (16 * t >= m) break;
+        const int e = 16 * t + col;
         int sq = 0;
         v4i acc = {0, 0, 0, 0};
 #pragma unroll
         for (int kk = 0; kk < NK; kk++) {
-          const v4i b = to_i8x16(ld16(row + (size_t)kk * 64));
+          const v4i b = to_i8x16(raw[t][kk]);
           sq = sq_i8x16(b, sq);
           acc = mfma_i8(A[kk], b, acc);
         }
@@ -875,7 +998,7 @@ __global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
     __syncthreads();
     uint32_t sid;
     float sdist;
-    const int nsel = greedy_u8<NK, NC>(P, u, m, R, a.coef, spos, dpos, valid, sid, sdist, evals);
+    const int nsel = greedy_u8_reg<NK, NC, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, valid, sid, sdist, evals);
     (void)sdist;
     if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? sid : kInvalid;
     if (ln == 0) P.deg[u] = (uint32_t)nsel;
@@ -886,9 +1009,112 @@ __global__ __launch_bounds__(64) void k_rebuild_mr(RebuildArgs a) {
   if (ln == 0) {
     atomicAdd(&a.ds->rb_prunes, prunes);
     atomicAdd(&a.ds->rb_evals, evals);
-    atomicAdd(&a.ds->dirty, nodes);
-    atomicAdd(&a.ds->rb_recs, recs);
     atomicAdd(&a.ds->rb_cand, cand);
+    if (a.count_nodes) {
+      atomicAdd(&a.ds->dirty, nodes);
+      atomicAdd(&a.ds->rb_recs, recs);
+    }
+  }
+}
+
+// Rebuild, fast path (R <= 64, R a multiple of 4): four dirty nodes per
+// wavefront, 16 lanes per node, four row slots per lane.  For dirty u the
+// records fit when there are at most min(16, P) of them, so scratch_u is all
+// of them; C = (N_out(u) u scratch_u) minus u, repeats and the delete batch.
+// When C fits in R it is installed here (kept entries in slot order, then
+// the new sources); every other node -- more records than that, or |C| > R,
+// which needs GrANDRobustPrune -- is flagged in `qflag` and later compacted
+// into `queue` for the general kernel.  No distance is needed on this path.
+__global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
+  __shared__ uint4 rowL[64];
+  __shared__ uint32_t srcL[64];
+  __shared__ uint32_t outL[4 * 64];
+  const int ln = lane(), s = ln >> 4, q = ln & 15;
+  const PoolView &P = a.pool;
+  const uint32_t R = P.R, R4 = R >> 2;
+  const uint32_t nd = *a.list_n;
+  const uint32_t lim = a.P < 16u ? a.P : 16u;
+  unsigned long long nodes = 0, recs = 0;
+  for (uint32_t b = blockIdx.x * 4u; b < nd; b += gridDim.x * 4u) {
+    const uint32_t idx = b + (uint32_t)s;
+    const bool has = idx < nd;
+    const uint32_t u = has ? a.list[idx] : 0u;
+    uint32_t g0 = 0, g1 = 0;
+    uint4 rw = make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+    if (has) {
+      g0 = a.goff[u];
+      g1 = a.goff[u + 1];
+      if ((uint32_t)q < R4) rw = *reinterpret_cast<const uint4 *>(P.adj + (size_t)u * R + 4 * q);
+    }
+    const uint32_t nrec = g1 - g0;
+    const bool light = has && nrec <= lim;
+    uint32_t src = kInvalid;
+    if (light && (uint32_t)q < nrec) src = a.gsrc[g0 + q];
+    const uint32_t id[4] = {rw.x, rw.y, rw.z, rw.w};
+    bool keep[4];
+#pragma unroll
+    for (int k = 0; k < 4; k++) keep[k] = id[k] != kInvalid && id[k] != u && !(a.in_batch && a.in_batch[id[k]]);
+    bool nw = kvalid(src) && src != u && !(a.in_batch && a.in_batch[src]);
+    rowL[ln] = make_uint4(keep[0] ? id[0] : kInvalid, keep[1] ? id[1] : kInvalid, keep[2] ? id[2] : kInvalid,
+                          keep[3] ? id[3] : kInvalid);
+    srcL[ln] = src;
+    __syncthreads();
+    // a source already in the kept row, or repeated by an earlier record
+#pragma unroll 4
+    for (int j = 0; j < 16; j++) {
+      const uint4 r = rowL[s * 16 + j];
+      const uint32_t o = srcL[s * 16 + j];
+      nw = nw & (r.x != src) & (r.y != src) & (r.z != src) & (r.w != src) & !((j < q) & (o == src));
+    }
+    // positions: kept entries in slot order, then the new sources
+    const int kc = (int)keep[0] + (int)keep[1] + (int)keep[2] + (int)keep[3];
+    int x = kc;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int y = __shfl_up(x, o, 16);
+      if (q >= o) x += y;
+    }
+    const int kr = __shfl(x, s * 16 + 15, 64);
+    const uint32_t gm = (uint32_t)(ballot(nw) >> (16 * s)) & 0xFFFFu;
+    const int m = kr + popc((uint64_t)gm);
+    const bool install = light && m <= (int)R;
+    if (install) {
+      int pos = x - kc;
+#pragma unroll
+      for (int k = 0; k < 4; k++)
+        if (keep[k]) outL[s * 64 + pos++] = id[k];
+      if (nw) outL[s * 64 + kr + popc((uint64_t)(gm & ((1u << q) - 1u)))] = src;
+    }
+    __syncthreads();
+    if (install && (uint32_t)q < R4) {
+      const int e = 4 * q;
+      uint4 o;
+      o.x = e + 0 < m ? outL[s * 64 + e + 0] : kInvalid;
+      o.y = e + 1 < m ? outL[s * 64 + e + 1] : kInvalid;
+      o.z = e + 2 < m ? outL[s * 64 + e + 2] : kInvalid;
+      o.w = e + 3 < m ? outL[s * 64 + e + 3] : kInvalid;
+      *reinterpret_cast<uint4 *>(P.adj + (size_t)u * R + e) = o;
+    }
+    if (install && q == 0) P.deg[u] = (uint32_t)m;
+    // nodes left for the general kernel are flagged by list position and
+    // compacted afterwards (no shared counter on this path)
+    if (has && q == 0) {
+      a.qflag[idx] = install ? 0u : 1u;
+      nodes++;
+      recs += nrec;
+    }
+    __syncthreads();
+  }
+  // one atomic per wave: the counts live in lanes 0, 16, 32, 48
+  unsigned long long tn = nodes, tr = recs;
+#pragma unroll
+  for (int k = 1; k < 4; k++) {
+    tn += __shfl(nodes, 16 * k, 64);
+    tr += __shfl(recs, 16 * k, 64);
+  }
+  if (ln == 0 && tn) {
+    atomicAdd(&a.ds->dirty, tn);
+    atomicAdd(&a.ds->rb_recs, tr);
   }
 }
 
@@ -955,10 +1181,26 @@ static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st
   }
 }
 
-hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const RebuildArgs &a, uint32_t grid,
+// Dirty nodes are rebuilt by the fast kernel when the row layout allows it
+// (R <= 64, R a multiple of 4); the nodes it leaves, and every node
+// otherwise, by the general kernel of the configuration.
+hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const RebuildArgs &a0, uint32_t grid,
                           hipStream_t st) {
   if (grid == 0) return hipSuccess;
   if (P > 128 || R + P > 256) return hipErrorInvalidValue;
+  RebuildArgs a = a0;
+  a.list = a0.dirty;
+  a.list_n = &a0.ds->n_dirty;
+  a.count_nodes = 1;
+  if (R <= 64 && R % 4 == 0) {
+    // grid >= min(records, 8192) >= the blocks needed at four nodes per wave
+    hipLaunchKernelGGL(k_rebuild_fast, dim3(grid), dim3(64), 0, st, a);
+    hipError_t e = launch_compact_flags(a.qflag, a.list, a.list_n, a0.flag_cap, a.queue, a.queue_n, a.scan_tmp, st);
+    if (e != hipSuccess) return e;
+    a.list = a0.queue;
+    a.list_n = a0.queue_n;
+    a.count_nodes = 0;
+  }
   GR_DISPATCH_KV(kind, vc, {
     if (P <= 64 && R + P <= 128) {
       launch_rebuild_t<KIND, LPV, CPL, 1, 2>(a, grid, st);
