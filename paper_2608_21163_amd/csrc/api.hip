@@ -98,8 +98,9 @@ hipEvent_t get_event(grand_index *h) {
     h->spare_events.pop_back();
     return e;
   }
+  // phase markers need timestamps only: no system-scope fence
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 

@@ -527,7 +527,7 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
 // computed once; the block-wise selection then touches no memory.
 template <int NK, int NR, int NT>
 __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
-                             const float *dpos, int *thr, bool (&valid)[NR], uint32_t &sid, float &sdist,
+                             const float *dpos, int *thr, uint32_t *oid, float *od, bool (&valid)[NR],
                              unsigned long long &evals) {
   static_assert(NT <= 4 * NR, "tiles beyond the candidate registers");
   const int ln = lane(), g = ln >> 4, col = ln & 15;
@@ -571,8 +571,6 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     for (int r = 1; r < NR; r++) v = r == (t >> 2) ? valid[r] : v;
     return (uint32_t)(ballot(v) >> (16 * (t & 3))) & 0xFFFFu;
   };
-  sid = kInvalid;
-  sdist = finf();
   int nsel = 0;
   bool done = false;
 #pragma unroll
@@ -583,31 +581,42 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     int rn[4];
 #pragma unroll
     for (int ii = 0; ii < 4; ii++) rn[ii] = __shfl(nrm[b], 4 * g + ii, 64);
-    uint32_t kmd = 0;
+    // kb (lane col < 16): the block's earlier positions that would kill col
+    uint32_t kb = 0;
     {
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[b][kk], acc);
+      const int th = thr[16 * b + col];
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) kmd |= (rn[ii] + nrm[b] - 2 * acc[ii] <= thr[16 * b + col]) ? (1u << (4 * g + ii)) : 0u;
-      kmd |= xshfl(kmd, 16);
-      kmd |= xshfl(kmd, 32);
+      for (int ii = 0; ii < 4; ii++) kb |= (rn[ii] + nrm[b] - 2 * acc[ii] <= th) ? (1u << (4 * g + ii)) : 0u;
+      kb |= xshfl(kb, 16);
+      kb |= xshfl(kb, 32);
+      kb &= (1u << col) - 1u;
     }
     evals += 256;
-    const uint32_t bid = spos[16 * b + col];
-    const float bd = dpos[16 * b + col];
-    uint32_t S = 0, alive = vb;
-    while (alive) {
-      const int t = __ffs(alive) - 1;
-      alive &= alive - 1;
-      S |= 1u << t;
-      const uint32_t sv = rdlane(bid, t);
-      const float sdv = rdlane(bd, t);
-      if (ln == nsel) { sid = sv; sdist = sdv; }
-      nsel++;
-      if (nsel == (int)R) { done = true; break; }
-      alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
+    // the block's pivots in order: a live position is selected unless an
+    // earlier selected one kills it
+    uint32_t S = 0, rest = vb;
+    const int room = (int)R - nsel;
+    int ns = 0;
+    while (rest) {
+      const int t = __ffs(rest) - 1;
+      rest &= rest - 1;
+      if ((rdlane(kb, t) & S) == 0u) {
+        S |= 1u << t;
+        if (++ns == room) {
+          done = true;
+          break;
+        }
+      }
     }
+    if (g == 0 && ((S >> col) & 1u)) {
+      const int pos = nsel + __popc(S & ((1u << col) - 1u));
+      oid[pos] = spos[16 * b + col];
+      od[pos] = dpos[16 * b + col];
+    }
+    nsel += ns;
     if (done) break;
 #pragma unroll
     for (int c = b + 1; c < NT; c++) {
@@ -616,9 +625,10 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[c][kk], acc);
+      const int th = thr[16 * c + col];
       uint32_t km = 0;
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nrm[c] - 2 * acc[ii] <= thr[16 * c + col]) ? (1u << (4 * g + ii)) : 0u;
+      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nrm[c] - 2 * acc[ii] <= th) ? (1u << (4 * g + ii)) : 0u;
       km |= xshfl(km, 16);
       km |= xshfl(km, 32);
       evals += 256;
@@ -626,6 +636,7 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
       valid[c >> 2] = valid[c >> 2] && !dead;
     }
   }
+  __syncthreads();
   return nsel;
 }
 
@@ -885,11 +896,13 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
 template <int NK>
 __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
   constexpr int NC = 2;
-  __shared__ uint32_t rowL[64];
+  __shared__ uint4 rowL[16];
   __shared__ uint32_t cl[64 * NC];
   __shared__ uint32_t spos[64 * NC];
   __shared__ float dpos[64 * NC];
   __shared__ int thrL[64 * NC];
+  __shared__ uint32_t oid[64];
+  __shared__ float od[64];
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const PoolView &P = a.pool;
   const uint32_t R = P.R;
@@ -906,7 +919,7 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
     const uint64_t kmask = ballot(keep);
     const int kr = popc(kmask);
-    rowL[ln] = keep ? rv : kInvalid;
+    reinterpret_cast<uint32_t *>(rowL)[ln] = keep ? rv : kInvalid;
     if (keep) cl[mbcnt(kmask)] = rv;
     __syncthreads();
     // scratch_u: the P smallest distinct (distance, source) records
@@ -923,7 +936,11 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     {
       const uint32_t sv = si[0];
       bool ok = kvalid(sv) && sv != u && !(a.in_batch && a.in_batch[sv]);
-      for (uint32_t t = 0; t < R; t++) ok = ok && rowL[t] != sv;
+#pragma unroll 4
+      for (int t = 0; t < 16; t++) {
+        const uint4 r4 = rowL[t];
+        ok = ok & (r4.x != sv) & (r4.y != sv) & (r4.z != sv) & (r4.w != sv);
+      }
       isnew = ok;
     }
     const uint64_t nmask = ballot(isnew);
@@ -978,29 +995,24 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     }
     evals += (unsigned long long)m;
     __syncthreads();
-    float kd[NC];
-    uint32_t kid[NC];
+    uint64_t key[NC];
 #pragma unroll
     for (int r = 0; r < NC; r++) {
       const int e = r * 64 + ln;
-      kd[r] = e < m ? dpos[e] : finf();
-      kid[r] = e < m ? cl[e] : kInvalid;
+      key[r] = e < m ? key64(dpos[e], cl[e]) : ~0ull;
     }
     __syncthreads();
-    wave_sort<NC>(kd, kid);
+    wave_sort64<NC>(key);
     bool valid[NC];
 #pragma unroll
     for (int r = 0; r < NC; r++) {
       valid[r] = r * 64 + ln < m;
-      spos[r * 64 + ln] = kid[r];
-      dpos[r * 64 + ln] = kd[r];
+      spos[r * 64 + ln] = (uint32_t)key[r];
+      dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
     }
     __syncthreads();
-    uint32_t sid;
-    float sdist;
-    const int nsel = greedy_u8_reg<NK, NC, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, valid, sid, sdist, evals);
-    (void)sdist;
-    if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? sid : kInvalid;
+    const int nsel = greedy_u8_reg<NK, NC, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, oid, od, valid, evals);
+    if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? oid[ln] : kInvalid;
     if (ln == 0) P.deg[u] = (uint32_t)nsel;
     prunes++;
     cand += (unsigned long long)m + 1;

@@ -28,6 +28,8 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   __shared__ uint32_t hsh[kHashSize];
   __shared__ uint32_t nid[64];
   __shared__ float nkey[64];
+  __shared__ uint32_t mid[64 * NR];
+  __shared__ float mkey[64 * NR];
   const int ln = lane();
   const uint32_t qi = blockIdx.x;
   if (qi >= a.nq) return;
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     evals += cnt;
     const float nd = ln < cnt ? nkey[ln] : finf();
     const uint32_t ni = ln < cnt ? nid[ln] : kInvalid;
-    wave_merge_new_fast<NR>(cd, ci, nd, ni, (int)a.ell);
+    wave_merge_lds<NR>(cd, ci, nd, ni, (int)a.ell, mkey, mid);
     __syncthreads();
   }
 

@@ -155,6 +155,8 @@ __device__ __forceinline__ void wave_dists(const Slice<KIND, LPV, CPL>& s, const
   constexpr int RIF = CPL >= 8 ? 1 : 8 / CPL;
   const int ln = lane(), grp = ln / LPV, sub = ln % LPV;
   for (int base = 0; base < cnt; base += G * RIF) {
+    // steps whose rows all lie beyond cnt are skipped (uniform branches)
+    const int steps = (cnt - base + G - 1) / G;
     uint4 b[RIF][CPL];
 #pragma unroll
     for (int rr = 0; rr < RIF; rr++) {
@@ -163,11 +165,12 @@ __device__ __forceinline__ void wave_dists(const Slice<KIND, LPV, CPL>& s, const
 #pragma unroll
       for (int k = 0; k < CPL; k++) {
         const int ch = sub + k * LPV;
-        b[rr][k] = (c < cnt && ch < nch) ? ld16(row + (size_t)ch * 16) : make_uint4(0, 0, 0, 0);
+        b[rr][k] = (rr < steps && c < cnt && ch < nch) ? ld16(row + (size_t)ch * 16) : make_uint4(0, 0, 0, 0);
       }
     }
 #pragma unroll
     for (int rr = 0; rr < RIF; rr++) {
+      if (rr >= steps) break;
       const int c = base + rr * G + grp;
       typename Acc<KIND>::T t = group_sum<LPV>(partial<KIND, LPV, CPL>(s, b[rr]));
       if (sub == 0 && c < cnt) out[c] = finalize<KIND>(t);

@@ -346,6 +346,140 @@ __device__ __forceinline__ void wave_merge_new_fast(float (&cd)[N], uint32_t (&c
     if (r * 64 + ln >= keep) { cd[r] = finf(); ci[r] = kInvalid; }
 }
 
+// 64-bit keys whose unsigned order is the (distance, id) order: the float's
+// bits mapped to an order-preserving unsigned integer (negative values
+// complemented, non-negative ones with the sign bit set) above the id with
+// its expanded flag masked off.
+__device__ __forceinline__ uint32_t sortable(float d) {
+  const uint32_t b = __float_as_uint(d);
+  return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+__device__ __forceinline__ uint64_t key64(float d, uint32_t id) {
+  return ((uint64_t)sortable(d) << 32) | (uint64_t)(id & kIdMask);
+}
+__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Same result as wave_merge_new_fast, with every survivor placed in one
+// pass: survivors (new keys below C's key at position keep-1) that repeat a
+// key of C are dropped; for the others, each C key counts the survivors
+// below it and each survivor the C keys and other survivors below it, which
+// gives every key its position in the merged order; keys at positions below
+// `keep` are written to the LDS scratch (ld, li: 64*N entries each) and read
+// back in order.  More than kBatchMax survivors take the sort-and-merge path.
+constexpr int kBatchMax = 32;
+template <int N>
+__device__ __forceinline__ void wave_merge_lds(float (&cd)[N], uint32_t (&ci)[N], float nd, uint32_t ni, int keep,
+                                               float *ld, uint32_t *li) {
+  const int ln = lane();
+  const int wr = (keep - 1) >> 6, wl = (keep - 1) & 63;
+  uint64_t ck[N];
+#pragma unroll
+  for (int r = 0; r < N; r++) ck[r] = key64(cd[r], ci[r]);
+  uint64_t wk = 0;
+#pragma unroll
+  for (int r = 0; r < N; r++)
+    if (r == wr) wk = rdlane64(ck[r], wl);
+  const uint64_t nk = key64(nd, ni);
+  const bool in = kvalid(ni) && nk < wk;
+  const uint64_t m = ballot(in);
+  if (!m) return;
+  if (popc(m) > kBatchMax) {
+    wave_merge_new<N>(cd, ci, in ? nd : finf(), in ? ni : kInvalid, keep);
+    return;
+  }
+  uint32_t cnt[N];
+#pragma unroll
+  for (int r = 0; r < N; r++) cnt[r] = 0;
+  uint32_t ltc = 0, rk = 0;
+  uint64_t live = 0, mm = m;
+  while (mm) {
+    const int l = ffs64(mm);
+    mm &= mm - 1;
+    const uint64_t xk = rdlane64(nk, l);
+    bool lt[N];
+    int below = 0;
+    bool dup = false;
+#pragma unroll
+    for (int r = 0; r < N; r++) {
+      lt[r] = ck[r] < xk;
+      below += popc(ballot(lt[r]));
+      dup |= ballot(ck[r] == xk) != 0;
+    }
+    if (dup) continue;
+    live |= 1ull << l;
+#pragma unroll
+    for (int r = 0; r < N; r++) cnt[r] += lt[r] ? 0u : 1u;
+    rk += xk < nk ? 1u : 0u;
+    ltc = ln == l ? (uint32_t)below : ltc;
+  }
+#pragma unroll
+  for (int r = 0; r < N; r++) {
+    const int p = r * 64 + ln + (int)cnt[r];
+    if (p < keep) { ld[p] = cd[r]; li[p] = ci[r]; }
+  }
+  if ((live >> ln) & 1) {
+    const int p = (int)(ltc + rk);
+    if (p < keep) { ld[p] = nd; li[p] = ni; }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < N; r++) {
+    const int e = r * 64 + ln;
+    const bool ok = e < keep;
+    cd[r] = ok ? ld[e] : finf();
+    ci[r] = ok ? li[e] : kInvalid;
+  }
+  __syncthreads();
+}
+
+// The float whose sortable() image is u.
+__device__ __forceinline__ float unsortable(uint32_t u) {
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+__device__ __forceinline__ uint64_t xshfl64(uint64_t v, int j) {
+  return ((uint64_t)xshfl((uint32_t)(v >> 32), j) << 32) | (uint64_t)xshfl((uint32_t)v, j);
+}
+
+// Bitonic sort, ascending, of N*64 64-bit keys held as element e = r*64 + lane
+// (one compare per exchange instead of the (distance, id) pair test).
+template <int N>
+__device__ __forceinline__ void wave_sort64(uint64_t (&k)[N]) {
+  const int ln = lane();
+#pragma unroll
+  for (int kk = 2; kk <= 64 * N; kk <<= 1) {
+#pragma unroll
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      if (j >= 64) {
+        const int jr = j >> 6;
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const int p = r ^ jr;
+          if (p > r) {
+            const bool up = ((r * 64 + ln) & kk) == 0;
+            const uint64_t a = k[r], b = k[p];
+            const bool sw = up ? (b < a) : (a < b);
+            k[r] = sw ? b : a;
+            k[p] = sw ? a : b;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const bool up = ((r * 64 + ln) & kk) == 0;
+          const bool keep_min = ((ln & j) == 0) == up;
+          const uint64_t o = xshfl64(k[r], j);
+          const bool take = keep_min ? (o < k[r]) : (k[r] < o);
+          k[r] = take ? o : k[r];
+        }
+      }
+    }
+  }
+}
+
 // Exclusive wave prefix sum of small non-negative ints.
 __device__ __forceinline__ int wave_excl_scan(int v, int& total) {
   int x = v;
