@@ -39,7 +39,8 @@ struct grand_index {
   // per-batch buffers
   uint32_t bcap = 0;
   uint32_t *b_ids = nullptr, *v_ids = nullptr, *v_n = nullptr, *c_ids = nullptr, *rcount = nullptr,
-           *rofs = nullptr;
+           *rofs = nullptr, *rchunk = nullptr, *coff = nullptr, *cmap = nullptr;
+  hipEvent_t ev_total = nullptr;  // record count of a delete batch copied to the host
   float *v_d = nullptr, *c_d = nullptr;
   uint8_t *b_vecs = nullptr;
   uint32_t c_stride = 0;
@@ -179,12 +180,15 @@ grand_status ensure_batch(grand_index *h, uint32_t n) {
   HCHK(h, hipStreamSynchronize(h->stream));
   uint32_t nc = std::max<uint32_t>(n, h->bcap + h->bcap / 2);
   dfree(h->b_ids); dfree(h->v_ids); dfree(h->v_n); dfree(h->c_ids); dfree(h->rcount); dfree(h->rofs);
-  dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs);
+  dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs); dfree(h->rchunk); dfree(h->coff); dfree(h->cmap);
   h->bcap = 0;
+  // work chunks of a delete batch: at most (in-edges of the batch) / 64 + 2 per deleted node
+  const size_t nchunk = (size_t)h->p.capacity * h->p.R / 64 + 2 * (size_t)nc + 1;
   const size_t vs = (size_t)nc * h->iters;
   if (dalloc(&h->b_ids, nc) || dalloc(&h->v_ids, vs) || dalloc(&h->v_d, vs) || dalloc(&h->v_n, nc) ||
       dalloc(&h->c_ids, (size_t)nc * h->c_stride) || dalloc(&h->c_d, (size_t)nc * h->c_stride) ||
       dalloc(&h->rcount, (size_t)nc + 1) || dalloc(&h->rofs, (size_t)nc + 1) ||
+      dalloc(&h->rchunk, (size_t)nc + 1) || dalloc(&h->coff, (size_t)nc + 1) || dalloc(&h->cmap, nchunk) ||
       dalloc(&h->b_vecs, (size_t)nc * h->stride)) {
     (void)hipGetLastError();
     return fail(h, GRAND_E_OOM, "device allocation of batch buffers failed");
@@ -432,23 +436,36 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   r.rev_by_batch = by_batch;
   r.c = h->p.c;
   r.rofs = h->rofs;
+  r.coff = h->coff;
+  r.cmap = h->cmap;
   r.ds = h->ds;
-  size_t total = 0;
-  {
-    HCHK(h, launch_repair_count(r, h->rcount, h->stream));
-    HCHK(h, launch_scan(h->rcount, h->rofs, n, h->scan_tmp, h->stream));
-    HCHK(h, hipMemcpyAsync(&h->hs->n_dirty, h->rofs + n, sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream));
-    HCHK(h, hipStreamSynchronize(h->stream));
-    total = h->hs->n_dirty;
+  // record offsets and work chunks; the record count reaches the host
+  // through an event while the repair runs, so the stream never drains
+  HCHK(h, launch_repair_plan(r, h->rcount, h->rchunk, h->stream));
+  HCHK(h, launch_scan(h->rcount, h->rofs, n, h->scan_tmp, h->stream));
+  const bool chunked = repair_chunked(h->kind, h->pool, kr, h->p.c);
+  if (chunked) {
+    HCHK(h, launch_scan(h->rchunk, h->coff, n, h->scan_tmp, h->stream));
+    HCHK(h, launch_repair_map(n, h->coff, h->cmap, h->stream));
   }
-  s = ensure_records(h, total);
-  if (s != GRAND_OK) return s;
-  {
+  HCHK(h, hipMemcpyAsync(&h->hs->n_dirty, h->rofs + n, sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream));
+  HCHK(h, hipEventRecord(h->ev_total, h->stream));
+  const uint32_t grid = chunked ? persistent_grid((size_t)h->p.capacity * h->p.R / 64 + 2 * (size_t)n) : n;
+  auto repair = [&]() -> grand_status {
     Phase ph(h, GRAND_PH_REPAIR);
     r.rec_t = h->rec_t;
     r.rec_s = h->rec_s;
     r.rec_d = h->rec_d;
-    HCHK(h, launch_repair(h->kind, h->vc, r, h->stream));
+    r.rcap = h->rcap;
+    HCHK(h, launch_repair(h->kind, h->vc, r, grid, h->stream));
+    return GRAND_OK;
+  };
+  if ((s = repair()) != GRAND_OK) return s;
+  HCHK(h, hipEventSynchronize(h->ev_total));
+  const size_t total = h->hs->n_dirty;
+  if (total > h->rcap) {  // the launch above wrote nothing: grow and repeat it
+    if ((s = ensure_records(h, total)) != GRAND_OK) return s;
+    if ((s = repair()) != GRAND_OK) return s;
   }
   s = run_group(h, total);
   if (s != GRAND_OK) return s;
@@ -512,6 +529,9 @@ void release(grand_index *h) {
   dfree(h->ds);
   if (h->hs) (void)hipHostFree(h->hs);
   h->hs = nullptr;
+  dfree(h->rchunk); dfree(h->coff); dfree(h->cmap);
+  if (h->ev_total) (void)hipEventDestroy(h->ev_total);
+  h->ev_total = nullptr;
   dfree(h->b_ids); dfree(h->v_ids); dfree(h->v_n); dfree(h->c_ids); dfree(h->rcount); dfree(h->rofs);
   dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs);
   dfree(h->rec_t); dfree(h->rec_s); dfree(h->rec_d); dfree(h->gsrc); dfree(h->gd);
@@ -603,7 +623,8 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
                                   dalloc(&h->rev.bo2, rev_fine_words(h->rev.plan)))) ||
              dalloc(&h->ds, 1) ||
              hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
-             hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess;
+             hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess ||
+             hipEventCreateWithFlags(&h->ev_total, hipEventDisableTiming) != hipSuccess;
   if (bad) {
     (void)hipGetLastError();
     release(h);

@@ -135,6 +135,9 @@ struct RepairArgs {
   int rev_by_batch;           // reverse rows indexed by batch position (1) or by id (0)
   uint32_t c;
   const uint32_t *rofs;       // record offsets per deleted node (n + 1)
+  const uint32_t *coff;       // work-chunk offsets per deleted node (n + 1)
+  const uint32_t *cmap;       // deleted node of every work chunk
+  size_t rcap;                // record capacity: nothing is written when rofs[n] exceeds it
   uint32_t *rec_t, *rec_s;
   float *rec_d;
   DevScalars *ds;
@@ -164,8 +167,10 @@ hipError_t launch_bootstrap(int kind, int vc, const BootArgs &a, hipStream_t s);
 hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPruneArgs &a, hipStream_t s);
 hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const RebuildArgs &a, uint32_t grid,
                           hipStream_t s);
-hipError_t launch_repair(int kind, int vc, const RepairArgs &a, hipStream_t s);
-hipError_t launch_repair_count(const RepairArgs &a, uint32_t *counts, hipStream_t s);
+hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t s);
+hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s);
+hipError_t launch_repair_map(uint32_t n, const uint32_t *coff, uint32_t *cmap, hipStream_t s);
+bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c);
 
 hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s);
 hipError_t launch_fill_u8(uint8_t *p, uint8_t v, size_t n, hipStream_t s);

@@ -1,6 +1,6 @@
 // k_repair.hip -- in-place delete repair of GrAND-Vamana (Alg. 6).
 //
-// For every deleted p_i (one wavefront each):
+// For every deleted p_i:
 //   in-neighbour repair : every z in N_in(p_i) outside the batch (exact, from
 //     the reverse graph) gets the c points of C_i closest to z as scratch
 //     records (z, y, Dist(z, y)), plus a marker record that makes z dirty
@@ -9,8 +9,14 @@
 //     to the scratch of the c points y of C_i closest to w: records
 //     (y, w, Dist(w, y)).
 // C_i is the first k_repair keys of the search from x_{p_i} outside the
-// batch.  Records go to fixed offsets (a prefix sum of per-node counts), so
-// no atomics are needed and the layout is deterministic.
+// batch.
+//
+// Record layout (fixed, so every piece of work knows where its records go
+// without a prefix over filtered neighbours): deleted node i owns
+// nin_i*(c+1) + R*c records from rofs[i]; in-neighbour e (in reverse-row
+// order) owns c+1 of them, out-slot t of N_out(p_i) owns c.  Neighbours in
+// the batch, empty slots and missing points give records whose target is
+// INVALID, which the grouping skips.
 #include "dispatch.h"
 
 namespace gr {
@@ -21,29 +27,34 @@ __device__ __forceinline__ void rev_row(const RepairArgs &a, uint32_t i, uint32_
   b1 = a.rev_off[r + 1];
 }
 
-// Records per deleted node, one wavefront each: (c + 1) per in-neighbour
-// and c per out-neighbour outside the batch.
-__global__ __launch_bounds__(64) void k_repair_count(RepairArgs a, uint32_t *counts) {
-  const uint32_t i = blockIdx.x;
+// Per deleted node: its record count and its work chunks (64 in-neighbours
+// each, plus one chunk for the out-slots).
+__global__ void k_repair_plan(RepairArgs a, uint32_t *counts, uint32_t *chunks) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
-  const int ln = lane();
-  const uint32_t p = a.ids[i];
   uint32_t b0, b1;
-  rev_row(a, i, p, b0, b1);
-  uint32_t nin = 0;
-  for (uint32_t base = b0; base < b1; base += 64) {
-    const uint32_t j = base + ln;
-    const uint32_t z = j < b1 ? a.rev_src[j] : kInvalid;
-    nin += (uint32_t)popc(ballot(z != kInvalid && !a.in_batch[z]));
-  }
-  const uint32_t w = ln < (int)a.pool.R ? a.pool.adj[(size_t)p * a.pool.R + ln] : kInvalid;
-  const uint32_t nout = (uint32_t)popc(ballot(w != kInvalid && !a.in_batch[w]));
-  if (ln == 0) counts[i] = nin * (a.c + 1) + nout * a.c;
+  rev_row(a, i, a.ids[i], b0, b1);
+  const uint32_t nin = b1 - b0;
+  counts[i] = nin * (a.c + 1) + a.pool.R * a.c;
+  chunks[i] = (nin + 63) / 64 + 1;
 }
 
-hipError_t launch_repair_count(const RepairArgs &a, uint32_t *counts, hipStream_t s) {
+// cmap[coff[i] + j] = i for every chunk j of deleted node i (one wave each).
+__global__ void k_repair_map(uint32_t n, const uint32_t *coff, uint32_t *cmap) {
+  const uint32_t i = blockIdx.x;
+  if (i >= n) return;
+  const uint32_t c0 = coff[i], c1 = coff[i + 1];
+  for (uint32_t q = c0 + threadIdx.x; q < c1; q += blockDim.x) cmap[q] = i;
+}
+
+hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_repair_count, dim3(a.n), dim3(64), 0, s, a, counts);
+  hipLaunchKernelGGL(k_repair_plan, dim3((a.n + 255) / 256), dim3(256), 0, s, a, counts, chunks);
+  return hipGetLastError();
+}
+hipError_t launch_repair_map(uint32_t n, const uint32_t *coff, uint32_t *cmap, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_repair_map, dim3(n), dim3(64), 0, s, n, coff, cmap);
   return hipGetLastError();
 }
 
@@ -72,258 +83,273 @@ __device__ __forceinline__ void closest_c(const RepairArgs &a, uint32_t cv, uint
   oi = id[0];
 }
 
+// One wavefront per deleted node, any element type: each neighbour's c
+// closest points of C_i come from a gather and a sort of its distances.
 template <int KIND, int LPV, int CPL>
 __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
   __shared__ uint32_t lst[64];
   __shared__ float ldist[64];
   const int ln = lane();
   const uint32_t i = blockIdx.x;
-  if (i >= a.n) return;
+  if (i >= a.n || (size_t)a.rofs[a.n] > a.rcap) return;
   const PoolView &P = a.pool;
   const uint32_t p = a.ids[i];
+  const uint32_t c = a.c;
   const uint32_t cv = ln < (int)a.kr ? a.ci[(size_t)i * a.kr + ln] : kInvalid;
-  uint32_t r = a.rofs[i];
-  unsigned long long evals = 0, rows = popc(ballot(kvalid(cv)));
+  unsigned long long evals = 0, rows = popc(ballot(kvalid(cv))), recs = 0;
   uint32_t b0, b1;
   rev_row(a, i, p, b0, b1);
-  for (uint32_t j = b0; j < b1; j++) {
-    const uint32_t z = a.rev_src[j];
-    if (a.in_batch[z]) continue;
+  const uint32_t r0 = a.rofs[i];
+  for (uint32_t e = 0; e < b1 - b0; e++) {
+    const uint32_t z = a.rev_src[b0 + e];
+    const uint32_t base = r0 + e * (c + 1);
+    if (z == kInvalid || a.in_batch[z]) {
+      for (uint32_t k = ln; k <= c; k += 64) a.rec_t[base + k] = kInvalid;
+      continue;
+    }
     float od;
     uint32_t oi;
     closest_c<KIND, LPV, CPL>(a, cv, z, lst, ldist, od, oi, evals);
     rows++;
-    if (ln < (int)a.c) {
-      a.rec_t[r + ln] = z;
-      a.rec_s[r + ln] = oi;
-      a.rec_d[r + ln] = kvalid(oi) ? od : 0.0f;
+    recs += c + 1;
+    if (ln < (int)c) {
+      a.rec_t[base + ln] = z;
+      a.rec_s[base + ln] = oi;
+      a.rec_d[base + ln] = kvalid(oi) ? od : 0.0f;
     }
     if (ln == 0) {
-      a.rec_t[r + a.c] = z;
-      a.rec_s[r + a.c] = kInvalid;
-      a.rec_d[r + a.c] = 0.0f;
+      a.rec_t[base + c] = z;
+      a.rec_s[base + c] = kInvalid;
+      a.rec_d[base + c] = 0.0f;
     }
-    r += a.c + 1;
   }
+  const uint32_t ro = r0 + (b1 - b0) * (c + 1);
   for (uint32_t t = 0; t < P.R; t++) {
     const uint32_t w = P.adj[(size_t)p * P.R + t];
-    if (w == kInvalid || a.in_batch[w]) continue;
+    const uint32_t base = ro + t * c;
+    if (w == kInvalid || a.in_batch[w]) {
+      for (uint32_t k = ln; k < c; k += 64) a.rec_t[base + k] = kInvalid;
+      continue;
+    }
     float od;
     uint32_t oi;
     closest_c<KIND, LPV, CPL>(a, cv, w, lst, ldist, od, oi, evals);
     rows++;
-    if (ln < (int)a.c) {
-      const bool v = kvalid(oi);
-      a.rec_t[r + ln] = v ? oi : kInvalid;
-      a.rec_s[r + ln] = v ? w : kInvalid;
-      a.rec_d[r + ln] = v ? od : 0.0f;
+    const bool v = kvalid(oi);
+    recs += (unsigned long long)popc(ballot(ln < (int)c && v));
+    if (ln < (int)c) {
+      a.rec_t[base + ln] = v ? oi : kInvalid;
+      a.rec_s[base + ln] = v ? w : kInvalid;
+      a.rec_d[base + ln] = v ? od : 0.0f;
     }
-    r += a.c;
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->records, (unsigned long long)(r - a.rofs[i]));
+    atomicAdd(&a.ds->records, recs);
     atomicAdd(&a.ds->rep_evals, evals);
     atomicAdd(&a.ds->rep_rows, rows);
-    atomicAdd(&a.ds->rep_recs, (unsigned long long)(r - a.rofs[i]));
+    atomicAdd(&a.ds->rep_recs, recs);
   }
 }
 
 // ---------------------------------------------------------------------------
 // uint8 repair on the matrix cores, for rows of 64*NK bytes, k_repair <= 64
-// and c <= K.  The "c closest points of C_i" of every repaired neighbour x
-// are rows of one distance matrix {x} x C_i, so C_i (at most 4 tiles of 16
-// candidates) is held in registers in the MFMA operand layout, the
-// neighbours are taken 16 at a time as the other operand, and each
-// 16 x 16 MFMA tile gives exact int32 distances (x ^ 0x80 operands).  Each
-// lane keeps, for the 4 output rows it holds, the K smallest (distance, id)
-// keys of its candidate column; the lists of the 16 lanes of a row are
-// merged by a butterfly.  Records and their offsets are those of k_repair.
+// and c <= K.  The c closest points of C_i of each repaired neighbour x are
+// found in one distance block {neighbours} x C_i (exact int32 from int8
+// MFMA on x ^ 0x80).  Work is split in chunks of at most 64 neighbours of
+// one deleted node (persistent waves over the chunk list), so a node with
+// a long in-neighbour list is spread over many waves.  Per chunk the C_i
+// tiles are the MFMA A operand and 16 neighbours at a time the B operand:
+// lane (g, col) then holds 16 candidate distances of neighbour col, keeps
+// its K smallest (distance, id) keys, and the four lanes of a neighbour
+// merge their lists (two exchanges).
 
-// Sorted list of the K smallest keys: inserts (d, id).
+// Sorted list of the K smallest 64-bit keys.
 template <int K>
-__device__ __forceinline__ void kl_insert(float (&ld)[K], uint32_t (&li)[K], float d, uint32_t id) {
-  bool lt[K];
+__device__ __forceinline__ void kl_insert64(uint64_t (&l)[K], uint64_t k) {
 #pragma unroll
-  for (int j = 0; j < K; j++) lt[j] = kless(d, id, ld[j], li[j]);
-#pragma unroll
-  for (int j = K - 1; j >= 0; j--) {
-    const bool shift = j > 0 && lt[j > 0 ? j - 1 : 0];
-    const float pd = ld[j > 0 ? j - 1 : 0];
-    const uint32_t pi = li[j > 0 ? j - 1 : 0];
-    ld[j] = shift ? pd : (lt[j] ? d : ld[j]);
-    li[j] = shift ? pi : (lt[j] ? id : li[j]);
+  for (int j = 0; j < K; j++) {
+    const uint64_t lo = k < l[j] ? k : l[j];
+    k = k < l[j] ? l[j] : k;
+    l[j] = lo;
   }
+}
+// l <- the K smallest of the two sorted lists l and o (bitonic merge).
+template <int K>
+__device__ __forceinline__ void kl_merge64(uint64_t (&l)[K], const uint64_t (&o)[K]) {
+#pragma unroll
+  for (int j = 0; j < K; j++) l[j] = o[K - 1 - j] < l[j] ? o[K - 1 - j] : l[j];
+#pragma unroll
+  for (int d = K / 2; d > 0; d >>= 1)
+#pragma unroll
+    for (int j = 0; j < K; j++)
+      if ((j & d) == 0) {
+        const uint64_t x = l[j], y = l[j + d];
+        l[j] = x < y ? x : y;
+        l[j + d] = x < y ? y : x;
+      }
 }
 
 template <int NK, int K>
 __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
-  constexpr int NT = 4;
-  __shared__ uint32_t xl[64];
+  constexpr int NT = 4;  // C_i tiles (k_repair <= 64)
+  __shared__ uint32_t cidL[64];
+  __shared__ int cnrL[64];
   const int ln = lane(), g = ln >> 4, col = ln & 15;
-  const uint32_t i = blockIdx.x;
-  if (i >= a.n) return;
   const PoolView &P = a.pool;
-  const uint32_t p = a.ids[i];
+  const uint32_t R = P.R;
   const size_t goff = (size_t)g * 16;
   const int kr = (int)a.kr, nt = (kr + 15) >> 4;
-  const int c = (int)a.c;
-  v4i B[NT][NK];
-  int nrmC[NT];
-  uint32_t cid[NT];
-  unsigned long long rows = 0;
+  const uint32_t c = a.c;
+  if ((size_t)a.rofs[a.n] > a.rcap) return;  // the host grows the buffers and launches again
+  const uint32_t total = a.coff[a.n];
+  unsigned long long evals = 0, rows = 0, recs = 0;
+  for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
+    const uint32_t i = a.cmap[q];
+    const uint32_t j = q - a.coff[i];
+    const uint32_t p = a.ids[i];
+    uint32_t b0, b1;
+    rev_row(a, i, p, b0, b1);
+    const uint32_t nin = b1 - b0, nci = (nin + 63) / 64;
+    const bool inbound = j < nci;
+    // this chunk's neighbours, lane e holding neighbour e
+    int cnt;
+    uint32_t x, rbase;
+    if (inbound) {
+      const uint32_t e0 = j * 64;
+      cnt = (int)min(64u, nin - e0);
+      x = ln < cnt ? a.rev_src[b0 + e0 + ln] : kInvalid;
+      rbase = a.rofs[i] + e0 * (c + 1);
+    } else {
+      cnt = (int)R;
+      x = ln < cnt ? P.adj[(size_t)p * R + ln] : kInvalid;
+      rbase = a.rofs[i] + nin * (c + 1);
+    }
+    const bool xok = x != kInvalid && !a.in_batch[x];
+    // C_i tiles (A operand: candidate 16t + col, bytes 16g + 64kk)
+    v4i Ct[NT][NK];
 #pragma unroll
-  for (int t = 0; t < NT; t++) {
-    cid[t] = kInvalid;
-    nrmC[t] = 0;
-    if (t < nt) {
+    for (int t = 0; t < NT; t++) {
       const int e = 16 * t + col;
-      const uint32_t cv = e < kr ? a.ci[(size_t)i * kr + e] : kInvalid;
-      cid[t] = cv;
+      const uint32_t cv = (t < nt && e < kr) ? a.ci[(size_t)i * kr + e] : kInvalid;
       const uint8_t *row = P.vecs + (size_t)(kvalid(cv) ? cv : p) * P.stride + goff;
       int sq = 0;
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) {
-        B[t][kk] = to_i8x16(ld16(row + (size_t)kk * 64));
-        sq = sq_i8x16(B[t][kk], sq);
+        Ct[t][kk] = t < nt ? to_i8x16(ld16(row + (size_t)kk * 64)) : v4i{0, 0, 0, 0};
+        sq = sq_i8x16(Ct[t][kk], sq);
       }
       sq += (int)xshfl((uint32_t)sq, 16);
       sq += (int)xshfl((uint32_t)sq, 32);
-      nrmC[t] = sq;
+      if (g == 0) {
+        cidL[e] = cv;
+        cnrL[e] = sq;
+      }
     }
-    rows += (unsigned long long)popc(ballot(g == 0 && kvalid(cid[t])));
-  }
-  const uint32_t r0 = a.rofs[i];
-  uint32_t r = r0;
-  uint32_t evals = 0;
-  // xl[0..cnt): neighbours; inbound: in-neighbours z (records to z plus a
-  // marker), else out-neighbours w (records to the chosen points)
-  auto process = [&](int cnt, bool inbound) {
-    for (int q = 0; q < cnt; q += 16) {
-      const int e = q + col;
-      const uint32_t x = xl[e < cnt ? e : q];
-      const uint8_t *row = P.vecs + (size_t)x * P.stride + goff;
-      v4i A[NK];
-      int na = 0;
+    __syncthreads();
+    if (j == 0) rows += (unsigned long long)popc(ballot(ln < kr && kvalid(cidL[ln])));
+    rows += (unsigned long long)popc(ballot(xok));
+    for (int s = 0; 16 * s < cnt; s++) {
+      // neighbours 16s .. 16s+15 as the B operand
+      const uint32_t xs = __shfl(x, 16 * s + col, 64);
+      const bool xsok = __shfl((int)xok, 16 * s + col, 64) != 0;
+      const uint8_t *row = P.vecs + (size_t)(xsok ? xs : p) * P.stride + goff;
+      v4i X[NK];
+      int nx = 0;
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) {
-        A[kk] = to_i8x16(ld16(row + (size_t)kk * 64));
-        na = sq_i8x16(A[kk], na);
+        X[kk] = to_i8x16(ld16(row + (size_t)kk * 64));
+        nx = sq_i8x16(X[kk], nx);
       }
-      na += (int)xshfl((uint32_t)na, 16);
-      na += (int)xshfl((uint32_t)na, 32);
-      int rn[4];
-      uint32_t rx[4];
+      nx += (int)xshfl((uint32_t)nx, 16);
+      nx += (int)xshfl((uint32_t)nx, 32);
+      uint64_t l[K];
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) {
-        const int xe = q + 4 * g + ii;
-        rn[ii] = __shfl(na, 4 * g + ii, 64);
-        rx[ii] = xe < cnt ? xl[xe] : kInvalid;
-      }
-      float ld[4][K];
-      uint32_t li[4][K];
-#pragma unroll
-      for (int ii = 0; ii < 4; ii++)
-#pragma unroll
-        for (int j = 0; j < K; j++) { ld[ii][j] = finf(); li[ii][j] = kInvalid; }
+      for (int k = 0; k < K; k++) l[k] = ~0ull;
 #pragma unroll
       for (int t = 0; t < NT; t++) {
-        if (t >= nt) continue;
+        if (t >= nt) break;
         v4i acc = {0, 0, 0, 0};
 #pragma unroll
-        for (int kk = 0; kk < NK; kk++) acc = mfma_i8(A[kk], B[t][kk], acc);
+        for (int kk = 0; kk < NK; kk++) acc = mfma_i8(Ct[t][kk], X[kk], acc);
 #pragma unroll
         for (int ii = 0; ii < 4; ii++) {
-          const bool ok = kvalid(cid[t]) && kvalid(rx[ii]) && cid[t] != rx[ii];
-          const float d = canon0((float)(rn[ii] + nrmC[t] - 2 * acc[ii]));
+          const int e = 16 * t + 4 * g + ii;
+          const uint32_t cv = cidL[e];
+          const bool ok = xsok && kvalid(cv) && cv != xs;
+          const uint32_t d = (uint32_t)(cnrL[e] + nx - 2 * acc[ii]);
           evals += ok ? 1u : 0u;
-          kl_insert<K>(ld[ii], li[ii], ok ? d : finf(), ok ? cid[t] : kInvalid);
+          kl_insert64<K>(l, ok ? (((uint64_t)d << 32) | cv) : ~0ull);
         }
       }
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1)
+      for (int o = 16; o < 64; o <<= 1) {
+        uint64_t ot[K];
 #pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          float od[K];
-          uint32_t oi[K];
+        for (int k = 0; k < K; k++) ot[k] = xshfl64(l[k], o);
+        kl_merge64<K>(l, ot);
+      }
+      // records of neighbour 16s + col: lane g writes entries g, g+4, ...
+      const int e = 16 * s + col;
+      if (e < cnt) {
+        const uint32_t nrec = inbound ? c + 1 : c;
+        const uint32_t base = rbase + (uint32_t)e * nrec;
+        for (uint32_t k = (uint32_t)g; k < nrec; k += 4) {
+          uint64_t key = ~0ull;
 #pragma unroll
-          for (int j = 0; j < K; j++) { od[j] = xshfl(ld[ii][j], o); oi[j] = xshfl(li[ii][j], o); }
-#pragma unroll
-          for (int j = 0; j < K; j++) kl_insert<K>(ld[ii], li[ii], od[j], oi[j]);
-        }
-#pragma unroll
-      for (int ii = 0; ii < 4; ii++) {
-        const int xe = q + 4 * g + ii;
-        if (xe >= cnt) continue;
-        const uint32_t xid = rx[ii];
-        float yd = finf();
-        uint32_t yi = kInvalid;
-#pragma unroll
-        for (int j = 0; j < K; j++)
-          if (j == col) { yd = ld[ii][j]; yi = li[ii][j]; }
-        const bool v = kvalid(yi);
-        if (inbound) {
-          const uint32_t base = r + (uint32_t)xe * (uint32_t)(c + 1);
-          if (col < c) {
-            a.rec_t[base + col] = xid;
-            a.rec_s[base + col] = yi;
-            a.rec_d[base + col] = v ? yd : 0.0f;
-          } else if (col == c) {
-            a.rec_t[base + c] = xid;
-            a.rec_s[base + c] = kInvalid;
-            a.rec_d[base + c] = 0.0f;
+          for (int kk = 0; kk < K; kk++)
+            if ((uint32_t)kk == k) key = l[kk];
+          const bool v = key != ~0ull;
+          const uint32_t yi = v ? (uint32_t)key : kInvalid;
+          const float yd = v ? (float)(uint32_t)(key >> 32) : 0.0f;
+          if (!xsok) {
+            a.rec_t[base + k] = kInvalid;
+          } else if (inbound) {
+            const bool marker = k == c;
+            a.rec_t[base + k] = xs;
+            a.rec_s[base + k] = marker ? kInvalid : yi;
+            a.rec_d[base + k] = marker ? 0.0f : yd;
+            recs++;
+          } else {
+            a.rec_t[base + k] = yi;
+            a.rec_s[base + k] = v ? xs : kInvalid;
+            a.rec_d[base + k] = yd;
+            recs += v ? 1u : 0u;
           }
-        } else if (col < c) {
-          const uint32_t base = r + (uint32_t)xe * (uint32_t)c;
-          a.rec_t[base + col] = v ? yi : kInvalid;
-          a.rec_s[base + col] = v ? xid : kInvalid;
-          a.rec_d[base + col] = v ? yd : 0.0f;
         }
       }
     }
-    r += (uint32_t)cnt * (uint32_t)(inbound ? c + 1 : c);
-    rows += (unsigned long long)cnt;
-  };
-  uint32_t b0, b1;
-  rev_row(a, i, p, b0, b1);
-  for (uint32_t base = b0; base < b1; base += 64) {
-    const uint32_t j = base + ln;
-    const uint32_t z = j < b1 ? a.rev_src[j] : kInvalid;
-    const bool ok = z != kInvalid && !a.in_batch[z];
-    const uint64_t m = ballot(ok);
     __syncthreads();
-    if (ok) xl[mbcnt(m)] = z;
-    __syncthreads();
-    if (m) process(popc(m), true);
   }
-  {
-    const uint32_t w = ln < (int)P.R ? P.adj[(size_t)p * P.R + ln] : kInvalid;
-    const bool ok = w != kInvalid && !a.in_batch[w];
-    const uint64_t m = ballot(ok);
-    __syncthreads();
-    if (ok) xl[mbcnt(m)] = w;
-    __syncthreads();
-    if (m) process(popc(m), false);
-  }
-  unsigned long long ev = evals;
+  unsigned long long ev = evals, rc = recs;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) ev += __shfl_xor(ev, o, 64);
-  if (ln == 0) {
-    atomicAdd(&a.ds->records, (unsigned long long)(r - r0));
+  for (int o = 32; o > 0; o >>= 1) {
+    ev += __shfl_xor(ev, o, 64);
+    rc += __shfl_xor(rc, o, 64);
+  }
+  if (ln == 0 && (ev | rc | rows)) {
+    atomicAdd(&a.ds->records, rc);
     atomicAdd(&a.ds->rep_evals, ev);
     atomicAdd(&a.ds->rep_rows, rows);
-    atomicAdd(&a.ds->rep_recs, (unsigned long long)(r - r0));
+    atomicAdd(&a.ds->rep_recs, rc);
   }
 }
 
-hipError_t launch_repair(int kind, int vc, const RepairArgs &a, hipStream_t st) {
+// The matrix-core form serves uint8 rows of 64 or 128 bytes with R <= 64,
+// k_repair <= 64 and c <= 4, over the chunk list; every other configuration
+// takes one wave per deleted node.
+bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c) {
+  return kind == kU8L2 && kr <= 64 && c <= 4 && p.R <= 64 && (p.nch == 4 || p.nch == 8);
+}
+
+hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  if (kind == kU8L2 && a.kr <= 64 && a.c <= 4 && (a.pool.nch == 4 || a.pool.nch == 8)) {
+  if (repair_chunked(kind, a.pool, a.kr, a.c)) {
     if (a.pool.nch == 8) {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(a.n), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(a.n), dim3(64), 0, st, a);
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(grid), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(grid), dim3(64), 0, st, a);
     } else {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(a.n), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(a.n), dim3(64), 0, st, a);
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(grid), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(grid), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }
