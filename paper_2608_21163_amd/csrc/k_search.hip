@@ -5,7 +5,8 @@
 //   C : the l closest (distance, id) keys seen so far, ascending, held in
 //       registers as NR rows of 64 keys (element e = row*64 + lane); the top
 //       id bit marks keys already expanded (the set V).
-//   a lossy hash of ids whose distance was already evaluated, in LDS.  An
+//   a lossy hash of ids whose distance was already evaluated, in LDS (16-bit
+//       tags when the pool allows, so more waves fit per CU).  An
 //       evaluated id either is in C or can never enter it again (the l-th
 //       key only decreases once C is full), so skipping it is exact; the
 //       hash may forget ids (they are then evaluated again and dropped by
@@ -21,11 +22,31 @@ namespace gr {
 constexpr int kHashBits = 11;
 constexpr int kHashSize = 1 << kHashBits;
 
-__device__ __forceinline__ uint32_t hslot(uint32_t v) { return (v * 0x9E3779B1u) >> (32 - kHashBits); }
+// Hash of evaluated ids.  With 16-bit entries an id v is split into a tag
+// (v >> kHashBits) and a slot ((v ^ tag * odd) & mask); tag and slot
+// together determine v, so a stored tag matching the probe's tag is an exact
+// hit.  The tag 0xFFFF marks an empty slot, so this form needs ids below
+// 0xFFFF << kHashBits; larger pools store whole 32-bit ids at a
+// multiplicative hash slot.
+template <class HW> struct IdHash;
+template <> struct IdHash<uint16_t> {
+  static __device__ __forceinline__ uint32_t slot(uint32_t v) {
+    return (v ^ ((v >> kHashBits) * 40503u)) & (kHashSize - 1);
+  }
+  static __device__ __forceinline__ uint16_t word(uint32_t v) { return (uint16_t)(v >> kHashBits); }
+  static constexpr uint16_t kEmpty = 0xFFFFu;
+};
+template <> struct IdHash<uint32_t> {
+  static __device__ __forceinline__ uint32_t slot(uint32_t v) { return (v * 0x9E3779B1u) >> (32 - kHashBits); }
+  static __device__ __forceinline__ uint32_t word(uint32_t v) { return v; }
+  static constexpr uint32_t kEmpty = kInvalid;
+};
+bool hash16_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFFFu << kHashBits); }
 
-template <int KIND, int LPV, int CPL, int NR>
+template <int KIND, int LPV, int CPL, int NR, class HW>
 __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
-  __shared__ uint32_t hsh[kHashSize];
+  typedef IdHash<HW> H;
+  __shared__ HW hsh[kHashSize];
   __shared__ uint32_t nid[64];
   __shared__ float nkey[64];
   __shared__ uint32_t mid[64 * NR];
@@ -37,7 +58,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   const uint8_t *qrow = a.qids ? P.vecs + (size_t)a.qids[qi] * P.stride : a.qbase + (size_t)qi * P.stride;
   Slice<KIND, LPV, CPL> s;
   load_slice<KIND, LPV, CPL>(s, qrow, P.nch);
-  for (int i = ln; i < kHashSize; i += 64) hsh[i] = kInvalid;
+  for (int i = ln; i < kHashSize; i += 64) hsh[i] = H::kEmpty;
 
   float cd[NR];
   uint32_t ci[NR];
@@ -48,7 +69,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     if (ln == 0) { cd[0] = d0; ci[0] = a.start; }
   }
   __syncthreads();
-  if (ln == 0) hsh[hslot(a.start)] = a.start;
+  if (ln == 0 && a.start < P.cap) hsh[H::slot(a.start)] = H::word(a.start);
   __syncthreads();
   uint32_t nv = 0, evals = 1;
 
@@ -78,10 +99,11 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     nv++;
     // C <- C u N_out(u), skipping ids already evaluated
     const uint32_t v = ln < (int)P.R ? P.adj[(size_t)u * P.R + ln] : kInvalid;
-    const uint32_t hs = hslot(v);
-    bool need = v != kInvalid && hsh[hs] != v;
+    const uint32_t hs = H::slot(v);
+    const HW hw = H::word(v);
+    bool need = v != kInvalid && hsh[hs] != hw;
     __syncthreads();
-    if (need) hsh[hs] = v;
+    if (need) hsh[hs] = hw;
     const uint64_t m = ballot(need);
     const int cnt = popc(m);
     if (cnt == 0) continue;
@@ -176,8 +198,10 @@ int vec_class(int nch) {
 
 hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
+  const bool h16 = hash16_ok(a.pool.cap);
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.ell, {
-    hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR>), dim3(a.nq), dim3(64), 0, st, a);
+    if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t>), dim3(a.nq), dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint32_t>), dim3(a.nq), dim3(64), 0, st, a);
     return hipGetLastError();
   }));
   return hipErrorInvalidValue;
