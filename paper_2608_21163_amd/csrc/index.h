@@ -205,6 +205,7 @@ struct RevPlan {
   // each coarse bucket
   int two, s1, s2;
   uint32_t nb1, nsub, nc2;
+  int rshift;      // log2 R when R is a power of two, else -1 (row of an edge index)
 };
 RevPlan rev_plan(uint32_t cap, uint32_t R);
 size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R);  // u32 words of each pair buffer

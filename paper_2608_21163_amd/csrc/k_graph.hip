@@ -395,7 +395,7 @@ __global__ void k_rev_hist(PoolView P, int by_batch, const uint8_t *in_batch, co
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
     const uint32_t v = P.adj[i];
     if (v == kInvalid) continue;
-    const uint32_t u = (uint32_t)(i / P.R);
+    const uint32_t u = (P.R & (P.R - 1)) == 0 ? (uint32_t)(i >> (__ffs(P.R) - 1)) : (uint32_t)(i / P.R);
     if (!P.active[u]) continue;
     if (by_batch) {
       if (in_batch[v]) atomicAdd(&cnt[bidx[v]], 1u);
@@ -410,7 +410,7 @@ __global__ void k_rev_scatter(PoolView P, int by_batch, const uint8_t *in_batch,
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
     const uint32_t v = P.adj[i];
     if (v == kInvalid) continue;
-    const uint32_t u = (uint32_t)(i / P.R);
+    const uint32_t u = (P.R & (P.R - 1)) == 0 ? (uint32_t)(i >> (__ffs(P.R) - 1)) : (uint32_t)(i / P.R);
     if (!P.active[u]) continue;
     uint32_t row;
     if (by_batch) {
@@ -440,12 +440,12 @@ constexpr int kRevThreads = 256;
 constexpr uint32_t kRevMaxBuckets = 16384;  // LDS counters of steps 1 and 3 (64 KB)
 constexpr int kRevMinShift = 8, kRevMaxShift = 13;  // bucket width 256 .. 8192 targets
 constexpr uint32_t kRev2Coarse = 256;      // coarse buckets (two-level form)
-constexpr int kRev2FineShift = 7;          // fine buckets of 128 targets
+constexpr int kRev2FineShift = 6;          // fine buckets of 64 targets
 constexpr uint32_t kRev2FineChunks = 16;   // chunks per coarse bucket
 constexpr uint32_t kRev2MaxSub = 256;      // fine buckets per coarse bucket
 constexpr int kRev2Per = 16;               // edges per thread per local-sort step
 constexpr int kRev2Step = kRevThreads * kRev2Per;  // edges per local-sort step
-constexpr uint32_t kRev2Stage = 12288;     // sources a fine bucket stages in LDS (48 KB)
+constexpr uint32_t kRev2Stage = 6144;      // sources a fine bucket stages in LDS (24 KB)
 
 RevPlan rev_plan(uint32_t cap, uint32_t R) {
   RevPlan p{};
@@ -457,7 +457,8 @@ RevPlan rev_plan(uint32_t cap, uint32_t R) {
   p.ch = (cap + p.ng - 1) / p.ng;
   const int idbits = cap > 1 ? 32 - __builtin_clz(cap - 1) : 1;
   p.packed = idbits + s <= 32;
-  p.ok = cap > 0 && p.nb <= kRevMaxBuckets && (uint64_t)cap * R < (1ull << 32);
+  // 32-bit edge indices, with headroom for the loop strides
+  p.ok = cap > 0 && p.nb <= kRevMaxBuckets && (uint64_t)cap * R + (1u << 20) < (1ull << 32);
   // two-level form: at most kRev2Coarse coarse buckets, fine buckets of
   // 2^kRev2FineShift targets, both partitions packed into 32 bits
   int s1 = kRev2FineShift + 1;
@@ -468,6 +469,11 @@ RevPlan rev_plan(uint32_t cap, uint32_t R) {
   p.nsub = 1u << (s1 - p.s2);
   p.nc2 = kRev2FineChunks;
   p.two = p.ok && idbits + s1 <= 32 && p.nsub <= kRev2MaxSub;
+  p.rshift = (R & (R - 1)) == 0 ? __builtin_ctz(R) : -1;
+  if (p.two) {  // more, smaller source chunks: more workgroups in flight
+    p.ng = std::max<uint32_t>(1, std::min<uint32_t>(4096, cap / 64));
+    p.ch = (cap + p.ng - 1) / p.ng;
+  }
   return p;
 }
 size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R) {
@@ -475,27 +481,32 @@ size_t rev_pair_words(const RevPlan &rp, uint32_t cap, uint32_t R) {
 }
 size_t rev_bucket_words(const RevPlan &rp) {
   if (!rp.ok) return 0;
-  return std::max((size_t)rp.nb * rp.ng, (size_t)rp.nb1 * rp.ng) + 1;
+  return (rp.two ? (size_t)rp.nb1 * rp.ng : (size_t)rp.nb * rp.ng) + 1;
 }
 size_t rev_fine_words(const RevPlan &rp) { return rp.two ? (size_t)rp.nb1 * rp.nsub * rp.nc2 + 1 : 0; }
+
+// Row of edge index i (the bucketed build requires cap * R < 2^32).
+__device__ __forceinline__ uint32_t edge_row(const RevPlan &rp, uint32_t i, uint32_t R) {
+  return rp.rshift >= 0 ? i >> rp.rshift : i / R;
+}
 
 // Edges of chunk blockIdx.x, four loads in flight per thread; f(u, v) for
 // every edge u -> v of an active row.
 template <class F>
 __device__ __forceinline__ void for_chunk_edges(const PoolView &P, const RevPlan &rp, F f) {
-  const size_t r0 = (size_t)blockIdx.x * rp.ch;
-  const size_t r1 = std::min<size_t>(P.cap, r0 + rp.ch);
+  const uint32_t r0 = blockIdx.x * rp.ch;
+  const uint32_t r1 = std::min<uint32_t>(P.cap, r0 + rp.ch);
   if (r0 >= r1) return;
-  const size_t e0 = r0 * P.R, e1 = r1 * P.R;
-  const size_t step = (size_t)blockDim.x;
-  for (size_t i = e0 + threadIdx.x; i < e1; i += 4 * step) {
+  const uint32_t e0 = r0 * P.R, e1 = r1 * P.R;
+  const uint32_t step = blockDim.x;
+  for (uint32_t i = e0 + threadIdx.x; i < e1; i += 4 * step) {
     uint32_t v[4];
 #pragma unroll
     for (int k = 0; k < 4; k++) v[k] = i + k * step < e1 ? P.adj[i + k * step] : kInvalid;
 #pragma unroll
     for (int k = 0; k < 4; k++) {
       if (v[k] == kInvalid) continue;
-      const uint32_t u = (uint32_t)((i + k * step) / P.R);
+      const uint32_t u = edge_row(rp, i + k * step, P.R);
       if (P.active[u]) f(u, v[k]);
     }
   }
@@ -607,11 +618,41 @@ __device__ __forceinline__ void rev2_local_sort(const uint32_t (&key)[kRev2Per],
   for (int k = 0; k < kRev2Per; k++) pos[k] = ok[k] ? lstart[key[k]] + rk[k] : 0u;
 }
 
+// Edges of chunk blockIdx.x read as 16-byte groups of one row (R a power
+// of two and a multiple of 4), four groups in flight per thread.
+template <class F>
+__device__ __forceinline__ void for_chunk_edges4(const PoolView &P, const RevPlan &rp, F f) {
+  const uint32_t r0 = blockIdx.x * rp.ch;
+  const uint32_t r1 = std::min<uint32_t>(P.cap, r0 + rp.ch);
+  if (r0 >= r1) return;
+  const uint32_t q0 = r0 * P.R / 4, q1 = r1 * P.R / 4;
+  const uint32_t step = blockDim.x;
+  const uint4 *adj4 = reinterpret_cast<const uint4 *>(P.adj);
+  for (uint32_t q = q0 + threadIdx.x; q < q1; q += 4 * step) {
+    uint4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; k++)
+      v[k] = q + k * step < q1 ? adj4[q + k * step] : make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      if (q + k * step >= q1) continue;
+      const uint32_t u = (4 * (q + k * step)) >> rp.rshift;
+      if (!P.active[u]) continue;
+      if (v[k].x != kInvalid) f(u, v[k].x);
+      if (v[k].y != kInvalid) f(u, v[k].y);
+      if (v[k].z != kInvalid) f(u, v[k].z);
+      if (v[k].w != kInvalid) f(u, v[k].w);
+    }
+  }
+}
+
 __global__ __launch_bounds__(kRevThreads) void k_rev2_count(PoolView P, RevPlan rp, uint32_t *bh) {
   __shared__ uint32_t lh[kRev2Coarse];
   for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) lh[b] = 0;
   __syncthreads();
-  for_chunk_edges(P, rp, [&](uint32_t, uint32_t v) { atomicAdd(&lh[v >> rp.s1], 1u); });
+  auto add = [&](uint32_t, uint32_t v) { atomicAdd(&lh[v >> rp.s1], 1u); };
+  if (rp.rshift >= 2) for_chunk_edges4(P, rp, add);
+  else for_chunk_edges(P, rp, add);
   __syncthreads();
   for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) bh[(size_t)b * rp.ng + blockIdx.x] = lh[b];
 }
@@ -623,22 +664,47 @@ __global__ __launch_bounds__(kRevThreads) void k_rev2_part1(PoolView P, RevPlan 
   __shared__ uint32_t sval[kRev2Step];
   __shared__ uint8_t skey[kRev2Step];
   for (uint32_t b = threadIdx.x; b < rp.nb1; b += blockDim.x) gpos[b] = bo[(size_t)b * rp.ng + blockIdx.x];
-  const size_t r0 = (size_t)blockIdx.x * rp.ch;
-  const size_t r1 = std::min<size_t>(P.cap, r0 + rp.ch);
-  const size_t e0 = r0 * P.R, e1 = r1 < r0 ? e0 : r1 * P.R;
+  const uint32_t r0 = blockIdx.x * rp.ch;
+  const uint32_t r1 = std::min<uint32_t>(P.cap, r0 + rp.ch);
+  const uint32_t e0 = r0 * P.R, e1 = r1 < r0 ? e0 : r1 * P.R;
   const uint32_t m1 = (1u << rp.s1) - 1u;
-  for (size_t base = e0; base < e1; base += kRev2Step) {
+  for (uint32_t base = e0; base < e1; base += kRev2Step) {
     uint32_t key[kRev2Per], val[kRev2Per], pos[kRev2Per];
     bool ok[kRev2Per];
+    if (rp.rshift >= 2) {
+      // 16-byte groups of one row, all four loads in flight
+      const uint4 *adj4 = reinterpret_cast<const uint4 *>(P.adj);
+      uint4 w[kRev2Per / 4];
 #pragma unroll
-    for (int k = 0; k < kRev2Per; k++) {
-      const size_t i = base + (size_t)k * blockDim.x + threadIdx.x;
-      const bool in = i < e1;
-      const uint32_t v = in ? P.adj[i] : kInvalid;
-      const uint32_t u = (uint32_t)((in ? i : e1 - 1) / P.R);
-      ok[k] = v != kInvalid && P.active[u] != 0;
-      key[k] = ok[k] ? v >> rp.s1 : 0u;
-      val[k] = (u << rp.s1) | (v & m1);
+      for (int k4 = 0; k4 < kRev2Per / 4; k4++) {
+        const uint32_t q = base / 4 + (uint32_t)k4 * blockDim.x + threadIdx.x;
+        w[k4] = 4 * q < e1 ? adj4[q] : make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+      }
+#pragma unroll
+      for (int k4 = 0; k4 < kRev2Per / 4; k4++) {
+        const uint32_t q = base / 4 + (uint32_t)k4 * blockDim.x + threadIdx.x;
+        const uint32_t u = (4 * q) >> rp.rshift;
+        const bool act = 4 * q < e1 && P.active[u] != 0;
+        const uint32_t vv[4] = {w[k4].x, w[k4].y, w[k4].z, w[k4].w};
+#pragma unroll
+        for (int t = 0; t < 4; t++) {
+          const int k = 4 * k4 + t;
+          ok[k] = act && vv[t] != kInvalid;
+          key[k] = ok[k] ? vv[t] >> rp.s1 : 0u;
+          val[k] = (u << rp.s1) | (vv[t] & m1);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kRev2Per; k++) {
+        const uint32_t i = base + (uint32_t)k * blockDim.x + threadIdx.x;
+        const bool in = i < e1;
+        const uint32_t v = in ? P.adj[i] : kInvalid;
+        const uint32_t u = edge_row(rp, in ? i : e1 - 1, P.R);
+        ok[k] = v != kInvalid && P.active[u] != 0;
+        key[k] = ok[k] ? v >> rp.s1 : 0u;
+        val[k] = (u << rp.s1) | (v & m1);
+      }
     }
     rev2_local_sort(key, ok, rp.nb1, lcnt, lstart, wsum, pos);
 #pragma unroll
