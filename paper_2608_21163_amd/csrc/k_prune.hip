@@ -368,6 +368,35 @@ __device__ int prune_mfma_u8(const PoolView &P, uint32_t p, int m, uint32_t R, d
   return nsel;
 }
 
+// Greedy selection inside one block of 16 sorted positions, resolved in
+// parallel: kb (lane col) holds the earlier positions that would kill col,
+// vb the live positions.  Each round, an undecided position is rejected if
+// a selected one kills it, and selected if no undecided earlier position
+// can; the lowest undecided position is always decided, so this ends with
+// exactly the set the one-by-one walk selects.
+__device__ __forceinline__ uint32_t block_greedy(uint32_t kb, uint32_t vb, int col, int g) {
+  uint32_t S = 0, U = vb;
+  while (U) {
+    const bool und = ((U >> col) & 1u) != 0;
+    const bool rej = und && (kb & S) != 0u;
+    const bool sel = und && !rej && (kb & U) == 0u;
+    const uint32_t sm = (uint32_t)ballot(sel && g == 0) & 0xFFFFu;
+    const uint32_t rm = (uint32_t)ballot(rej && g == 0) & 0xFFFFu;
+    S |= sm;
+    U &= ~(sm | rm);
+  }
+  return S;
+}
+// The lowest n set bits of m.
+__device__ __forceinline__ uint32_t first_bits(uint32_t m, int n) {
+  uint32_t r = 0;
+  for (int k = 0; k < n && m; k++) {
+    r |= m & (0u - m);
+    m &= m - 1u;
+  }
+  return r;
+}
+
 // The largest integer distance d with coef * d <= D (fp64 product, as in the
 // prune test), for an integer-valued D >= 0; every d up to it passes, since
 // rounding is monotone.
@@ -426,6 +455,7 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
   sdist = finf();
   int nsel = 0;
   bool done = false;
+  uint32_t S_blk = 0;
   for (int b = 0; b < nt && !done; b++) {
     const uint32_t vb = tile_valid(b);
     if (!vb) continue;
@@ -446,20 +476,27 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       kmd |= xshfl(kmd, 32);
     }
     evals += 256;
-    const uint32_t bid = spos[16 * b + col];
-    const float bd = dpos[16 * b + col];
-    uint32_t S = 0, alive = vb;
-    while (alive) {
-      const int t = __ffs(alive) - 1;
-      alive &= alive - 1;
-      S |= 1u << t;
-      const uint32_t sv = rdlane(bid, t);
-      const float sdv = rdlane(bd, t);
-      if (ln == nsel) { sid = sv; sdist = sdv; }
-      nsel++;
-      if (nsel == (int)R) { done = true; break; }
-      alive &= ~((uint32_t)ballot(g == 0 && ((kmd >> t) & 1u)) & 0xFFFFu);
+    {
+      // kmd (lane col): positions of the block that kill col; only earlier
+      // ones matter
+      uint32_t S = block_greedy(kmd & ((1u << col) - 1u), vb, col, g);
+      int ns = __popc(S);
+      if (ns >= (int)R - nsel) {
+        ns = (int)R - nsel;
+        S = first_bits(S, ns);
+        done = true;
+      }
+      // lane nsel + k takes the k-th selected position of the block
+      const int k = ln - nsel;
+      if (k >= 0 && k < ns) {
+        const int t = __ffs(first_bits(S, k + 1) & ~first_bits(S, k)) - 1;
+        sid = spos[16 * b + t];
+        sdist = dpos[16 * b + t];
+      }
+      nsel += ns;
+      S_blk = S;
     }
+    const uint32_t S = S_blk;
     if (done) break;
     // later tiles that still hold a valid candidate, kGroup at a time: all
     // loads of a group are issued before any is used
@@ -597,19 +634,13 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     evals += 256;
     // the block's pivots in order: a live position is selected unless an
     // earlier selected one kills it
-    uint32_t S = 0, rest = vb;
+    uint32_t S = block_greedy(kb, vb, col, g);
+    int ns = __popc(S);
     const int room = (int)R - nsel;
-    int ns = 0;
-    while (rest) {
-      const int t = __ffs(rest) - 1;
-      rest &= rest - 1;
-      if ((rdlane(kb, t) & S) == 0u) {
-        S |= 1u << t;
-        if (++ns == room) {
-          done = true;
-          break;
-        }
-      }
+    if (ns >= room) {  // selection stops at R: keep the first `room`
+      S = first_bits(S, room);
+      ns = room;
+      done = true;
     }
     if (g == 0 && ((S >> col) & 1u)) {
       const int pos = nsel + __popc(S & ((1u << col) - 1u));
