@@ -1,0 +1,90 @@
+"""GPU parity at the benchmark's full size: 1,000,000 x 128 uint8 vectors,
+Vamana R=64, L=128, alpha=1.2, batches of 10,000, in the launch
+configuration the benchmark times.
+
+The GPU builds the base index exactly as the benchmark does (100 insert
+batches of 10,000, then one refresh pass).  Its state is imported into the
+oracle, and one round of the streaming workload (+10,000 inserts, -10,000
+deletes, 10,000 queries) is applied on both.  uint8 distances are exact
+integers on both sides, so after every batch the whole graph must be
+identical (lists as sets, degrees, active map, medoid), the reverse graph
+must be the exact transpose, and the query results must match id for id.
+"""
+import time
+
+import numpy as np
+import pytest
+
+from helpers import INVALID, canonical_rows, check_graph_invariants
+from oracle.oracle import Oracle
+from parity import compare_search, say
+from workloads import make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def _same_graph(gst, ost, tag):
+    assert np.array_equal(gst["active"], ost["active"]), tag
+    assert gst["medoid"] == ost["medoid"], (tag, gst["medoid"], ost["medoid"])
+    assert np.array_equal(gst["deg"], ost["deg"]), tag
+    a, b = canonical_rows(gst["adj"]), canonical_rows(ost["adj"])
+    bad = np.flatnonzero(np.any(a != b, axis=1))
+    assert bad.size == 0, f"{tag}: {bad.size} lists differ, e.g. {bad[:5]}"
+
+
+def test_full_size_round_matches_oracle():
+    import torch
+
+    from paper_2608_21163_amd import GrandIndex
+
+    t0 = time.perf_counter()
+    w = make_workload("sift1m_u8", seed=0, stream=dict(n_rounds=1)).keep_vectors()
+    cfg, spec = w.cfg, w.spec
+    assert spec.base_n == 1_000_000 and cfg.dim == 128 and cfg.R == 64 and cfg.L_build == 128
+    stream = torch.cuda.current_stream()
+    g = GrandIndex.from_config(cfg, max_batch=max(spec.build_batch, spec.n_insert, spec.n_delete),
+                               stream=stream.cuda_stream)
+    dev = torch.device("cuda:0")
+    base = []
+    for op in w.base_batches():
+        ids = torch.from_numpy(op.ids.astype(np.int32)).to(dev)
+        vecs = torch.from_numpy(op.vecs).to(dev)
+        g.insert(ids, vecs)
+        base.append((ids, vecs))
+    for ids, vecs in base:
+        g.delete(ids)
+        g.insert(ids, vecs)
+    del base
+    torch.cuda.synchronize()
+    say(f"[full size] GPU base build {time.perf_counter() - t0:.1f} s")
+
+    st = g.export()
+    check_graph_invariants(st, cfg.R)
+    o = Oracle(cfg, threads=16)
+    o.import_graph(w.vectors, st["adj"], st["deg"], st["active"], st["medoid"])
+    say(f"[full size] state imported into the oracle, {time.perf_counter() - t0:.1f} s")
+
+    for op in w.round_ops(0):
+        t1 = time.perf_counter()
+        if op.kind == "insert":
+            assert o.insert(op.ids, op.vecs) == 0
+            g.insert(torch.from_numpy(op.ids.astype(np.int32)).to(dev), torch.from_numpy(op.vecs).to(dev))
+            _same_graph(g.export(), o.export(), "insert")
+        elif op.kind == "delete":
+            assert o.delete(op.ids) == 0
+            g.delete(torch.from_numpy(op.ids.astype(np.int32)).to(dev))
+            gst = g.export(with_reverse=True)
+            ost = o.export(with_reverse=True)
+            _same_graph(gst, ost, "delete")
+            check_graph_invariants(gst, cfg.R)
+            assert np.array_equal(gst["rev_offsets"], ost["rev_offsets"])
+            assert np.array_equal(gst["rev_srcs"], ost["rev_srcs"])
+        else:
+            gi, gd = g.search(op.vecs, spec.k, spec.beam)
+            oi, od = o.search(op.vecs, spec.k, spec.beam)
+            assert compare_search(gi, gd, oi, od, 0.0) == 0
+            assert np.array_equal(gi, oi) and np.array_equal(gd, od)
+            assert (gi != INVALID).all()
+        say(f"[full size] {op.kind} of {len(op.vecs) if op.ids is None else len(op.ids)} matches the oracle "
+            f"({time.perf_counter() - t1:.1f} s)")
+    g.close()
