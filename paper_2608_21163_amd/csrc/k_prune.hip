@@ -560,16 +560,20 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
 
 // greedy_u8 with every candidate tile resident in registers: the NT tiles
 // (16 sorted candidates each, at most 16*NT candidates) are loaded once, all
-// loads in flight together, and each tile's norms and kill thresholds are
-// computed once; the block-wise selection then touches no memory.
-template <int NK, int NR, int NT>
+// loads in flight together.  Live positions are kept as lane masks (bit e of
+// vm[e / 64] for sorted position e), and per tile column the kill threshold
+// minus the row's norm, so a kill test is one multiply-add and a compare:
+// Dist(i, j) <= thr_j  <=>  |y_i|^2 - 2 y_i.y_j <= thr_j - |y_j|^2.  Against
+// a later tile the compares of the block's rows are ballots, masked with the
+// rows the block selected, and folded to the killed columns.  The selected
+// positions go to oid/od (LDS) in order; returns their number.
+template <int NK, int NT>
 __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
-                             const float *dpos, int *thr, uint32_t *oid, float *od, bool (&valid)[NR],
-                             unsigned long long &evals) {
-  static_assert(NT <= 4 * NR, "tiles beyond the candidate registers");
+                             const float *dpos, int *thr, int *nrmL, uint32_t *oid, float *od, uint32_t &ntile) {
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const size_t goff = (size_t)g * 16;
   const int nt = (m + 15) >> 4;
+  constexpr int NR = (NT + 3) / 4;
   v4i T[NT][NK];
   {
     uint4 raw[NT][NK];
@@ -585,13 +589,14 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) T[t][kk] = to_i8x16(raw[t][kk]);
   }
-  // kill thresholds of every sorted position (LDS), norms of the tile rows
+  // kill thresholds of the sorted positions (LDS), norms of the tile rows
 #pragma unroll
   for (int r = 0; r < NR; r++) {
     const int e = r * 64 + ln;
     thr[e] = e < m ? kill_threshold(coef, dpos[e]) : -1;
   }
-  int nrm[NT];
+  __syncthreads();
+  int t2[NT];
 #pragma unroll
   for (int t = 0; t < NT; t++) {
     int sq = 0;
@@ -599,39 +604,36 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     for (int kk = 0; kk < NK; kk++) sq = sq_i8x16(T[t][kk], sq);
     sq += (int)xshfl((uint32_t)sq, 16);
     sq += (int)xshfl((uint32_t)sq, 32);
-    nrm[t] = sq;
+    if (g == 0) nrmL[16 * t + col] = sq;
+    t2[t] = thr[16 * t + col] - sq;
   }
   __syncthreads();
-  auto tile_valid = [&](int t) -> uint32_t {
-    bool v = valid[0];
+  uint64_t vm[NR];
 #pragma unroll
-    for (int r = 1; r < NR; r++) v = r == (t >> 2) ? valid[r] : v;
-    return (uint32_t)(ballot(v) >> (16 * (t & 3))) & 0xFFFFu;
-  };
+  for (int r = 0; r < NR; r++) vm[r] = ballot(r * 64 + ln < m);
   int nsel = 0;
   bool done = false;
 #pragma unroll
   for (int b = 0; b < NT; b++) {
     if (b >= nt || done) break;
-    const uint32_t vb = tile_valid(b);
+    const uint32_t vb = (uint32_t)(vm[b >> 2] >> (16 * (b & 3))) & 0xFFFFu;
     if (!vb) continue;
     int rn[4];
 #pragma unroll
-    for (int ii = 0; ii < 4; ii++) rn[ii] = __shfl(nrm[b], 4 * g + ii, 64);
+    for (int ii = 0; ii < 4; ii++) rn[ii] = nrmL[16 * b + 4 * g + ii];
     // kb (lane col < 16): the block's earlier positions that would kill col
     uint32_t kb = 0;
     {
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[b][kk], acc);
-      const int th = thr[16 * b + col];
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) kb |= (rn[ii] + nrm[b] - 2 * acc[ii] <= th) ? (1u << (4 * g + ii)) : 0u;
+      for (int ii = 0; ii < 4; ii++) kb |= (rn[ii] - 2 * acc[ii] <= t2[b]) ? (1u << (4 * g + ii)) : 0u;
       kb |= xshfl(kb, 16);
       kb |= xshfl(kb, 32);
       kb &= (1u << col) - 1u;
     }
-    evals += 256;
+    ntile++;
     // the block's pivots in order: a live position is selected unless an
     // earlier selected one kills it
     uint32_t S = block_greedy(kb, vb, col, g);
@@ -649,22 +651,28 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     }
     nsel += ns;
     if (done) break;
+    // lanes (g, col) whose block row 4g + ii was selected
+    uint64_t selm[4];
+#pragma unroll
+    for (int ii = 0; ii < 4; ii++) {
+      uint64_t mk = 0;
+#pragma unroll
+      for (int gg = 0; gg < 4; gg++) mk |= ((S >> (4 * gg + ii)) & 1u) ? (0xFFFFull << (16 * gg)) : 0ull;
+      selm[ii] = mk;
+    }
 #pragma unroll
     for (int c = b + 1; c < NT; c++) {
       if (c >= nt) break;
-      if (!tile_valid(c)) continue;
+      if (!((vm[c >> 2] >> (16 * (c & 3))) & 0xFFFFull)) continue;
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[c][kk], acc);
-      const int th = thr[16 * c + col];
-      uint32_t km = 0;
+      uint64_t dm = 0;
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) km |= (rn[ii] + nrm[c] - 2 * acc[ii] <= th) ? (1u << (4 * g + ii)) : 0u;
-      km |= xshfl(km, 16);
-      km |= xshfl(km, 32);
-      evals += 256;
-      const bool dead = g == (c & 3) && (km & S) != 0;
-      valid[c >> 2] = valid[c >> 2] && !dead;
+      for (int ii = 0; ii < 4; ii++) dm |= ballot(rn[ii] - 2 * acc[ii] <= t2[c]) & selm[ii];
+      const uint64_t d = (dm | (dm >> 16) | (dm >> 32) | (dm >> 48)) & 0xFFFFull;
+      vm[c >> 2] &= ~(d << (16 * (c & 3)));
+      ntile++;
     }
   }
   __syncthreads();
@@ -925,13 +933,14 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
 // candidate tile are live at a time, so many waves fit per SIMD to hide
 // the gathers.
 template <int NK>
-__global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
+__global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
   constexpr int NC = 2;
   __shared__ uint4 rowL[16];
   __shared__ uint32_t cl[64 * NC];
   __shared__ uint32_t spos[64 * NC];
   __shared__ float dpos[64 * NC];
   __shared__ int thrL[64 * NC];
+  __shared__ int nrmL[64 * NC];
   __shared__ uint32_t oid[64];
   __shared__ float od[64];
   const int ln = lane(), g = ln >> 4, col = ln & 15;
@@ -1034,15 +1043,15 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     }
     __syncthreads();
     wave_sort64<NC>(key);
-    bool valid[NC];
 #pragma unroll
     for (int r = 0; r < NC; r++) {
-      valid[r] = r * 64 + ln < m;
       spos[r * 64 + ln] = (uint32_t)key[r];
       dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
     }
     __syncthreads();
-    const int nsel = greedy_u8_reg<NK, NC, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, oid, od, valid, evals);
+    uint32_t ntile = 0;
+    const int nsel = greedy_u8_reg<NK, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, nrmL, oid, od, ntile);
+    evals += 256ull * ntile;
     if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? oid[ln] : kInvalid;
     if (ln == 0) P.deg[u] = (uint32_t)nsel;
     prunes++;

@@ -461,7 +461,7 @@ __device__ __forceinline__ void wave_sort64(uint64_t (&k)[N]) {
           if (p > r) {
             const bool up = ((r * 64 + ln) & kk) == 0;
             const uint64_t a = k[r], b = k[p];
-            const bool sw = up ? (b < a) : (a < b);
+            const bool sw = (b < a) == up;
             k[r] = sw ? b : a;
             k[p] = sw ? a : b;
           }
@@ -472,8 +472,8 @@ __device__ __forceinline__ void wave_sort64(uint64_t (&k)[N]) {
           const bool up = ((r * 64 + ln) & kk) == 0;
           const bool keep_min = ((ln & j) == 0) == up;
           const uint64_t o = xshfl64(k[r], j);
-          const bool take = keep_min ? (o < k[r]) : (k[r] < o);
-          k[r] = take ? o : k[r];
+          // equal keys may swap either way: the values are the same
+          k[r] = ((o < k[r]) == keep_min) ? o : k[r];
         }
       }
     }
