@@ -87,6 +87,7 @@ __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
   const int ln = lane();
   const PoolView &P = a.pool;
   const uint32_t nt = a.ds->n_dirty;
+  uint32_t nodes = 0;
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
     const uint32_t q = a.list[it];
     const uint32_t g0 = a.goff[q], g1 = a.goff[q + 1];
@@ -119,12 +120,11 @@ __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
       done += nb;
     }
     const uint64_t m = ballot(ln < (int)P.R && rv != kInvalid);
-    if (ln == 0) {
-      P.deg[q] = (uint32_t)popc(m);
-      atomicAdd(&a.ds->dirty, 1ull);
-    }
+    if (ln == 0) P.deg[q] = (uint32_t)popc(m);
+    nodes++;
     __syncthreads();
   }
+  if (ln == 0 && nodes) atomicAdd(&a.ds->dirty, (unsigned long long)nodes);  // one counter update per wave
 }
 hipError_t launch_cagra_detour(const CagraArgs &a, uint32_t grid, hipStream_t s) {
   if (grid == 0) return hipSuccess;
@@ -189,10 +189,19 @@ __global__ void k_cagra_affected(const uint32_t *ids, uint32_t n, const uint8_t 
   const uint32_t i = blockIdx.x;
   if (i >= n) return;
   const uint32_t row = by_batch ? i : ids[i];
-  for (uint32_t j = rev_off[row] + threadIdx.x; j < rev_off[row + 1]; j += blockDim.x) {
-    const uint32_t z = rev_src[j];
-    if (in_batch[z]) continue;
-    if (atomicExch(&mark[z], epoch) != epoch) list[atomicAdd(&ds->n_dirty, 1u)] = z;
+  const uint32_t b0 = rev_off[row], b1 = rev_off[row + 1];
+  for (uint32_t base = b0; base < b1; base += 64) {
+    const uint32_t j = base + lane();
+    const uint32_t z = j < b1 ? rev_src[j] : kInvalid;
+    const bool add = z != kInvalid && !in_batch[z] && atomicExch(&mark[z], epoch) != epoch;
+    // one list reservation per wave
+    const uint64_t m = ballot(add);
+    if (!m) continue;
+    const int l0 = ffs64(m);
+    uint32_t at = 0;
+    if (lane() == l0) at = atomicAdd(&ds->n_dirty, (uint32_t)popc(m));
+    at = rdlane(at, l0);
+    if (add) list[at + (uint32_t)mbcnt(m)] = z;
   }
 }
 __global__ void k_zero_ndirty2(DevScalars *ds) { ds->n_dirty = 0; }
@@ -212,6 +221,7 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   const PoolView &P = a.pool;
   const bool inrow = ln < (int)P.R;
   const uint32_t nt = a.ds->n_dirty;
+  uint32_t nodes = 0;
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
     const uint32_t u = a.list[it];
     uint32_t rv = inrow ? P.adj[(size_t)u * P.R + ln] : kInvalid;
@@ -259,11 +269,10 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
       __syncthreads();
     }
     const uint64_t m = ballot(inrow && rv != kInvalid);
-    if (ln == 0) {
-      P.deg[u] = (uint32_t)popc(m);
-      atomicAdd(&a.ds->dirty, 1ull);
-    }
+    if (ln == 0) P.deg[u] = (uint32_t)popc(m);
+    nodes++;
   }
+  if (ln == 0 && nodes) atomicAdd(&a.ds->dirty, (unsigned long long)nodes);  // one counter update per wave
 }
 hipError_t launch_cagra_pickone(const CagraArgs &a, uint32_t grid, hipStream_t s) {
   if (grid == 0) return hipSuccess;
