@@ -21,15 +21,26 @@ namespace gr {
 
 constexpr int kHashBits = 11;
 constexpr int kHashSize = 1 << kHashBits;
+constexpr int kHashBits8 = 12;  // 8-bit tags: twice the slots in the same bytes
 
-// Hash of evaluated ids.  With 16-bit entries an id v is split into a tag
-// (v >> kHashBits) and a slot ((v ^ tag * odd) & mask); tag and slot
-// together determine v, so a stored tag matching the probe's tag is an exact
-// hit.  The tag 0xFFFF marks an empty slot, so this form needs ids below
-// 0xFFFF << kHashBits; larger pools store whole 32-bit ids at a
-// multiplicative hash slot.
+// Hash of evaluated ids.  With 8- or 16-bit entries an id v is split into a
+// tag (v >> bits) and a slot ((v ^ tag * odd) & mask); tag and slot together
+// determine v, so a stored tag matching the probe's tag is an exact hit.  The
+// all-ones tag marks an empty slot, so the 8-bit form (4096 slots) needs ids
+// below 0xFF << 12 and the 16-bit form (2048 slots) ids below 0xFFFF << 11;
+// larger pools store whole 32-bit ids at a multiplicative hash slot.  Both
+// narrow forms take 4 KB of LDS.
 template <class HW> struct IdHash;
+template <> struct IdHash<uint8_t> {
+  static constexpr int kBits = kHashBits8;
+  static __device__ __forceinline__ uint32_t slot(uint32_t v) {
+    return (v ^ ((v >> kBits) * 40503u)) & ((1u << kBits) - 1u);
+  }
+  static __device__ __forceinline__ uint8_t word(uint32_t v) { return (uint8_t)(v >> kBits); }
+  static constexpr uint8_t kEmpty = 0xFFu;
+};
 template <> struct IdHash<uint16_t> {
+  static constexpr int kBits = kHashBits;
   static __device__ __forceinline__ uint32_t slot(uint32_t v) {
     return (v ^ ((v >> kHashBits) * 40503u)) & (kHashSize - 1);
   }
@@ -37,16 +48,19 @@ template <> struct IdHash<uint16_t> {
   static constexpr uint16_t kEmpty = 0xFFFFu;
 };
 template <> struct IdHash<uint32_t> {
+  static constexpr int kBits = kHashBits;
   static __device__ __forceinline__ uint32_t slot(uint32_t v) { return (v * 0x9E3779B1u) >> (32 - kHashBits); }
   static __device__ __forceinline__ uint32_t word(uint32_t v) { return v; }
   static constexpr uint32_t kEmpty = kInvalid;
 };
 bool hash16_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFFFu << kHashBits); }
+bool hash8_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFu << kHashBits8); }
 
 template <int KIND, int LPV, int CPL, int NR, class HW>
 __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   typedef IdHash<HW> H;
-  __shared__ HW hsh[kHashSize];
+  constexpr int kSlots = 1 << H::kBits;
+  __shared__ HW hsh[kSlots];
   __shared__ uint32_t nid[64];
   __shared__ float nkey[64];
   __shared__ uint32_t mid[64 * NR];
@@ -58,7 +72,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   const uint8_t *qrow = a.qids ? P.vecs + (size_t)a.qids[qi] * P.stride : a.qbase + (size_t)qi * P.stride;
   Slice<KIND, LPV, CPL> s;
   load_slice<KIND, LPV, CPL>(s, qrow, P.nch);
-  for (int i = ln; i < kHashSize; i += 64) hsh[i] = H::kEmpty;
+  for (int i = ln; i < kSlots; i += 64) hsh[i] = H::kEmpty;
 
   float cd[NR];
   uint32_t ci[NR];
@@ -198,9 +212,10 @@ int vec_class(int nch) {
 
 hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
-  const bool h16 = hash16_ok(a.pool.cap);
+  const bool h8 = hash8_ok(a.pool.cap), h16 = hash16_ok(a.pool.cap);
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.ell, {
-    if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t>), dim3(a.nq), dim3(64), 0, st, a);
+    if (h8) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t>), dim3(a.nq), dim3(64), 0, st, a);
+    else if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t>), dim3(a.nq), dim3(64), 0, st, a);
     else hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint32_t>), dim3(a.nq), dim3(64), 0, st, a);
     return hipGetLastError();
   }));
