@@ -743,7 +743,18 @@ __global__ __launch_bounds__(kRevThreads) void k_rev2_count2(RevPlan rp, const u
   uint32_t x0, x1;
   rev2_chunk(rp, bo, b1, c, x0, x1);
   const uint32_t m1 = (1u << rp.s1) - 1u;
-  for (uint32_t j = x0 + threadIdx.x; j < x1; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
+  // unaligned head and tail word by word, the middle as 16-byte groups
+  const uint32_t a0 = std::min(x1, (x0 + 3u) & ~3u), a1 = std::max(a0, x1 & ~3u);
+  for (uint32_t j = x0 + threadIdx.x; j < a0; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
+  for (uint32_t j = a1 + threadIdx.x; j < x1; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
+  const uint4 *p4 = reinterpret_cast<const uint4 *>(pairs);
+  for (uint32_t q = a0 / 4 + threadIdx.x; q < a1 / 4; q += blockDim.x) {
+    const uint4 v = p4[q];
+    atomicAdd(&lh[(v.x & m1) >> rp.s2], 1u);
+    atomicAdd(&lh[(v.y & m1) >> rp.s2], 1u);
+    atomicAdd(&lh[(v.z & m1) >> rp.s2], 1u);
+    atomicAdd(&lh[(v.w & m1) >> rp.s2], 1u);
+  }
   __syncthreads();
   for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x) bh2[((size_t)b1 * rp.nsub + b) * rp.nc2 + c] = lh[b];
 }
@@ -790,11 +801,12 @@ __global__ __launch_bounds__(kRevThreads) void k_rev2_part2(RevPlan rp, const ui
   }
 }
 
-__global__ __launch_bounds__(kRevThreads) void k_rev2_fill(RevPlan rp, uint32_t cap, const uint32_t *bo2,
-                                                           const uint32_t *pairs2, uint32_t *off, uint32_t *src) {
+constexpr int kFillThreads = 512;  // more loads in flight per fine bucket
+__global__ __launch_bounds__(kFillThreads) void k_rev2_fill(RevPlan rp, uint32_t cap, const uint32_t *bo2,
+                                                            const uint32_t *pairs2, uint32_t *off, uint32_t *src) {
   constexpr uint32_t W = 1u << kRev2FineShift;
   __shared__ uint32_t cnt[W];
-  __shared__ uint32_t wsum[kRevThreads / 64];
+  __shared__ uint32_t wsum[kFillThreads / 64];
   __shared__ uint32_t stage[kRev2Stage];
   const uint32_t fb = blockIdx.x;  // fine bucket = coarse * nsub + sub
   const size_t nfine = (size_t)rp.nb1 * rp.nsub;
@@ -844,7 +856,7 @@ hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, con
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_rev2_part2, dim3(rp.nb1 * rp.nc2), dim3(kRevThreads), 0, s, rp, rb.bo, rb.bo2, rb.pairs,
                        rb.pairs2);
-    hipLaunchKernelGGL(k_rev2_fill, dim3(rp.nb1 * rp.nsub), dim3(kRevThreads), 0, s, rp, p.cap, rb.bo2, rb.pairs2,
+    hipLaunchKernelGGL(k_rev2_fill, dim3(rp.nb1 * rp.nsub), dim3(kFillThreads), 0, s, rp, p.cap, rb.bo2, rb.pairs2,
                        off, src);
     hipLaunchKernelGGL(k_count_edges, dim3(1), dim3(64), 0, s, off, nrows, ds);
     return hipGetLastError();
