@@ -334,22 +334,184 @@ __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
   }
 }
 
-// The matrix-core form serves uint8 rows of 64 or 128 bytes with R <= 64,
-// k_repair <= 64 and c <= 4, over the chunk list; every other configuration
-// takes one wave per deleted node.
+// ---------------------------------------------------------------------------
+// fp32 repair over the same work chunks: one lane per neighbour.  C_i is
+// taken 16 candidates at a time; their rows pass through LDS in slices of 64
+// floats (each value read once per slice, by every lane at the same address)
+// while each lane streams its own neighbour's row in pieces of 16 floats and
+// accumulates the 16 distances in fp64, in dimension order -- the summation
+// the oracle performs, so the rounded distances are identical.  Each lane
+// keeps its neighbour's K smallest (distance, id) keys; the records and their
+// offsets are those of the uint8 form.
+template <int KIND, int K>
+__global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
+  constexpr int GC = 16, SL = 64;
+  __shared__ float cs[GC][SL];
+  __shared__ uint32_t cidL[64];
+  const int ln = lane();
+  const PoolView &P = a.pool;
+  const uint32_t R = P.R;
+  const uint32_t c = a.c;
+  const int kr = (int)a.kr;
+  const int nfl = P.nch * 4;  // floats per padded row (padding is zero)
+  if ((size_t)a.rofs[a.n] > a.rcap) return;  // the host grows the buffers and launches again
+  const uint32_t total = a.coff[a.n];
+  unsigned long long evals = 0, rows = 0, recs = 0;
+  for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
+    const uint32_t i = a.cmap[q];
+    const uint32_t j = q - a.coff[i];
+    const uint32_t p = a.ids[i];
+    uint32_t b0, b1;
+    rev_row(a, i, p, b0, b1);
+    const uint32_t nin = b1 - b0, nci = (nin + 63) / 64;
+    const bool inbound = j < nci;
+    int cnt;
+    uint32_t x, rbase;
+    if (inbound) {
+      const uint32_t e0 = j * 64;
+      cnt = (int)min(64u, nin - e0);
+      x = ln < cnt ? a.rev_src[b0 + e0 + ln] : kInvalid;
+      rbase = a.rofs[i] + e0 * (c + 1);
+    } else {
+      cnt = (int)R;
+      x = ln < cnt ? P.adj[(size_t)p * R + ln] : kInvalid;
+      rbase = a.rofs[i] + nin * (c + 1);
+    }
+    const bool xok = x != kInvalid && !a.in_batch[x];
+    cidL[ln] = ln < kr ? a.ci[(size_t)i * kr + ln] : kInvalid;
+    __syncthreads();
+    if (j == 0) rows += (unsigned long long)popc(ballot(ln < kr && kvalid(cidL[ln])));
+    rows += (unsigned long long)popc(ballot(xok));
+    const float *xrow = reinterpret_cast<const float *>(P.vecs + (size_t)(xok ? x : p) * P.stride);
+    uint64_t l[K];
+#pragma unroll
+    for (int k = 0; k < K; k++) l[k] = ~0ull;
+    for (int g0 = 0; g0 < kr; g0 += GC) {
+      double acc[GC];
+#pragma unroll
+      for (int k = 0; k < GC; k++) acc[k] = 0.0;
+      for (int d0 = 0; d0 < nfl; d0 += SL) {
+        // candidates g0 .. g0+15, floats d0 .. d0+63 (zeros past the row or
+        // for missing candidates), 16 floats per lane
+        __syncthreads();
+        {
+          const int cand = ln >> 2, part = ln & 3;
+          const int e = g0 + cand;
+          const uint32_t cv = e < kr ? cidL[e] : kInvalid;
+          const float *crow = reinterpret_cast<const float *>(P.vecs + (size_t)(kvalid(cv) ? cv : p) * P.stride);
+#pragma unroll
+          for (int h = 0; h < 4; h++) {
+            const int f = d0 + 16 * part + 4 * h;
+            const uint4 v = (kvalid(cv) && f < nfl) ? *reinterpret_cast<const uint4 *>(crow + f) : make_uint4(0, 0, 0, 0);
+            *reinterpret_cast<uint4 *>(&cs[cand][16 * part + 4 * h]) = v;
+          }
+        }
+        __syncthreads();
+        for (int pc = 0; pc < SL && d0 + pc < nfl; pc += 16) {
+          float xv[16];
+#pragma unroll
+          for (int h = 0; h < 4; h++) {
+            const int f = d0 + pc + 4 * h;  // rows hold nfl floats, a multiple of 4
+            const uint4 v = f < nfl ? *reinterpret_cast<const uint4 *>(xrow + f) : make_uint4(0, 0, 0, 0);
+            xv[4 * h + 0] = __uint_as_float(v.x);
+            xv[4 * h + 1] = __uint_as_float(v.y);
+            xv[4 * h + 2] = __uint_as_float(v.z);
+            xv[4 * h + 3] = __uint_as_float(v.w);
+          }
+#pragma unroll
+          for (int k = 0; k < GC; k++)
+#pragma unroll
+            for (int t = 0; t < 16; t++) {
+              if (KIND == kF32L2) {
+                const double df = (double)cs[k][pc + t] - (double)xv[t];
+                acc[k] = __builtin_fma(df, df, acc[k]);
+              } else {
+                acc[k] = __builtin_fma((double)xv[t], (double)cs[k][pc + t], acc[k]);
+              }
+            }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < GC; k++) {
+        const int e = g0 + k;
+        const uint32_t cv = e < kr ? cidL[e] : kInvalid;
+        const bool ok = xok && kvalid(cv) && cv != x;
+        evals += ok ? 1u : 0u;
+        const float dk = finalize<KIND>(acc[k]);
+        kl_insert64<K>(l, ok ? key64(dk, cv) : ~0ull);
+      }
+    }
+    if (ln < cnt) {
+      const uint32_t nrec = inbound ? c + 1 : c;
+      const uint32_t base = rbase + (uint32_t)ln * nrec;
+      for (uint32_t k = 0; k < nrec; k++) {
+        uint64_t key = ~0ull;
+#pragma unroll
+        for (int kk = 0; kk < K; kk++)
+          if ((uint32_t)kk == k) key = l[kk];
+        const bool v = key != ~0ull;
+        const uint32_t yi = v ? (uint32_t)key : kInvalid;
+        const float yd = v ? unsortable((uint32_t)(key >> 32)) : 0.0f;
+        if (!xok) {
+          a.rec_t[base + k] = kInvalid;
+        } else if (inbound) {
+          const bool marker = k == c;
+          a.rec_t[base + k] = x;
+          a.rec_s[base + k] = marker ? kInvalid : yi;
+          a.rec_d[base + k] = marker ? 0.0f : yd;
+          recs++;
+        } else {
+          a.rec_t[base + k] = yi;
+          a.rec_s[base + k] = v ? x : kInvalid;
+          a.rec_d[base + k] = yd;
+          recs += v ? 1u : 0u;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  unsigned long long ev = evals, rc = recs;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    ev += __shfl_xor(ev, o, 64);
+    rc += __shfl_xor(rc, o, 64);
+  }
+  if (ln == 0 && (ev | rc | rows)) {
+    atomicAdd(&a.ds->records, rc);
+    atomicAdd(&a.ds->rep_evals, ev);
+    atomicAdd(&a.ds->rep_rows, rows);
+    atomicAdd(&a.ds->rep_recs, rc);
+  }
+}
+
+// Chunked forms (R <= 64, k_repair <= 64, c <= 4): the matrix-core form for
+// uint8 rows of 64 or 128 bytes, the lane-per-neighbour form for fp32 rows;
+// every other configuration takes one wave per deleted node.
 bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c) {
-  return kind == kU8L2 && kr <= 64 && c <= 4 && p.R <= 64 && (p.nch == 4 || p.nch == 8);
+  if (kr > 64 || c > 4 || p.R > 64) return false;
+  if (kind == kU8L2) return p.nch == 4 || p.nch == 8;
+  return kind == kF32L2 || kind == kF32IP;
 }
 
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  if (repair_chunked(kind, a.pool, a.kr, a.c)) {
+  if (kind == kU8L2 && repair_chunked(kind, a.pool, a.kr, a.c)) {
     if (a.pool.nch == 8) {
       if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(grid), dim3(64), 0, st, a);
       else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(grid), dim3(64), 0, st, a);
     } else {
       if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(grid), dim3(64), 0, st, a);
       else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(grid), dim3(64), 0, st, a);
+    }
+    return hipGetLastError();
+  }
+  if (repair_chunked(kind, a.pool, a.kr, a.c)) {
+    if (kind == kF32L2) {
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_vec<kF32L2, 2>), dim3(grid), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_vec<kF32L2, 4>), dim3(grid), dim3(64), 0, st, a);
+    } else {
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_vec<kF32IP, 2>), dim3(grid), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_vec<kF32IP, 4>), dim3(grid), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }
