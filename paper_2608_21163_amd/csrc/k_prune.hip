@@ -925,6 +925,51 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
   }
 }
 
+// C of dirty node u (R <= 64, P <= 64): the kept entries of N_out(u) (minus
+// u and the delete batch) in slot order, then the sources of the P smallest
+// distinct records that are not already kept; written to cl (LDS).  Returns
+// |C|; nrec is the number of records addressed to u.
+__device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL, uint32_t *cl, uint32_t &nrec) {
+  const int ln = lane();
+  const PoolView &P = a.pool;
+  const uint32_t R = P.R;
+  const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
+  const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
+  nrec = g1 - g0;
+  const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
+  const uint64_t kmask = ballot(keep);
+  const int kr = popc(kmask);
+  reinterpret_cast<uint32_t *>(rowL)[ln] = keep ? rv : kInvalid;
+  if (keep) cl[mbcnt(kmask)] = rv;
+  __syncthreads();
+  // scratch_u: the P smallest distinct (distance, source) records
+  float sd[1] = {finf()};
+  uint32_t si[1] = {kInvalid};
+  for (uint32_t base = g0; base < g1; base += 64) {
+    const uint32_t j = base + ln;
+    uint32_t sv = j < g1 ? a.gsrc[j] : kInvalid;
+    float dv = j < g1 ? a.gd[j] : finf();
+    if (!kvalid(sv)) { sv = kInvalid; dv = finf(); }
+    wave_merge_new_fast<1>(sd, si, dv, sv, (int)a.P);
+  }
+  bool isnew;
+  {
+    const uint32_t sv = si[0];
+    bool ok = kvalid(sv) && sv != u && !(a.in_batch && a.in_batch[sv]);
+#pragma unroll 4
+    for (int t = 0; t < 16; t++) {
+      const uint4 r4 = rowL[t];
+      ok = ok & (r4.x != sv) & (r4.y != sv) & (r4.z != sv) & (r4.w != sv);
+    }
+    isnew = ok;
+  }
+  const uint64_t nmask = ballot(isnew);
+  const int m = kr + popc(nmask);
+  if (isnew) cl[kr + mbcnt(nmask)] = si[0];
+  __syncthreads();
+  return m;
+}
+
 // Rebuild of dirty nodes for uint8 rows of 64*NK bytes with R <= 64 and
 // R + P <= 128 (the same steps as k_rebuild).  When a node prunes, D_u of
 // every candidate comes from int8 MFMA of u's row against the candidates,
@@ -953,40 +998,9 @@ __global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
   for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
     const uint32_t u = a.list[it];
     nodes++;
-    const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
-    const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
-    recs += g1 - g0;
-    const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
-    const uint64_t kmask = ballot(keep);
-    const int kr = popc(kmask);
-    reinterpret_cast<uint32_t *>(rowL)[ln] = keep ? rv : kInvalid;
-    if (keep) cl[mbcnt(kmask)] = rv;
-    __syncthreads();
-    // scratch_u: the P smallest distinct (distance, source) records
-    float sd[1] = {finf()};
-    uint32_t si[1] = {kInvalid};
-    for (uint32_t base = g0; base < g1; base += 64) {
-      const uint32_t j = base + ln;
-      uint32_t sv = j < g1 ? a.gsrc[j] : kInvalid;
-      float dv = j < g1 ? a.gd[j] : finf();
-      if (!kvalid(sv)) { sv = kInvalid; dv = finf(); }
-      wave_merge_new_fast<1>(sd, si, dv, sv, (int)a.P);
-    }
-    bool isnew;
-    {
-      const uint32_t sv = si[0];
-      bool ok = kvalid(sv) && sv != u && !(a.in_batch && a.in_batch[sv]);
-#pragma unroll 4
-      for (int t = 0; t < 16; t++) {
-        const uint4 r4 = rowL[t];
-        ok = ok & (r4.x != sv) & (r4.y != sv) & (r4.z != sv) & (r4.w != sv);
-      }
-      isnew = ok;
-    }
-    const uint64_t nmask = ballot(isnew);
-    const int m = kr + popc(nmask);
-    if (isnew) cl[kr + mbcnt(nmask)] = si[0];
-    __syncthreads();
+    uint32_t nrec;
+    const int m = collect_candidates(a, u, rowL, cl, nrec);
+    recs += nrec;
     if (m <= (int)R) {
       if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? cl[ln] : kInvalid;
       if (ln == 0) P.deg[u] = (uint32_t)m;
@@ -1170,6 +1184,301 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// fp32 GrANDRobustPrune with one lane per candidate position.  Distances
+// are accumulated in fp64 in dimension order -- the oracle's summation, so
+// every rounded distance is identical -- between each lane's own rows
+// (streamed from the pool in pieces of 16 floats) and up to 16 rows staged in
+// LDS, one slice of kVecSlice floats at a time, which every lane reads at the
+// same address.
+constexpr int kVecSlice = 64;
+
+// st[k][0..kVecSlice) <- floats [d0, d0 + kVecSlice) of pool row ids[k]
+// (k < ns; zeros past the row or for an invalid id).  Lane (k, part) copies
+// 16 floats.
+__device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids, int ns, int d0, int nfl,
+                                          float (*st)[kVecSlice]) {
+  const int ln = lane(), k = ln >> 2, part = ln & 3;
+  if (k >= ns) return;
+  const uint32_t id = ids[k];
+  const float *row = reinterpret_cast<const float *>(P.vecs + (size_t)(kvalid(id) ? id : 0u) * P.stride);
+#pragma unroll
+  for (int h = 0; h < 4; h++) {
+    const int f = d0 + 16 * part + 4 * h;
+    const uint4 v = (kvalid(id) && f < nfl) ? *reinterpret_cast<const uint4 *>(row + f) : make_uint4(0, 0, 0, 0);
+    *reinterpret_cast<uint4 *>(&st[k][16 * part + 4 * h]) = v;
+  }
+}
+
+// acc[r][k] += the terms of floats [d0, d0 + kVecSlice) between this lane's
+// row own[r] and staged row k, for every register row r with work (act[r],
+// uniform).
+template <int KIND, int NCL, int NS>
+__device__ __forceinline__ void vec_accumulate(const float (*st)[kVecSlice], const float *const (&own)[NCL],
+                                               const bool (&act)[NCL], int d0, int nfl,
+                                               double (&acc)[NCL][NS]) {
+  for (int pc = 0; pc < kVecSlice && d0 + pc < nfl; pc += 16) {
+#pragma unroll
+    for (int r = 0; r < NCL; r++) {
+      if (!act[r]) continue;
+      float xv[16];
+#pragma unroll
+      for (int h = 0; h < 4; h++) {
+        const int f = d0 + pc + 4 * h;  // rows hold nfl floats, a multiple of 4
+        const uint4 v = f < nfl ? *reinterpret_cast<const uint4 *>(own[r] + f) : make_uint4(0, 0, 0, 0);
+        xv[4 * h + 0] = __uint_as_float(v.x);
+        xv[4 * h + 1] = __uint_as_float(v.y);
+        xv[4 * h + 2] = __uint_as_float(v.z);
+        xv[4 * h + 3] = __uint_as_float(v.w);
+      }
+#pragma unroll
+      for (int k = 0; k < NS; k++)
+#pragma unroll
+        for (int t = 0; t < 16; t++) {
+          if (KIND == kF32IP) {
+            acc[r][k] = __builtin_fma((double)xv[t], (double)st[k][pc + t], acc[r][k]);
+          } else {
+            const double df = (double)st[k][pc + t] - (double)xv[t];
+            acc[r][k] = __builtin_fma(df, df, acc[r][k]);
+          }
+        }
+    }
+  }
+}
+
+// GrANDRobustPrune over m candidates sorted by (D_p, id) (spos/dpos in LDS,
+// positions e = r*64 + lane, at most 64*NCL).  Positions are taken in blocks
+// of NPB pivots: the block's rows are staged and every lane computes the
+// distances from them to its later positions; the block's own selections
+// come from the parallel fixpoint, and later positions that a selected pivot
+// kills (coef * Dist <= D, in fp64 on the rounded distance) are dropped.
+// The selections go to oid/od (LDS) in order; returns their number.
+template <int KIND, int NCL, int NPB>
+__device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
+                         const float *dpos, float (*st)[kVecSlice], uint32_t *oid, float *od, uint32_t &evals) {
+  static_assert(NPB <= 16 && 64 % NPB == 0, "pivot blocks inside one register row");
+  const int ln = lane(), g = ln >> 4, col = ln & 15;
+  const int nfl = P.nch * 4;
+  uint64_t vm[NCL];
+#pragma unroll
+  for (int r = 0; r < NCL; r++) vm[r] = ballot(r * 64 + ln < m);
+  const float *own[NCL];
+#pragma unroll
+  for (int r = 0; r < NCL; r++) {
+    const int e = r * 64 + ln;
+    own[r] = reinterpret_cast<const float *>(P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride);
+  }
+  int nsel = 0;
+  const int nb = (m + NPB - 1) / NPB;
+  for (int b = 0; b < nb; b++) {
+    const int p0 = b * NPB;
+    uint64_t vr = 0;
+#pragma unroll
+    for (int r = 0; r < NCL; r++)
+      if (r == (p0 >> 6)) vr = vm[r];
+    const uint32_t vb = (uint32_t)(vr >> (p0 & 63)) & ((1u << NPB) - 1u);
+    if (!vb) continue;
+    bool act[NCL];
+#pragma unroll
+    for (int r = 0; r < NCL; r++) act[r] = r * 64 + 63 >= p0 && r * 64 < m;
+    double acc[NCL][NPB];
+#pragma unroll
+    for (int r = 0; r < NCL; r++)
+#pragma unroll
+      for (int k = 0; k < NPB; k++) acc[r][k] = 0.0;
+    for (int d0 = 0; d0 < nfl; d0 += kVecSlice) {
+      __syncthreads();
+      vec_stage(P, spos + p0, min(NPB, m - p0), d0, nfl, st);
+      __syncthreads();
+      vec_accumulate<KIND, NCL, NPB>(st, own, act, d0, nfl, acc);
+    }
+    // km[r]: pivots of the block that kill this lane's position
+    uint32_t km[NCL];
+#pragma unroll
+    for (int r = 0; r < NCL; r++) {
+      const int e = r * 64 + ln;
+      km[r] = 0;
+      if (act[r]) {
+        const double De = e < m ? (double)dpos[e] : 0.0;
+#pragma unroll
+        for (int k = 0; k < NPB; k++) {
+          const bool kill = e > p0 + k && e < m && coef * (double)finalize<KIND>(acc[r][k]) <= De;
+          km[r] |= kill ? (1u << k) : 0u;
+        }
+      }
+    }
+    evals += (uint32_t)(NPB * (m - p0));
+    // the block's own positions: lanes (p0 & 63) + col of register row p0 >> 6
+    uint32_t kbr = 0;
+#pragma unroll
+    for (int r = 0; r < NCL; r++)
+      if (r == (p0 >> 6)) kbr = km[r];
+    const uint32_t kb = (uint32_t)__shfl((int)kbr, ((p0 & 63) + col) & 63, 64) & ((1u << col) - 1u);
+    uint32_t S = block_greedy(kb, vb, col, g);
+    int ns = __popc(S);
+    const int room = (int)R - nsel;
+    bool done = false;
+    if (ns >= room) {
+      S = first_bits(S, room);
+      ns = room;
+      done = true;
+    }
+    if (g == 0 && ((S >> col) & 1u)) {
+      const int pos = nsel + __popc(S & ((1u << col) - 1u));
+      oid[pos] = spos[p0 + col];
+      od[pos] = dpos[p0 + col];
+    }
+    nsel += ns;
+    if (done) break;
+#pragma unroll
+    for (int r = 0; r < NCL; r++) {
+      const int e = r * 64 + ln;
+      vm[r] &= ~ballot(e >= p0 + NPB && (km[r] & S) != 0u);
+    }
+  }
+  __syncthreads();
+  return nsel;
+}
+
+// Rebuild of queued dirty nodes for fp32 rows with R <= 64 and R + P <= 128:
+// C as in k_rebuild_mr; D_u of every candidate from u's staged row, a
+// 64-bit-key sort, then prune_vec.
+template <int KIND>
+__global__ __launch_bounds__(64) void k_rebuild_vec(RebuildArgs a) {
+  constexpr int NC = 2;
+  __shared__ uint4 rowL[16];
+  __shared__ uint32_t cl[64 * NC];
+  __shared__ uint32_t spos[64 * NC];
+  __shared__ float dpos[64 * NC];
+  __shared__ float st[16][kVecSlice];
+  __shared__ uint32_t oid[64];
+  __shared__ float od[64];
+  __shared__ uint32_t uid[1];
+  const int ln = lane();
+  const PoolView &P = a.pool;
+  const uint32_t R = P.R;
+  const int nfl = P.nch * 4;
+  const uint32_t nd_total = *a.list_n;
+  uint32_t evals = 0, prunes = 0, nodes = 0, recs = 0, cand = 0;
+  for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
+    const uint32_t u = a.list[it];
+    nodes++;
+    uint32_t nrec;
+    const int m = collect_candidates(a, u, rowL, cl, nrec);
+    recs += nrec;
+    if (m <= (int)R) {
+      if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? cl[ln] : kInvalid;
+      if (ln == 0) P.deg[u] = (uint32_t)m;
+      __syncthreads();
+      continue;
+    }
+    // D_u of every candidate (list order)
+    {
+      const float *own[NC];
+      bool act[NC];
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        const int e = r * 64 + ln;
+        own[r] = reinterpret_cast<const float *>(P.vecs + (size_t)(e < m ? cl[e] : u) * P.stride);
+        act[r] = r * 64 < m;
+      }
+      double du[NC][1];
+#pragma unroll
+      for (int r = 0; r < NC; r++) du[r][0] = 0.0;
+      if (ln == 0) uid[0] = u;
+      for (int d0 = 0; d0 < nfl; d0 += kVecSlice) {
+        __syncthreads();
+        vec_stage(P, uid, 1, d0, nfl, st);
+        __syncthreads();
+        vec_accumulate<KIND, NC, 1>(st, own, act, d0, nfl, du);
+      }
+      evals += (uint32_t)m;
+      uint64_t key[NC];
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        const int e = r * 64 + ln;
+        key[r] = e < m ? key64(finalize<KIND>(du[r][0]), cl[e]) : ~0ull;
+      }
+      __syncthreads();
+      wave_sort64<NC>(key);
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        spos[r * 64 + ln] = (uint32_t)key[r];
+        dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
+      }
+      __syncthreads();
+    }
+    const int nsel = prune_vec<KIND, NC, 16>(P, u, m, R, a.coef, spos, dpos, st, oid, od, evals);
+    if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? oid[ln] : kInvalid;
+    if (ln == 0) P.deg[u] = (uint32_t)nsel;
+    prunes++;
+    cand += (uint32_t)m + 1;
+    __syncthreads();
+  }
+  if (ln == 0) {
+    atomicAdd(&a.ds->rb_prunes, (unsigned long long)prunes);
+    atomicAdd(&a.ds->rb_evals, (unsigned long long)evals);
+    atomicAdd(&a.ds->rb_cand, (unsigned long long)cand);
+    if (a.count_nodes) {
+      atomicAdd(&a.ds->dirty, (unsigned long long)nodes);
+      atomicAdd(&a.ds->rb_recs, (unsigned long long)recs);
+    }
+  }
+}
+
+// Forward GrANDRobustPrune of new fp32 points: V_i with the search's D, a
+// 64-bit-key sort, then prune_vec (blocks of 8 pivots for 256 candidates).
+template <int KIND, int NR>
+__global__ __launch_bounds__(64) void k_fwd_prune_vec(FwdPruneArgs a) {
+  constexpr int NPB = NR >= 4 ? 8 : 16;
+  __shared__ uint32_t spos[64 * NR];
+  __shared__ float dpos[64 * NR];
+  __shared__ float st[16][kVecSlice];
+  __shared__ uint32_t oid[64];
+  __shared__ float od[64];
+  const int ln = lane();
+  const uint32_t i = blockIdx.x;
+  if (i >= a.n) return;
+  const PoolView &P = a.pool;
+  const uint32_t p = a.ids[i];
+  const uint32_t nv = a.v_n[i];
+  const uint32_t R = P.R;
+  uint64_t key[NR];
+  int m = 0;
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    const uint32_t e = r * 64 + ln;
+    const uint32_t id = e < nv ? a.v_ids[(size_t)i * a.v_stride + e] : kInvalid;
+    const bool ok = kvalid(id) && id != p;
+    key[r] = ok ? key64(a.v_d[(size_t)i * a.v_stride + e], id) : ~0ull;
+    m += popc(ballot(ok));
+  }
+  // V_i holds distinct ids: the sort alone gives the candidate order
+  wave_sort64<NR>(key);
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    spos[r * 64 + ln] = (uint32_t)key[r];
+    dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
+  }
+  __syncthreads();
+  uint32_t evals = 0;
+  const int nsel = prune_vec<KIND, NR, NPB>(P, p, m, R, a.coef, spos, dpos, st, oid, od, evals);
+  if (ln < (int)R) {
+    const bool in = ln < nsel;
+    const uint32_t sid = in ? oid[ln] : kInvalid;
+    P.adj[(size_t)p * R + ln] = sid;
+    a.rec_t[(size_t)i * R + ln] = sid;
+    a.rec_s[(size_t)i * R + ln] = p;
+    a.rec_d[(size_t)i * R + ln] = in ? od[ln] : 0.0f;
+  }
+  if (ln == 0) {
+    P.deg[p] = (uint32_t)nsel;
+    atomicAdd(&a.ds->fwd_prunes, 1ull);
+    atomicAdd(&a.ds->fwd_evals, (unsigned long long)evals);
+    atomicAdd(&a.ds->records, (unsigned long long)nsel);
+  }
+}
+
 // LDS bytes for staging `rows` candidate rows plus the node's own row.
 static size_t staged_bytes(size_t stride, uint32_t rows) { return (size_t)(rows + 1) * lds_stride(stride); }
 constexpr size_t kMaxStagedLds = 16 * 1024;  // larger footprints limit occupancy more than staging saves
@@ -1184,6 +1493,15 @@ hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPrune
     GR_DISPATCH_N(max_iters, {
       if (a.pool.nch == 8) hipLaunchKernelGGL((k_fwd_prune_mr<2, NR>), dim3(a.n), dim3(64), 0, st, a);
       else hipLaunchKernelGGL((k_fwd_prune_mr<1, NR>), dim3(a.n), dim3(64), 0, st, a);
+      return hipGetLastError();
+    });
+  }
+  // fp32 rows longer than 128 floats: one lane per candidate (the per-pivot
+  // walk of the general kernel costs more there; measured at d = 96 and 960)
+  if (kind != kU8L2 && a.pool.R <= 64 && a.pool.nch > 32) {
+    GR_DISPATCH_N(max_iters, {
+      if (kind == kF32L2) hipLaunchKernelGGL((k_fwd_prune_vec<kF32L2, NR>), dim3(a.n), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_fwd_prune_vec<kF32IP, NR>), dim3(a.n), dim3(64), 0, st, a);
       return hipGetLastError();
     });
   }
@@ -1210,6 +1528,12 @@ template <int KIND, int LPV, int CPL, int NP, int NC>
 static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {
   const size_t lds = staged_bytes(a.pool.stride, 64 * NC);
   const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NC);
+  if constexpr (KIND != kU8L2 && NC == 2 && NP == 1) {
+    if (a.pool.R <= 64) {
+      hipLaunchKernelGGL((k_rebuild_vec<KIND>), dim3(grid), dim3(64), 0, st, a);
+      return;
+    }
+  }
   if constexpr (KIND == kU8L2 && NC == 2 && NP == 1) {
     if (a.pool.R <= 64 && a.pool.nch == 8) {
       hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(grid), dim3(64), 0, st, a);
