@@ -177,7 +177,10 @@ typedef struct {
   uint64_t phase_calls[GRAND_NPHASE];
 } grand_stats_t;
 
-/* Enables (1) or disables (0) per-phase HIP event timing on the stream. */
+/* Enables (1) or disables (0) per-phase HIP event timing on the stream.
+ * Phases of a few microseconds (validate, stage, clear, medoid) are not
+ * timed, since each recorded event adds a short gap on the stream; their
+ * phase_ms stay 0. */
 grand_status grand_set_timing(grand_index *h, int enable);
 grand_status grand_get_stats(grand_index *h, grand_stats_t *out);
 grand_status grand_reset_stats(grand_index *h);

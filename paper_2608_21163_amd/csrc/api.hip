@@ -106,18 +106,24 @@ hipEvent_t get_event(grand_index *h) {
 }
 
 // Records HIP events around one phase of a call when timing is enabled.
+// Phases of a few microseconds (validation, staging, clearing, the medoid
+// check) are not timed: every recorded event leaves a gap of several
+// microseconds between kernels on the stream.
+static bool timed_phase(int ph) {
+  return ph != GRAND_PH_VALIDATE && ph != GRAND_PH_STAGE && ph != GRAND_PH_CLEAR && ph != GRAND_PH_MEDOID;
+}
 struct Phase {
   grand_index *h;
   int ph;
   Phase(grand_index *h_, int ph_) : h(h_), ph(ph_) {
-    if (!h->timing) return;
+    if (!h->timing || !timed_phase(ph)) return;
     hipEvent_t e = get_event(h);
     if (!e) return;
     (void)hipEventRecord(e, h->stream);
     h->pending.emplace_back(ph, e, nullptr);
   }
   ~Phase() {
-    if (!h->timing || h->pending.empty()) return;
+    if (!h->timing || !timed_phase(ph) || h->pending.empty()) return;
     auto &last = h->pending.back();
     if (std::get<0>(last) != ph || std::get<2>(last) != nullptr) return;
     hipEvent_t e = get_event(h);
