@@ -1524,23 +1524,39 @@ hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPrune
   return hipErrorInvalidValue;
 }
 
+// Workgroups of 64 lanes of `kern` (no dynamic LDS) that are resident on
+// the current device at once, or 0 if the runtime cannot say.  A persistent
+// loop over a queue split over exactly this many workgroups leaves no
+// workgroup to start after the first ones finish.
+static uint32_t resident_blocks(const void *kern) {
+  int dev = 0, ncu = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, 64, 0) != hipSuccess) return 0;
+  return per > 0 && ncu > 0 ? (uint32_t)per * (uint32_t)ncu : 0u;
+}
+static uint32_t clamp_resident(uint32_t grid, uint32_t res) { return res && res < grid ? res : grid; }
+
 template <int KIND, int LPV, int CPL, int NP, int NC>
 static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {
   const size_t lds = staged_bytes(a.pool.stride, 64 * NC);
   const size_t mlds = mfma_lds_bytes(a.pool.stride, 64 * NC);
   if constexpr (KIND != kU8L2 && NC == 2 && NP == 1) {
     if (a.pool.R <= 64) {
-      hipLaunchKernelGGL((k_rebuild_vec<KIND>), dim3(grid), dim3(64), 0, st, a);
+      static const uint32_t res = resident_blocks((const void *)k_rebuild_vec<KIND>);
+      hipLaunchKernelGGL((k_rebuild_vec<KIND>), dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
       return;
     }
   }
   if constexpr (KIND == kU8L2 && NC == 2 && NP == 1) {
     if (a.pool.R <= 64 && a.pool.nch == 8) {
-      hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(grid), dim3(64), 0, st, a);
+      static const uint32_t res = resident_blocks((const void *)k_rebuild_mr<2>);
+      hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
       return;
     }
     if (a.pool.R <= 64 && a.pool.nch == 4) {
-      hipLaunchKernelGGL(k_rebuild_mr<1>, dim3(grid), dim3(64), 0, st, a);
+      static const uint32_t res = resident_blocks((const void *)k_rebuild_mr<1>);
+      hipLaunchKernelGGL(k_rebuild_mr<1>, dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
       return;
     }
   }
