@@ -29,6 +29,7 @@ struct grand_index {
   uint32_t *bidx = nullptr, *mark = nullptr, *cnt = nullptr, *off = nullptr, *dirty = nullptr, *queue = nullptr, *qflag = nullptr;
   uint32_t *rev_off = nullptr, *rev_src = nullptr, *rev_sorted = nullptr, *scan_tmp = nullptr;
   RevBufs rev{};  // bucketed full reverse-graph build
+  GroupBufs grp{};  // two-level grouping of records (null members: one-level form)
   size_t rev_sorted_cap = 0;
   void *med_tmp = nullptr;
   uint32_t epoch = 0;
@@ -209,13 +210,20 @@ grand_status ensure_records(grand_index *h, size_t n) {
   HCHK(h, hipStreamSynchronize(h->stream));
   size_t nc = std::max<size_t>(n, h->rcap + h->rcap / 2);
   dfree(h->rec_t); dfree(h->rec_s); dfree(h->rec_d); dfree(h->gsrc); dfree(h->gd);
+  dfree(h->grp.pt); dfree(h->grp.ps); dfree(h->grp.pd); dfree(h->grp.mat); dfree(h->grp.mato); dfree(h->grp.tmp);
   h->rcap = 0;
+  h->grp.rcap = 0;
+  const bool two = group_two_level(h->p.capacity);
+  const size_t mw = two ? group_mat_words(h->p.capacity, nc) : 0;
   if (dalloc(&h->rec_t, nc) || dalloc(&h->rec_s, nc) || dalloc(&h->rec_d, nc) || dalloc(&h->gsrc, nc) ||
-      dalloc(&h->gd, nc)) {
+      dalloc(&h->gd, nc) ||
+      (two && (dalloc(&h->grp.pt, nc) || dalloc(&h->grp.ps, nc) || dalloc(&h->grp.pd, nc) ||
+               dalloc(&h->grp.mat, mw) || dalloc(&h->grp.mato, mw) || dalloc(&h->grp.tmp, scan_tmp_words(mw))))) {
     (void)hipGetLastError();
     return fail(h, GRAND_E_OOM, "device allocation of record buffers failed");
   }
   h->rcap = nc;
+  if (two) h->grp.rcap = nc;
   return GRAND_OK;
 }
 
@@ -249,8 +257,9 @@ uint32_t persistent_grid(size_t upper) {
 
 grand_status run_group(grand_index *h, size_t nrec) {
   Phase ph(h, GRAND_PH_GROUP);
+  const GroupBufs *gb = h->grp.dpad && h->grp.rcap >= nrec ? &h->grp : nullptr;
   HCHK(h, launch_group(h->rec_t, h->rec_s, h->rec_d, nrec, h->p.capacity, h->cnt, h->off, h->scan_tmp, h->gsrc,
-                       h->gd, h->dirty, h->ds, h->stream));
+                       h->gd, h->dirty, h->ds, gb, h->stream));
   return GRAND_OK;
 }
 
@@ -541,6 +550,8 @@ void release(grand_index *h) {
   dfree(h->b_ids); dfree(h->v_ids); dfree(h->v_n); dfree(h->c_ids); dfree(h->rcount); dfree(h->rofs);
   dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs);
   dfree(h->rec_t); dfree(h->rec_s); dfree(h->rec_d); dfree(h->gsrc); dfree(h->gd);
+  dfree(h->grp.pt); dfree(h->grp.ps); dfree(h->grp.pd); dfree(h->grp.mat); dfree(h->grp.mato); dfree(h->grp.tmp);
+  dfree(h->grp.dpad); dfree(h->grp.dcnt);
   dfree(h->q_vecs); dfree(h->q_ids); dfree(h->q_d);
   for (auto &t : h->pending) {
     if (std::get<1>(t)) (void)hipEventDestroy(std::get<1>(t));
@@ -627,6 +638,8 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
              (h->rev.plan.two && (dalloc(&h->rev.pairs2, rev_pair_words(h->rev.plan, p->capacity, p->R)) ||
                                   dalloc(&h->rev.bh2, rev_fine_words(h->rev.plan)) ||
                                   dalloc(&h->rev.bo2, rev_fine_words(h->rev.plan)))) ||
+             (group_two_level(p->capacity) && (dalloc(&h->grp.dpad, group_pad_words(p->capacity)) ||
+                                               dalloc(&h->grp.dcnt, group_buckets(p->capacity)))) ||
              dalloc(&h->ds, 1) ||
              hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
              hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess ||

@@ -183,9 +183,29 @@ hipError_t launch_stage(PoolView p, const uint8_t *rows, const uint32_t *ids, ui
 hipError_t launch_mark_batch(const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t *bidx, uint8_t v,
                              hipStream_t s);
 hipError_t launch_clear_rows(PoolView p, const uint32_t *ids, uint32_t n, hipStream_t s);
+// Buffers of the two-level grouping (capacities up to 2^24 ids).
+struct GroupBufs {
+  uint32_t *pt, *ps;  // records moved to their coarse buckets: targets, sources
+  float *pd;          // and distances (rcap each)
+  uint32_t *mat;      // per (coarse bucket, record tile) counts, group_mat_words
+  uint32_t *mato;     // their exclusive scan, group_mat_words
+  uint32_t *tmp;      // scan scratch, scan_tmp_words(group_mat_words)
+  uint32_t *dpad;     // targets with a record, per coarse bucket, group_pad_words
+  uint32_t *dcnt;     // their number per coarse bucket, group_buckets
+  size_t rcap;        // records the buffers hold
+};
+uint32_t group_buckets(uint32_t cap);
+bool group_two_level(uint32_t cap);
+size_t group_mat_words(uint32_t cap, size_t rcap);
+size_t group_pad_words(uint32_t cap);
+// Groups the records by target: off[0..cap] group offsets, gsrc/gd the
+// grouped sources and distances, dirty[0..n_dirty) the targets with a
+// record in ascending order (ds->n_dirty).  gb selects the two-level form
+// (no global atomics) when the capacity allows it; else the one-level form
+// with `cnt` (all zero before and after).
 hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec,
                         uint32_t cap, uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc,
-                        float *gd, uint32_t *dirty, DevScalars *ds, hipStream_t s);
+                        float *gd, uint32_t *dirty, DevScalars *ds, const GroupBufs *gb, hipStream_t s);
 hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s);
 // out[0..k) = the items[i] with flags[i] != 0, i < *n (n on the device, at
 // most cap), in order; *out_n = k.

@@ -368,9 +368,154 @@ __global__ void k_group_scatter(const uint32_t *rec_t, const uint32_t *rec_s, co
   }
 }
 
+// Two-level form (capacities up to 2^24 ids), with no global atomics:
+//  count  per tile of kGrpTile records, LDS counts of the coarse buckets
+//         (target >> kGrpShift), stored at mat[bucket * ntiles + tile];
+//  scan   of mat (bucket-major): mato[bucket * ntiles + tile] is where the
+//         tile's records of that bucket start;
+//  part   the same tiles move their records there (LDS cursors);
+//  bucket one workgroup per coarse bucket counts its records per target in
+//         LDS, writes the group offsets of its kGrpWidth targets and its
+//         targets with a record (ascending) to its pad row, and moves the
+//         records into their groups (LDS cursors);
+//  dirty  each pad row is copied after those of the buckets before it, so
+//         the dirty list is in ascending id order as in the one-level form.
+constexpr int kGrpShift = 12;
+constexpr uint32_t kGrpWidth = 1u << kGrpShift;
+constexpr int kGrpThreads = 256;
+constexpr int kGrpPer = 8;
+constexpr uint32_t kGrpTile = kGrpThreads * kGrpPer;
+constexpr uint32_t kGrpMaxBuckets = 4096;
+constexpr int kGrpBucketThreads = 1024;
+
+uint32_t group_buckets(uint32_t cap) { return (uint32_t)(((size_t)cap + kGrpWidth - 1) >> kGrpShift); }
+bool group_two_level(uint32_t cap) { return group_buckets(cap) <= kGrpMaxBuckets; }
+size_t group_mat_words(uint32_t cap, size_t rcap) {
+  return (size_t)group_buckets(cap) * ((rcap + kGrpTile - 1) / kGrpTile) + 1;
+}
+size_t group_pad_words(uint32_t cap) { return (size_t)group_buckets(cap) * kGrpWidth; }
+
+__global__ __launch_bounds__(kGrpThreads) void k_grp_count(const uint32_t *rec_t, size_t nrec, uint32_t cap,
+                                                           uint32_t nb1, uint32_t ntiles, uint32_t *mat) {
+  __shared__ uint32_t h[kGrpMaxBuckets];
+  for (uint32_t b = threadIdx.x; b < nb1; b += kGrpThreads) h[b] = 0;
+  __syncthreads();
+  const size_t base = (size_t)blockIdx.x * kGrpTile + threadIdx.x;
+  uint32_t t[kGrpPer];
+#pragma unroll
+  for (int k = 0; k < kGrpPer; k++) {
+    const size_t i = base + (size_t)k * kGrpThreads;
+    t[k] = i < nrec ? rec_t[i] : kInvalid;
+  }
+#pragma unroll
+  for (int k = 0; k < kGrpPer; k++)
+    if (t[k] < cap) atomicAdd(&h[t[k] >> kGrpShift], 1u);
+  __syncthreads();
+  for (uint32_t b = threadIdx.x; b < nb1; b += kGrpThreads) mat[(size_t)b * ntiles + blockIdx.x] = h[b];
+}
+
+__global__ __launch_bounds__(kGrpThreads) void k_grp_part(const uint32_t *rec_t, const uint32_t *rec_s,
+                                                          const float *rec_d, size_t nrec, uint32_t cap, uint32_t nb1,
+                                                          uint32_t ntiles, const uint32_t *mato, uint32_t *pt,
+                                                          uint32_t *ps, float *pd) {
+  __shared__ uint32_t cur[kGrpMaxBuckets];
+  for (uint32_t b = threadIdx.x; b < nb1; b += kGrpThreads) cur[b] = mato[(size_t)b * ntiles + blockIdx.x];
+  __syncthreads();
+  const size_t base = (size_t)blockIdx.x * kGrpTile + threadIdx.x;
+  uint32_t t[kGrpPer];
+#pragma unroll
+  for (int k = 0; k < kGrpPer; k++) {
+    const size_t i = base + (size_t)k * kGrpThreads;
+    t[k] = i < nrec ? rec_t[i] : kInvalid;
+  }
+#pragma unroll
+  for (int k = 0; k < kGrpPer; k++) {
+    if (t[k] >= cap) continue;
+    const size_t i = base + (size_t)k * kGrpThreads;
+    const uint32_t pos = atomicAdd(&cur[t[k] >> kGrpShift], 1u);
+    pt[pos] = t[k];
+    ps[pos] = rec_s[i];
+    pd[pos] = rec_d[i];
+  }
+}
+
+__global__ __launch_bounds__(kGrpBucketThreads) void k_grp_bucket(const uint32_t *pt, const uint32_t *ps,
+                                                                  const float *pd, uint32_t cap, uint32_t nb1,
+                                                                  uint32_t ntiles, const uint32_t *mato, uint32_t *off,
+                                                                  uint32_t *gsrc, float *gd, uint32_t *dpad,
+                                                                  uint32_t *dcnt) {
+  constexpr int kq = kGrpWidth / kGrpBucketThreads;  // targets per thread in the scan
+  __shared__ uint32_t h[kGrpWidth];
+  __shared__ uint32_t wsum[kGrpBucketThreads / 64];
+  const uint32_t b = blockIdx.x;
+  const uint32_t lo = mato[(size_t)b * ntiles], hi = mato[(size_t)(b + 1) * ntiles];
+  for (uint32_t k = threadIdx.x; k < kGrpWidth; k += kGrpBucketThreads) h[k] = 0;
+  __syncthreads();
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kGrpBucketThreads) atomicAdd(&h[pt[i] & (kGrpWidth - 1)], 1u);
+  __syncthreads();
+  uint32_t c[kq], sum = 0, nz = 0;
+#pragma unroll
+  for (int k = 0; k < kq; k++) {
+    c[k] = h[kq * threadIdx.x + k];
+    sum += c[k];
+    nz += c[k] != 0u;
+  }
+  uint32_t total, ndirty;
+  uint32_t run = lo + block_excl_scan(sum, wsum, total);
+  uint32_t frun = block_excl_scan(nz, wsum, ndirty);
+  const uint32_t t0 = (b << kGrpShift) + kq * threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < kq; k++) {
+    const uint32_t t = t0 + k;
+    if (t < cap) off[t] = run;
+    if (c[k]) dpad[(size_t)b * kGrpWidth + frun++] = t;
+    h[kq * threadIdx.x + k] = run;  // this thread's own entries become cursors
+    run += c[k];
+  }
+  if (threadIdx.x == 0) {
+    dcnt[b] = ndirty;
+    if (b == nb1 - 1) off[cap] = hi;
+  }
+  __syncthreads();
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kGrpBucketThreads) {
+    const uint32_t pos = atomicAdd(&h[pt[i] & (kGrpWidth - 1)], 1u);
+    gsrc[pos] = ps[i];
+    gd[pos] = pd[i];
+  }
+}
+
+__global__ __launch_bounds__(kGrpThreads) void k_grp_dirty(const uint32_t *dpad, const uint32_t *dcnt, uint32_t nb1,
+                                                           uint32_t *dirty, DevScalars *ds) {
+  __shared__ uint32_t wsum[kGrpThreads / 64];
+  const uint32_t b = blockIdx.x;
+  uint32_t s = 0;
+  for (uint32_t k = threadIdx.x; k < b; k += kGrpThreads) s += dcnt[k];
+  uint32_t before;
+  block_excl_scan(s, wsum, before);
+  const uint32_t n = dcnt[b];
+  for (uint32_t k = threadIdx.x; k < n; k += kGrpThreads) dirty[before + k] = dpad[(size_t)b * kGrpWidth + k];
+  if (b == nb1 - 1 && threadIdx.x == 0) ds->n_dirty = before + n;
+}
+
 hipError_t launch_group(const uint32_t *rec_t, const uint32_t *rec_s, const float *rec_d, size_t nrec, uint32_t cap,
                         uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *gsrc, float *gd,
-                        uint32_t *dirty, DevScalars *ds, hipStream_t s) {
+                        uint32_t *dirty, DevScalars *ds, const GroupBufs *gb, hipStream_t s) {
+  if (gb && group_two_level(cap) && cap > 0) {
+    if (nrec > gb->rcap) return hipErrorInvalidValue;
+    const uint32_t nb1 = group_buckets(cap);
+    const uint32_t ntiles = (uint32_t)((nrec + kGrpTile - 1) / kGrpTile);
+    if (ntiles)
+      hipLaunchKernelGGL(k_grp_count, dim3(ntiles), dim3(kGrpThreads), 0, s, rec_t, nrec, cap, nb1, ntiles, gb->mat);
+    hipError_t e = launch_scan(gb->mat, gb->mato, (size_t)nb1 * ntiles, gb->tmp, s);
+    if (e != hipSuccess) return e;
+    if (ntiles)
+      hipLaunchKernelGGL(k_grp_part, dim3(ntiles), dim3(kGrpThreads), 0, s, rec_t, rec_s, rec_d, nrec, cap, nb1,
+                         ntiles, gb->mato, gb->pt, gb->ps, gb->pd);
+    hipLaunchKernelGGL(k_grp_bucket, dim3(nb1), dim3(kGrpBucketThreads), 0, s, gb->pt, gb->ps, gb->pd, cap, nb1,
+                       ntiles, gb->mato, off, gsrc, gd, gb->dpad, gb->dcnt);
+    hipLaunchKernelGGL(k_grp_dirty, dim3(nb1), dim3(kGrpThreads), 0, s, gb->dpad, gb->dcnt, nb1, dirty, ds);
+    return hipGetLastError();
+  }
   uint32_t g = blocks_for(nrec, 256);
   if (g > 8192) g = 8192;
   if (nrec) hipLaunchKernelGGL(k_group_hist, dim3(g), dim3(256), 0, s, rec_t, nrec, cnt);
