@@ -305,3 +305,54 @@ def test_reverse_graph_large_random_graph_is_exact_transpose():
     want_off = np.cumsum(want_off)
     assert np.array_equal(e["rev_offsets"].astype(np.int64), want_off)
     assert np.array_equal(e["rev_srcs"].astype(np.int64), src[order])
+
+
+def test_large_capacity_forms_match_the_small_index():
+    """A capacity just above 2^24 ids takes the one-level forms of the
+    record grouping (global atomics) and of the search's visited hash
+    (16-bit tags); a 12,000-slot index takes the two-level grouping and the
+    8-bit hash.  Both receive the same batches, with ids below 12,000 only,
+    so the graphs, the reverse graphs and the query results must be
+    identical (uint8 distances are exact on both)."""
+    import dataclasses
+
+    from helpers import canonical_rows
+    from paper_2608_21163_amd import GrandIndex
+    say("[large capacity forms] u8_d128")
+    w = _workload("u8_d128")
+    small = w.cfg
+    big = dataclasses.replace(small, capacity=(1 << 24) + 1)
+    gs = GrandIndex.from_config(small, max_batch=2_000)
+    gb = GrandIndex.from_config(big, max_batch=2_000)
+    for op in w.base_batches():
+        gs.insert(op.ids, op.vecs)
+        gb.insert(op.ids, op.vecs)
+    n = small.capacity
+
+    def same(tag):
+        a, b = gs.export(with_reverse=True), gb.export(with_reverse=True)
+        assert np.array_equal(a["active"], b["active"][:n]) and not b["active"][n:].any(), tag
+        assert a["medoid"] == b["medoid"], tag
+        assert np.array_equal(a["deg"], b["deg"][:n]), tag
+        assert np.array_equal(canonical_rows(a["adj"]), canonical_rows(b["adj"][:n])), tag
+        assert np.array_equal(a["rev_offsets"], b["rev_offsets"][: n + 1]), tag
+        assert (b["rev_offsets"][n:] == a["rev_offsets"][n]).all(), tag
+        assert np.array_equal(a["rev_srcs"], b["rev_srcs"]), tag
+
+    same("base")
+    for r, ops in w.rounds(1):
+        for op in ops:
+            if op.kind == "insert":
+                gs.insert(op.ids, op.vecs)
+                gb.insert(op.ids, op.vecs)
+                same(f"round {r} insert")
+            elif op.kind == "delete":
+                gs.delete(op.ids)
+                gb.delete(op.ids)
+                same(f"round {r} delete")
+            else:
+                si, sd = gs.search(op.vecs, 10, 64)
+                bi, bd = gb.search(op.vecs, 10, 64)
+                assert np.array_equal(si, bi) and np.array_equal(sd, bd)
+    gs.close()
+    gb.close()
