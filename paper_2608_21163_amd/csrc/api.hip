@@ -137,7 +137,7 @@ struct Phase {
 // End of every call: wait for the stream, fold timings, refresh the host
 // mirror of the device scalars (medoid, counters).
 grand_status finish(grand_index *h) {
-  HCHK(h, hipMemcpyAsync(h->hs, h->ds, sizeof(DevScalars), hipMemcpyDeviceToHost, h->stream));
+  HCHK(h, hipMemcpyAsync(h->hs, h->ds, kScalarBytes, hipMemcpyDeviceToHost, h->stream));
   HCHK(h, hipStreamSynchronize(h->stream));
   for (auto &t : h->pending) {
     float ms = 0.0f;
@@ -164,7 +164,7 @@ grand_status check_usable(grand_index *h) {
 
 // Reads the validation result (one synchronisation) and maps it to a status.
 grand_status read_validation(grand_index *h) {
-  HCHK(h, hipMemcpyAsync(h->hs, h->ds, sizeof(DevScalars), hipMemcpyDeviceToHost, h->stream));
+  HCHK(h, hipMemcpyAsync(h->hs, h->ds, kScalarBytes, hipMemcpyDeviceToHost, h->stream));
   HCHK(h, hipStreamSynchronize(h->stream));
   const uint32_t code = h->hs->err_code, id = h->hs->err_id;
   if (code == 0) return GRAND_OK;
@@ -923,23 +923,28 @@ grand_status grand_get_stats(grand_index *h, grand_stats_t *out) {
   if (s != GRAND_OK) return s;
   if (!out || out->struct_size != sizeof(grand_stats_t)) return fail(h, GRAND_E_ARG, "bad stats struct");
   if ((s = finish(h)) != GRAND_OK) return s;
+  HCHK(h, hipMemcpyAsync(h->hs->stat, h->ds->stat, sizeof(h->hs->stat), hipMemcpyDeviceToHost, h->stream));
+  HCHK(h, hipStreamSynchronize(h->stream));
+  unsigned long long c[kStatCount] = {};
+  for (int slot = 0; slot < kStatSlots; slot++)
+    for (int k = 0; k < kStatCount; k++) c[k] += h->hs->stat[(size_t)slot * kStatWords + k];
   grand_stats_t r = h->st;
   for (int i = 0; i < 3; i++) {
-    r.search_hops[i] = h->hs->hops[i];
-    r.search_evals[i] = h->hs->evals[i];
+    r.search_hops[i] = c[kStHops + i];
+    r.search_evals[i] = c[kStEvals + i];
   }
-  r.fwd_evals = h->hs->fwd_evals;
-  r.fwd_prunes = h->hs->fwd_prunes;
-  r.rebuild_evals = h->hs->rb_evals;
-  r.rebuild_prunes = h->hs->rb_prunes;
-  r.dirty = h->hs->dirty;
-  r.rebuild_records = h->hs->rb_recs;
-  r.records = h->hs->records;
-  r.rev_edges = h->hs->rev_edges;
-  r.repair_evals = h->hs->rep_evals;
-  r.rebuild_rows = h->hs->rb_cand;
-  r.repair_rows = h->hs->rep_rows;
-  r.repair_records = h->hs->rep_recs;
+  r.fwd_evals = c[kStFwdEvals];
+  r.fwd_prunes = c[kStFwdPrunes];
+  r.rebuild_evals = c[kStRbEvals];
+  r.rebuild_prunes = c[kStRbPrunes];
+  r.dirty = c[kStDirty];
+  r.rebuild_records = c[kStRbRecs];
+  r.records = c[kStRecords];
+  r.rev_edges = c[kStRevEdges];
+  r.repair_evals = c[kStRepEvals];
+  r.rebuild_rows = c[kStRbCand];
+  r.repair_rows = c[kStRepRows];
+  r.repair_records = c[kStRepRecs];
   *out = r;
   return GRAND_OK;
 }
@@ -952,7 +957,7 @@ grand_status grand_reset_stats(grand_index *h) {
   memset(&h->st, 0, sizeof h->st);
   h->st.struct_size = sizeof(grand_stats_t);
   h->st.timing_enabled = t;
-  HCHK(h, hipMemsetAsync(h->ds, 0, offsetof(DevScalars, err_code), h->stream));
+  HCHK(h, hipMemsetAsync(h->ds->stat, 0, sizeof(h->ds->stat), h->stream));
   HCHK(h, hipStreamSynchronize(h->stream));
   return GRAND_OK;
 }

@@ -2,6 +2,7 @@
 // kernel translation units of the library.
 #pragma once
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include <string>
@@ -11,32 +12,52 @@
 
 namespace gr {
 
-// Device-side counters and small scalars, one struct per index.
+// Work counters.  Many workgroups finish at the same moment, and device
+// atomics on one address are serialised, so every counter is spread over
+// kStatSlots slots (slot rows of kStatWords words, 256 bytes apart):
+// workgroup b adds into slot b % kStatSlots, and the host sums the slots
+// when it reads the counters.
+enum StatId {
+  kStHops = 0,     // nodes expanded by [insert, delete, query] searches (3)
+  kStEvals = 3,    // row gathers of those searches (3)
+  kStFwdEvals = 6, // pairwise distances in forward prunes
+  kStFwdPrunes,
+  kStRbEvals,      // distances in dirty rebuilds (D_u and pairwise)
+  kStRbPrunes,     // rebuilds that pruned
+  kStDirty,        // dirty nodes rebuilt / CAGRA targets / affected nodes
+  kStRbRecs,       // scratch records read by rebuilds
+  kStRecords,      // reverse-edge and repair records emitted
+  kStRevEdges,
+  kStRepEvals,     // distances in delete repair
+  kStRbCand,       // vector rows a pruning rebuild needs: |C| + 1
+  kStRepRows,      // vector rows a repair needs: neighbours + |C_i|
+  kStRepRecs,      // records written by repairs
+  kStatCount
+};
+constexpr int kStatWords = 32;
+constexpr int kStatSlots = 256;
+static_assert(kStatCount <= kStatWords, "stat slot too small");
+
+// Device-side scalars and the work counters, one struct per index.  The
+// scalars come first: the host copies only them after each call.
 struct DevScalars {
-  unsigned long long hops[3];       // nodes expanded by [insert, delete, query] searches
-  unsigned long long evals[3];      // row gathers of those searches
-  unsigned long long fwd_evals;      // pairwise distances in forward prunes
-  unsigned long long fwd_prunes;
-  unsigned long long rb_evals;       // distances in dirty rebuilds (D_u and pairwise)
-  unsigned long long rb_prunes;      // rebuilds that pruned
-  unsigned long long dirty;          // dirty nodes rebuilt / CAGRA targets / affected nodes
-  unsigned long long rb_recs;        // scratch records read by rebuilds
-  unsigned long long records;        // reverse-edge and repair records emitted
-  unsigned long long rev_edges;
-  unsigned long long rep_evals;      // distances in delete repair
-  unsigned long long rb_cand;        // vector rows a pruning rebuild needs: |C| + 1
-  unsigned long long rep_rows;       // vector rows a repair needs: neighbours + |C_i|
-  unsigned long long rep_recs;       // records written by repairs
   uint32_t err_code;                // first validation error (0 = none)
   uint32_t err_id;
   uint32_t n_dirty;                 // number of entries in the dirty / affected list
   uint32_t n_queue;                 // dirty nodes left by the fast rebuild for the general one
   uint32_t medoid;
-  unsigned long long best_bits;     // medoid search: smallest squared distance (bit pattern)
   uint32_t best_id;
+  unsigned long long best_bits;     // medoid search: smallest squared distance (bit pattern)
   uint32_t need_medoid;             // medoid kernels run only when set
+  uint32_t pad_;
   unsigned long long n_count;       // scratch counter (active ids at import)
+  unsigned long long stat[kStatSlots * kStatWords];
 };
+constexpr size_t kScalarBytes = offsetof(DevScalars, stat);
+
+__device__ __forceinline__ void stat_add(DevScalars *ds, int id, unsigned long long v) {
+  if (v) atomicAdd(&ds->stat[(size_t)(blockIdx.x % kStatSlots) * kStatWords + id], v);
+}
 
 enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4 };
 

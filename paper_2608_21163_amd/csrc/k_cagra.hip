@@ -124,7 +124,7 @@ __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
     nodes++;
     __syncthreads();
   }
-  if (ln == 0 && nodes) atomicAdd(&a.ds->dirty, (unsigned long long)nodes);  // one counter update per wave
+  if (ln == 0 && nodes) stat_add(a.ds, kStDirty, (unsigned long long)nodes);  // one counter update per wave
 }
 hipError_t launch_cagra_detour(const CagraArgs &a, uint32_t grid, hipStream_t s) {
   if (grid == 0) return hipSuccess;
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
     if (ln == 0) P.deg[u] = (uint32_t)popc(m);
     nodes++;
   }
-  if (ln == 0 && nodes) atomicAdd(&a.ds->dirty, (unsigned long long)nodes);  // one counter update per wave
+  if (ln == 0 && nodes) stat_add(a.ds, kStDirty, (unsigned long long)nodes);  // one counter update per wave
 }
 hipError_t launch_cagra_pickone(const CagraArgs &a, uint32_t grid, hipStream_t s) {
   if (grid == 0) return hipSuccess;

@@ -569,7 +569,7 @@ __global__ void k_rev_scatter(PoolView P, int by_batch, const uint8_t *in_batch,
   }
 }
 __global__ void k_count_edges(const uint32_t *off, uint32_t nrows, DevScalars *ds) {
-  if (threadIdx.x == 0) atomicAdd(&ds->rev_edges, (unsigned long long)off[nrows]);
+  if (threadIdx.x == 0) stat_add(ds, kStRevEdges, (unsigned long long)off[nrows]);
 }
 
 // Full reverse graph without global atomics, as a two-level counting sort:

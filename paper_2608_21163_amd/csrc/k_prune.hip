@@ -739,9 +739,9 @@ __global__ __launch_bounds__(64) void k_fwd_prune_mr(FwdPruneArgs a) {
   }
   if (ln == 0) {
     P.deg[p] = (uint32_t)nsel;
-    atomicAdd(&a.ds->fwd_prunes, 1ull);
-    atomicAdd(&a.ds->fwd_evals, evals);
-    atomicAdd(&a.ds->records, (unsigned long long)nsel);
+    stat_add(a.ds, kStFwdPrunes, 1ull);
+    stat_add(a.ds, kStFwdEvals, evals);
+    stat_add(a.ds, kStRecords, (unsigned long long)nsel);
   }
 }
 
@@ -804,9 +804,9 @@ __global__ __launch_bounds__(64) void k_fwd_prune(FwdPruneArgs a) {
   }
   if (ln == 0) {
     P.deg[p] = (uint32_t)nsel;
-    atomicAdd(&a.ds->fwd_prunes, 1ull);
-    atomicAdd(&a.ds->fwd_evals, evals);
-    atomicAdd(&a.ds->records, (unsigned long long)nsel);
+    stat_add(a.ds, kStFwdPrunes, 1ull);
+    stat_add(a.ds, kStFwdEvals, evals);
+    stat_add(a.ds, kStRecords, (unsigned long long)nsel);
   }
 }
 
@@ -915,12 +915,12 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
     __syncthreads();
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->rb_prunes, prunes);
-    atomicAdd(&a.ds->rb_evals, evals);
-    atomicAdd(&a.ds->rb_cand, cand);
+    stat_add(a.ds, kStRbPrunes, prunes);
+    stat_add(a.ds, kStRbEvals, evals);
+    stat_add(a.ds, kStRbCand, cand);
     if (a.count_nodes) {
-      atomicAdd(&a.ds->dirty, nodes);
-      atomicAdd(&a.ds->rb_recs, recs);
+      stat_add(a.ds, kStDirty, nodes);
+      stat_add(a.ds, kStRbRecs, recs);
     }
   }
 }
@@ -1073,12 +1073,12 @@ __global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
     __syncthreads();
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->rb_prunes, prunes);
-    atomicAdd(&a.ds->rb_evals, evals);
-    atomicAdd(&a.ds->rb_cand, cand);
+    stat_add(a.ds, kStRbPrunes, prunes);
+    stat_add(a.ds, kStRbEvals, evals);
+    stat_add(a.ds, kStRbCand, cand);
     if (a.count_nodes) {
-      atomicAdd(&a.ds->dirty, nodes);
-      atomicAdd(&a.ds->rb_recs, recs);
+      stat_add(a.ds, kStDirty, nodes);
+      stat_add(a.ds, kStRbRecs, recs);
     }
   }
 }
@@ -1179,8 +1179,8 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
     tr += __shfl(recs, 16 * k, 64);
   }
   if (ln == 0 && tn) {
-    atomicAdd(&a.ds->dirty, tn);
-    atomicAdd(&a.ds->rb_recs, tr);
+    stat_add(a.ds, kStDirty, tn);
+    stat_add(a.ds, kStRbRecs, tr);
   }
 }
 
@@ -1416,12 +1416,12 @@ __global__ __launch_bounds__(64) void k_rebuild_vec(RebuildArgs a) {
     __syncthreads();
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->rb_prunes, (unsigned long long)prunes);
-    atomicAdd(&a.ds->rb_evals, (unsigned long long)evals);
-    atomicAdd(&a.ds->rb_cand, (unsigned long long)cand);
+    stat_add(a.ds, kStRbPrunes, (unsigned long long)prunes);
+    stat_add(a.ds, kStRbEvals, (unsigned long long)evals);
+    stat_add(a.ds, kStRbCand, (unsigned long long)cand);
     if (a.count_nodes) {
-      atomicAdd(&a.ds->dirty, (unsigned long long)nodes);
-      atomicAdd(&a.ds->rb_recs, (unsigned long long)recs);
+      stat_add(a.ds, kStDirty, (unsigned long long)nodes);
+      stat_add(a.ds, kStRbRecs, (unsigned long long)recs);
     }
   }
 }
@@ -1473,9 +1473,9 @@ __global__ __launch_bounds__(64) void k_fwd_prune_vec(FwdPruneArgs a) {
   }
   if (ln == 0) {
     P.deg[p] = (uint32_t)nsel;
-    atomicAdd(&a.ds->fwd_prunes, 1ull);
-    atomicAdd(&a.ds->fwd_evals, (unsigned long long)evals);
-    atomicAdd(&a.ds->records, (unsigned long long)nsel);
+    stat_add(a.ds, kStFwdPrunes, 1ull);
+    stat_add(a.ds, kStFwdEvals, (unsigned long long)evals);
+    stat_add(a.ds, kStRecords, (unsigned long long)nsel);
   }
 }
 

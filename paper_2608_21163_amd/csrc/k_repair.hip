@@ -144,10 +144,10 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
     }
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->records, recs);
-    atomicAdd(&a.ds->rep_evals, evals);
-    atomicAdd(&a.ds->rep_rows, rows);
-    atomicAdd(&a.ds->rep_recs, recs);
+    stat_add(a.ds, kStRecords, recs);
+    stat_add(a.ds, kStRepEvals, evals);
+    stat_add(a.ds, kStRepRows, rows);
+    stat_add(a.ds, kStRepRecs, recs);
   }
 }
 
@@ -327,10 +327,10 @@ __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
     rc += __shfl_xor(rc, o, 64);
   }
   if (ln == 0 && (ev | rc | rows)) {
-    atomicAdd(&a.ds->records, rc);
-    atomicAdd(&a.ds->rep_evals, ev);
-    atomicAdd(&a.ds->rep_rows, rows);
-    atomicAdd(&a.ds->rep_recs, rc);
+    stat_add(a.ds, kStRecords, rc);
+    stat_add(a.ds, kStRepEvals, ev);
+    stat_add(a.ds, kStRepRows, rows);
+    stat_add(a.ds, kStRepRecs, rc);
   }
 }
 
@@ -477,10 +477,10 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
     rc += __shfl_xor(rc, o, 64);
   }
   if (ln == 0 && (ev | rc | rows)) {
-    atomicAdd(&a.ds->records, rc);
-    atomicAdd(&a.ds->rep_evals, ev);
-    atomicAdd(&a.ds->rep_rows, rows);
-    atomicAdd(&a.ds->rep_recs, rc);
+    stat_add(a.ds, kStRecords, rc);
+    stat_add(a.ds, kStRepEvals, ev);
+    stat_add(a.ds, kStRepRows, rows);
+    stat_add(a.ds, kStRepRecs, rc);
   }
 }
 

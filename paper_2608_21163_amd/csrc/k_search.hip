@@ -153,8 +153,8 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     }
   }
   if (ln == 0) {
-    atomicAdd(&a.ds->hops[a.which], (unsigned long long)nv);
-    atomicAdd(&a.ds->evals[a.which], (unsigned long long)evals);
+    stat_add(a.ds, kStHops + a.which, (unsigned long long)nv);
+    stat_add(a.ds, kStEvals + a.which, (unsigned long long)evals);
   }
 }
 
