@@ -160,6 +160,7 @@ __device__ __forceinline__ void wave_dists(const Slice<KIND, LPV, CPL>& s, const
     uint4 b[RIF][CPL];
 #pragma unroll
     for (int rr = 0; rr < RIF; rr++) {
+      if (rr >= steps) break;
       const int c = base + rr * G + grp;
       const uint8_t* row = vecs + (size_t)(c < cnt ? ids[c] : 0u) * stride;
 #pragma unroll
