@@ -893,12 +893,22 @@ __global__ __launch_bounds__(kRevThreads) void k_rev2_count2(RevPlan rp, const u
   for (uint32_t j = x0 + threadIdx.x; j < a0; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
   for (uint32_t j = a1 + threadIdx.x; j < x1; j += blockDim.x) atomicAdd(&lh[(pairs[j] & m1) >> rp.s2], 1u);
   const uint4 *p4 = reinterpret_cast<const uint4 *>(pairs);
-  for (uint32_t q = a0 / 4 + threadIdx.x; q < a1 / 4; q += blockDim.x) {
-    const uint4 v = p4[q];
-    atomicAdd(&lh[(v.x & m1) >> rp.s2], 1u);
-    atomicAdd(&lh[(v.y & m1) >> rp.s2], 1u);
-    atomicAdd(&lh[(v.z & m1) >> rp.s2], 1u);
-    atomicAdd(&lh[(v.w & m1) >> rp.s2], 1u);
+  const uint32_t qe = a1 / 4;
+  for (uint32_t q = a0 / 4 + threadIdx.x; q < qe; q += 4 * blockDim.x) {
+    uint4 v[4];  // four groups in flight per thread
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      const uint32_t qq = q + (uint32_t)k * blockDim.x;
+      v[k] = qq < qe ? p4[qq] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; k++) {
+      if (q + (uint32_t)k * blockDim.x >= qe) break;
+      atomicAdd(&lh[(v[k].x & m1) >> rp.s2], 1u);
+      atomicAdd(&lh[(v[k].y & m1) >> rp.s2], 1u);
+      atomicAdd(&lh[(v[k].z & m1) >> rp.s2], 1u);
+      atomicAdd(&lh[(v[k].w & m1) >> rp.s2], 1u);
+    }
   }
   __syncthreads();
   for (uint32_t b = threadIdx.x; b < rp.nsub; b += blockDim.x) bh2[((size_t)b1 * rp.nsub + b) * rp.nc2 + c] = lh[b];
@@ -957,9 +967,26 @@ __global__ __launch_bounds__(kFillThreads) void k_rev2_fill(RevPlan rp, uint32_t
   const size_t nfine = (size_t)rp.nb1 * rp.nsub;
   const uint32_t s0 = bo2[(size_t)fb * rp.nc2], s1 = bo2[(size_t)(fb + 1) * rp.nc2];
   const uint32_t m2 = W - 1u;
+  const uint32_t n = s1 - s0;
+  const bool staged = n <= kRev2Stage;
   for (uint32_t i = threadIdx.x; i < W; i += blockDim.x) cnt[i] = 0;
   __syncthreads();
-  for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) atomicAdd(&cnt[pairs2[j] & m2], 1u);
+  // a bucket that fits the stage is read once, all of a thread's pairs in
+  // flight together, and kept in registers for the placement pass
+  constexpr int kPer = kRev2Stage / kFillThreads;
+  uint32_t xr[kPer];
+  if (staged) {
+#pragma unroll
+    for (int k = 0; k < kPer; k++) {
+      const uint32_t j = s0 + (uint32_t)k * blockDim.x + threadIdx.x;
+      xr[k] = j < s1 ? pairs2[j] : 0u;
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; k++)
+      if (s0 + (uint32_t)k * blockDim.x + threadIdx.x < s1) atomicAdd(&cnt[xr[k] & m2], 1u);
+  } else {
+    for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) atomicAdd(&cnt[pairs2[j] & m2], 1u);
+  }
   __syncthreads();
   // offsets: W = 128 counts, thread t < W owns count t
   const uint32_t c = threadIdx.x < W ? cnt[threadIdx.x] : 0u;
@@ -970,12 +997,10 @@ __global__ __launch_bounds__(kFillThreads) void k_rev2_fill(RevPlan rp, uint32_t
   __syncthreads();
   if (threadIdx.x < W) cnt[threadIdx.x] = ex;
   __syncthreads();
-  const uint32_t n = s1 - s0;
-  if (n <= kRev2Stage) {
-    for (uint32_t j = s0 + threadIdx.x; j < s1; j += blockDim.x) {
-      const uint32_t x = pairs2[j];
-      stage[atomicAdd(&cnt[x & m2], 1u)] = x >> rp.s2;
-    }
+  if (staged) {
+#pragma unroll
+    for (int k = 0; k < kPer; k++)
+      if (s0 + (uint32_t)k * blockDim.x + threadIdx.x < s1) stage[atomicAdd(&cnt[xr[k] & m2], 1u)] = xr[k] >> rp.s2;
     __syncthreads();
     for (uint32_t j = threadIdx.x; j < n; j += blockDim.x) src[s0 + j] = stage[j];
   } else {
