@@ -970,6 +970,10 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   return m;
 }
 
+// Candidate tiles a rebuild keeps in registers (|C| <= 80: the kept row and
+// up to 16 records); larger candidate sets take greedy_u8.
+constexpr int kRegTiles = 5;
+
 // Rebuild of dirty nodes for uint8 rows of 64*NK bytes with R <= 64 and
 // R + P <= 128 (the same steps as k_rebuild).  When a node prunes, D_u of
 // every candidate comes from int8 MFMA of u's row against the candidates,
@@ -978,7 +982,7 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
 // candidate tile are live at a time, so many waves fit per SIMD to hide
 // the gathers.
 template <int NK>
-__global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
+__global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
   constexpr int NC = 2;
   __shared__ uint4 rowL[16];
   __shared__ uint32_t cl[64 * NC];
@@ -1019,32 +1023,34 @@ __global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
       }
       np += (int)xshfl((uint32_t)np, 16);
       np += (int)xshfl((uint32_t)np, 32);
-      // every candidate tile is loaded before the first is used
-      constexpr int NT = 4 * NC;
-      uint4 raw[NT][NK];
+      // candidate tiles kRegTiles at a time (one batch when |C| <= 80), all
+      // loads of a batch issued before the first is used
+      for (int t0 = 0; 16 * t0 < m; t0 += kRegTiles) {
+        uint4 raw[kRegTiles][NK];
 #pragma unroll
-      for (int t = 0; t < NT; t++) {
-        const int e = 16 * t + col;
-        const uint8_t *row = P.vecs + (size_t)(e < m ? cl[e] : u) * P.stride + goff;
+        for (int h = 0; h < kRegTiles; h++) {
+          const int e = 16 * (t0 + h) + col;
 #pragma unroll
-        for (int kk = 0; kk < NK; kk++)
-          raw[t][kk] = 16 * t < m ? ld16(row + (size_t)kk * 64) : make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int t = 0; t < NT; t++) {
-        if (16 * t >= m) break;
-        const int e = 16 * t + col;
-        int sq = 0;
-        v4i acc = {0, 0, 0, 0};
-#pragma unroll
-        for (int kk = 0; kk < NK; kk++) {
-          const v4i b = to_i8x16(raw[t][kk]);
-          sq = sq_i8x16(b, sq);
-          acc = mfma_i8(A[kk], b, acc);
+          for (int kk = 0; kk < NK; kk++)
+            raw[h][kk] = e - col < m ? ld16(P.vecs + (size_t)(e < m ? cl[e] : u) * P.stride + goff + (size_t)kk * 64)
+                                     : make_uint4(0, 0, 0, 0);
         }
-        sq += (int)xshfl((uint32_t)sq, 16);
-        sq += (int)xshfl((uint32_t)sq, 32);
-        if (g == 0) dpos[e] = canon0((float)(np + sq - 2 * acc[0]));
+#pragma unroll
+        for (int h = 0; h < kRegTiles; h++) {
+          const int e = 16 * (t0 + h) + col;
+          if (e - col >= m) break;
+          int sq = 0;
+          v4i acc = {0, 0, 0, 0};
+#pragma unroll
+          for (int kk = 0; kk < NK; kk++) {
+            const v4i b = to_i8x16(raw[h][kk]);
+            sq = sq_i8x16(b, sq);
+            acc = mfma_i8(A[kk], b, acc);
+          }
+          sq += (int)xshfl((uint32_t)sq, 16);
+          sq += (int)xshfl((uint32_t)sq, 32);
+          if (g == 0) dpos[e] = canon0((float)(np + sq - 2 * acc[0]));
+        }
       }
     }
     evals += (unsigned long long)m;
@@ -1063,9 +1069,24 @@ __global__ __launch_bounds__(64, 3) void k_rebuild_mr(RebuildArgs a) {
       dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
     }
     __syncthreads();
-    uint32_t ntile = 0;
-    const int nsel = greedy_u8_reg<NK, 4 * NC>(P, u, m, R, a.coef, spos, dpos, thrL, nrmL, oid, od, ntile);
-    evals += 256ull * ntile;
+    int nsel;
+    if (m <= 16 * kRegTiles) {  // every candidate tile resident in registers
+      uint32_t ntile = 0;
+      nsel = greedy_u8_reg<NK, kRegTiles>(P, u, m, R, a.coef, spos, dpos, thrL, nrmL, oid, od, ntile);
+      evals += 256ull * ntile;
+    } else {  // more candidates (more than 16 records): tiles loaded per block
+      bool valid[NC];
+#pragma unroll
+      for (int r = 0; r < NC; r++) valid[r] = r * 64 + ln < m;
+      uint32_t sid;
+      float sdist;
+      nsel = greedy_u8<NK, NC>(P, u, m, R, a.coef, spos, dpos, valid, sid, sdist, evals);
+      if (ln < nsel) {
+        oid[ln] = sid;
+        od[ln] = sdist;
+      }
+      __syncthreads();
+    }
     if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? oid[ln] : kInvalid;
     if (ln == 0) P.deg[u] = (uint32_t)nsel;
     prunes++;
