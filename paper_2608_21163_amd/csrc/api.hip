@@ -536,7 +536,7 @@ bool params_ok(const grand_params *p, std::string &why) {
 
 void release(grand_index *h) {
   if (h->pool.vecs) (void)hipSetDevice(h->p.device);
-  dfree(h->pool.vecs); dfree(h->pool.adj); dfree(h->pool.deg); dfree(h->pool.active);
+  dfree(h->pool.vecs); dfree(h->pool.adj); dfree(h->pool.deg); dfree(h->pool.active); dfree(h->pool.adjd);
   dfree(h->in_batch); dfree(h->bidx); dfree(h->mark); dfree(h->cnt); dfree(h->off); dfree(h->dirty); dfree(h->queue); dfree(h->qflag);
   dfree(h->rev_off); dfree(h->rev_src); dfree(h->rev_sorted); dfree(h->scan_tmp); dfree(h->med_tmp);
   dfree(h->rev.pairs); dfree(h->rev.bh); dfree(h->rev.bo);
@@ -626,7 +626,10 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
   P.nch = h->nch;
   P.R = p->R;
   P.cap = p->capacity;
+  P.adjd = nullptr;
+  const bool stored = p->algo == GRAND_VAMANA && adj_dists_apply(h->kind, p->R, h->nch, p->P);
   bool bad = dalloc(&P.vecs, cap * h->stride) || dalloc(&P.adj, cap * p->R) || dalloc(&P.deg, cap) ||
+             (stored && dalloc(&P.adjd, cap * p->R)) ||
              dalloc(&P.active, cap) || dalloc(&h->in_batch, cap) || dalloc(&h->bidx, cap) ||
              dalloc(&h->mark, cap) || dalloc(&h->cnt, cap + 1) || dalloc(&h->off, cap + 1) ||
              dalloc(&h->dirty, cap) || dalloc(&h->queue, cap) || dalloc(&h->qflag, cap) || dalloc(&h->rev_off, cap + 1) || dalloc(&h->rev_src, cap * p->R) ||
@@ -881,6 +884,7 @@ grand_status grand_import_graph(grand_index *h, const void *vecs, const uint32_t
   HCHK(h, hipMemcpyAsync(h->pool.adj, adj, cap * h->p.R * 4, hipMemcpyDefault, h->stream));
   HCHK(h, hipMemcpyAsync(h->pool.deg, deg, cap * 4, hipMemcpyDefault, h->stream));
   HCHK(h, hipMemcpyAsync(h->pool.active, active, cap, hipMemcpyDefault, h->stream));
+  HCHK(h, launch_adj_dists(h->pool, h->stream));
   if ((s = clear_errors(h)) != GRAND_OK) return s;
   HCHK(h, hipMemsetAsync(&h->ds->n_count, 0, sizeof(unsigned long long), h->stream));
   hipLaunchKernelGGL(k_import_check, dim3(4096), dim3(256), 0, h->stream, h->pool, h->ds);

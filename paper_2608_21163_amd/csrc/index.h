@@ -71,6 +71,7 @@ struct PoolView {
   uint32_t *adj;
   uint32_t *deg;
   uint8_t *active;
+  float *adjd;     // Dist(u, N_out(u)[s]) beside every list entry, when stored (else null)
   size_t stride;   // bytes per pool row (multiple of 16)
   int nch;         // 16-byte chunks per row
   uint32_t R;
@@ -199,6 +200,12 @@ hipError_t launch_validate_ids(const uint32_t *ids, uint32_t n, uint32_t cap, co
                                uint32_t *mark, uint32_t epoch, int want_active, DevScalars *ds, hipStream_t s);
 hipError_t launch_check_finite(const uint8_t *rows, uint32_t n, size_t stride, uint32_t dim, DevScalars *ds,
                                hipStream_t s);
+// Stored list distances apply to Vamana uint8 pools whose list writers are
+// the forward prune and rebuild kernels that maintain them (R <= 64, R a
+// multiple of 4, rows of 64 or 128 bytes, P <= 64, R + P <= 128).
+bool adj_dists_apply(int kind, uint32_t R, int nch, uint32_t P);
+// Dist(u, v) for every entry of every list (after a bulk import).
+hipError_t launch_adj_dists(PoolView p, hipStream_t s);
 hipError_t launch_stage(PoolView p, const uint8_t *rows, const uint32_t *ids, uint32_t n, uint32_t *bidx,
                         hipStream_t s);
 hipError_t launch_mark_batch(const uint32_t *ids, uint32_t n, uint8_t *in_batch, uint32_t *bidx, uint8_t v,

@@ -733,6 +733,7 @@ __global__ __launch_bounds__(64) void k_fwd_prune_mr(FwdPruneArgs a) {
   if (ln < (int)R) {
     const bool in = ln < nsel;
     P.adj[(size_t)p * R + ln] = in ? sid : kInvalid;
+    if (P.adjd) P.adjd[(size_t)p * R + ln] = in ? sdist : 0.0f;
     a.rec_t[(size_t)i * R + ln] = in ? sid : kInvalid;
     a.rec_s[(size_t)i * R + ln] = p;
     a.rec_d[(size_t)i * R + ln] = in ? sdist : 0.0f;
@@ -927,20 +928,27 @@ __global__ __launch_bounds__(64) void k_rebuild(RebuildArgs a) {
 
 // C of dirty node u (R <= 64, P <= 64): the kept entries of N_out(u) (minus
 // u and the delete batch) in slot order, then the sources of the P smallest
-// distinct records that are not already kept; written to cl (LDS).  Returns
-// |C|; nrec is the number of records addressed to u.
-__device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL, uint32_t *cl, uint32_t &nrec) {
+// distinct records that are not already kept; written to cl (LDS), and
+// with cdl (LDS, given when the pool stores list distances) D_u of each:
+// the stored distance of a kept entry, the record's distance of a new one.
+// Returns |C|; nrec is the number of records addressed to u.
+__device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL, uint32_t *cl, uint32_t &nrec,
+                                  float *cdl = nullptr) {
   const int ln = lane();
   const PoolView &P = a.pool;
   const uint32_t R = P.R;
   const uint32_t g0 = a.goff[u], g1 = a.goff[u + 1];
   const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
+  const float rdv = cdl && ln < (int)R ? P.adjd[(size_t)u * R + ln] : 0.0f;
   nrec = g1 - g0;
   const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
   const uint64_t kmask = ballot(keep);
   const int kr = popc(kmask);
   reinterpret_cast<uint32_t *>(rowL)[ln] = keep ? rv : kInvalid;
-  if (keep) cl[mbcnt(kmask)] = rv;
+  if (keep) {
+    cl[mbcnt(kmask)] = rv;
+    if (cdl) cdl[mbcnt(kmask)] = rdv;
+  }
   __syncthreads();
   // scratch_u: the P smallest distinct (distance, source) records
   float sd[1] = {finf()};
@@ -965,7 +973,10 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   }
   const uint64_t nmask = ballot(isnew);
   const int m = kr + popc(nmask);
-  if (isnew) cl[kr + mbcnt(nmask)] = si[0];
+  if (isnew) {
+    cl[kr + mbcnt(nmask)] = si[0];
+    if (cdl) cdl[kr + mbcnt(nmask)] = sd[0];
+  }
   __syncthreads();
   return m;
 }
@@ -986,6 +997,7 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
   constexpr int NC = 2;
   __shared__ uint4 rowL[16];
   __shared__ uint32_t cl[64 * NC];
+  __shared__ float cdL[64 * NC];  // D_u of the candidates, from the stored list distances
   __shared__ uint32_t spos[64 * NC];
   __shared__ float dpos[64 * NC];
   __shared__ int thrL[64 * NC];
@@ -1003,16 +1015,22 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     const uint32_t u = a.list[it];
     nodes++;
     uint32_t nrec;
-    const int m = collect_candidates(a, u, rowL, cl, nrec);
+    const int m = collect_candidates(a, u, rowL, cl, nrec, P.adjd ? cdL : nullptr);
     recs += nrec;
     if (m <= (int)R) {
       if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < m ? cl[ln] : kInvalid;
+      if (P.adjd && ln < (int)R) P.adjd[(size_t)u * R + ln] = ln < m ? cdL[ln] : 0.0f;
       if (ln == 0) P.deg[u] = (uint32_t)m;
       __syncthreads();
       continue;
     }
-    // D_u of every candidate (list order), into dpos
-    {
+    // D_u of every candidate (list order), into dpos: stored, or by int8
+    // MFMA of u's row against the candidates
+    if (P.adjd) {
+#pragma unroll
+      for (int r = 0; r < NC; r++)
+        if (r * 64 + ln < m) dpos[r * 64 + ln] = cdL[r * 64 + ln];
+    } else {
       v4i A[NK];
       int np = 0;
       const uint8_t *urow = P.vecs + (size_t)u * P.stride + goff;
@@ -1053,7 +1071,7 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
         }
       }
     }
-    evals += (unsigned long long)m;
+    if (!P.adjd) evals += (unsigned long long)m;
     __syncthreads();
     uint64_t key[NC];
 #pragma unroll
@@ -1088,9 +1106,10 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
       __syncthreads();
     }
     if (ln < (int)R) P.adj[(size_t)u * R + ln] = ln < nsel ? oid[ln] : kInvalid;
+    if (P.adjd && ln < (int)R) P.adjd[(size_t)u * R + ln] = ln < nsel ? od[ln] : 0.0f;
     if (ln == 0) P.deg[u] = (uint32_t)nsel;
     prunes++;
-    cand += (unsigned long long)m + 1;
+    cand += (unsigned long long)m + (P.adjd ? 0u : 1u);
     __syncthreads();
   }
   if (ln == 0) {
@@ -1116,6 +1135,7 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
   __shared__ uint4 rowL[64];
   __shared__ uint32_t srcL[64];
   __shared__ uint32_t outL[4 * 64];
+  __shared__ float outD[4 * 64];  // stored list distances, when the pool keeps them
   const int ln = lane(), s = ln >> 4, q = ln & 15;
   const PoolView &P = a.pool;
   const uint32_t R = P.R, R4 = R >> 2;
@@ -1128,15 +1148,24 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
     const uint32_t u = has ? a.list[idx] : 0u;
     uint32_t g0 = 0, g1 = 0;
     uint4 rw = make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+    float4 rd = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     if (has) {
       g0 = a.goff[u];
       g1 = a.goff[u + 1];
-      if ((uint32_t)q < R4) rw = *reinterpret_cast<const uint4 *>(P.adj + (size_t)u * R + 4 * q);
+      if ((uint32_t)q < R4) {
+        rw = *reinterpret_cast<const uint4 *>(P.adj + (size_t)u * R + 4 * q);
+        if (P.adjd) rd = *reinterpret_cast<const float4 *>(P.adjd + (size_t)u * R + 4 * q);
+      }
     }
     const uint32_t nrec = g1 - g0;
     const bool light = has && nrec <= lim;
     uint32_t src = kInvalid;
-    if (light && (uint32_t)q < nrec) src = a.gsrc[g0 + q];
+    float srd = 0.0f;
+    if (light && (uint32_t)q < nrec) {
+      src = a.gsrc[g0 + q];
+      srd = a.gd[g0 + q];
+    }
+    const float dk[4] = {rd.x, rd.y, rd.z, rd.w};
     const uint32_t id[4] = {rw.x, rw.y, rw.z, rw.w};
     bool keep[4];
 #pragma unroll
@@ -1169,8 +1198,16 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
       int pos = x - kc;
 #pragma unroll
       for (int k = 0; k < 4; k++)
-        if (keep[k]) outL[s * 64 + pos++] = id[k];
-      if (nw) outL[s * 64 + kr + popc((uint64_t)(gm & ((1u << q) - 1u)))] = src;
+        if (keep[k]) {
+          outL[s * 64 + pos] = id[k];
+          outD[s * 64 + pos] = dk[k];
+          pos++;
+        }
+      if (nw) {
+        const int e = kr + popc((uint64_t)(gm & ((1u << q) - 1u)));
+        outL[s * 64 + e] = src;
+        outD[s * 64 + e] = srd;
+      }
     }
     __syncthreads();
     if (install && (uint32_t)q < R4) {
@@ -1181,6 +1218,14 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
       o.z = e + 2 < m ? outL[s * 64 + e + 2] : kInvalid;
       o.w = e + 3 < m ? outL[s * 64 + e + 3] : kInvalid;
       *reinterpret_cast<uint4 *>(P.adj + (size_t)u * R + e) = o;
+      if (P.adjd) {
+        float4 d;
+        d.x = e + 0 < m ? outD[s * 64 + e + 0] : 0.0f;
+        d.y = e + 1 < m ? outD[s * 64 + e + 1] : 0.0f;
+        d.z = e + 2 < m ? outD[s * 64 + e + 2] : 0.0f;
+        d.w = e + 3 < m ? outD[s * 64 + e + 3] : 0.0f;
+        *reinterpret_cast<float4 *>(P.adjd + (size_t)u * R + e) = d;
+      }
     }
     if (install && q == 0) P.deg[u] = (uint32_t)m;
     // nodes left for the general kernel are flagged by list position and
@@ -1592,6 +1637,44 @@ static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st
   } else {
     hipLaunchKernelGGL((k_rebuild<KIND, LPV, CPL, NP, NC, kGlobal>), dim3(grid), dim3(64), 0, st, a);
   }
+}
+
+bool adj_dists_apply(int kind, uint32_t R, int nch, uint32_t P) {
+  return kind == kU8L2 && R <= 64 && R % 4 == 0 && (nch == 8 || nch == 4) && P <= 64 && R + P <= 128;
+}
+
+// One wave per row, lane s for list entry s: the exact uint8 squared
+// distance of u and its s-th neighbour (0 for an empty slot).
+__global__ void k_adj_dists(PoolView P) {
+  const int ln = threadIdx.x & 63;
+  const uint32_t w0 = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, nw = (gridDim.x * blockDim.x) >> 6;
+  for (uint32_t u = w0; u < P.cap; u += nw) {
+    if (ln >= (int)P.R) continue;
+    const uint32_t v = P.adj[(size_t)u * P.R + ln];
+    float d = 0.0f;
+    if (kvalid(v) && v < P.cap) {
+      const uint4 *x = reinterpret_cast<const uint4 *>(P.vecs + (size_t)u * P.stride);
+      const uint4 *y = reinterpret_cast<const uint4 *>(P.vecs + (size_t)v * P.stride);
+      uint32_t acc = 0;
+      for (int c = 0; c < P.nch; c++) {
+        const uint4 a = x[c], b = y[c];
+        acc = udot4(a.x, a.x, acc);
+        acc = udot4(a.y, a.y, acc);
+        acc = udot4(a.z, a.z, acc);
+        acc = udot4(a.w, a.w, acc);
+        acc = u8l2_4(a, b, acc);  // + |b|^2 - 2 a.b
+      }
+      d = canon0((float)acc);
+    }
+    P.adjd[(size_t)u * P.R + ln] = d;
+  }
+}
+hipError_t launch_adj_dists(PoolView p, hipStream_t s) {
+  if (!p.adjd || p.cap == 0) return hipSuccess;
+  size_t g = ((size_t)p.cap * 64 + 255) / 256;
+  if (g > 16384) g = 16384;
+  hipLaunchKernelGGL(k_adj_dists, dim3((uint32_t)g), dim3(256), 0, s, p);
+  return hipGetLastError();
 }
 
 // Dirty nodes are rebuilt by the fast kernel when the row layout allows it
