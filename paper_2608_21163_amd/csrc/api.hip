@@ -42,6 +42,10 @@ struct grand_index {
   uint32_t *b_ids = nullptr, *v_ids = nullptr, *v_n = nullptr, *c_ids = nullptr, *rcount = nullptr,
            *rofs = nullptr, *rchunk = nullptr, *coff = nullptr, *cmap = nullptr;
   hipEvent_t ev_total = nullptr;  // record count of a delete batch copied to the host
+  // second stream: a delete batch builds the reverse graph there while its
+  // searches run on the main stream (both only read the graph)
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   float *v_d = nullptr, *c_d = nullptr;
   uint8_t *b_vecs = nullptr;
   uint32_t c_stride = 0;
@@ -116,11 +120,12 @@ static bool timed_phase(int ph) {
 struct Phase {
   grand_index *h;
   int ph;
-  Phase(grand_index *h_, int ph_) : h(h_), ph(ph_) {
+  hipStream_t st;  // stream the phase's work goes to
+  Phase(grand_index *h_, int ph_, hipStream_t st_ = nullptr) : h(h_), ph(ph_), st(st_ ? st_ : h_->stream) {
     if (!h->timing || !timed_phase(ph)) return;
     hipEvent_t e = get_event(h);
     if (!e) return;
-    (void)hipEventRecord(e, h->stream);
+    (void)hipEventRecord(e, st);
     h->pending.emplace_back(ph, e, nullptr);
   }
   ~Phase() {
@@ -129,7 +134,7 @@ struct Phase {
     if (std::get<0>(last) != ph || std::get<2>(last) != nullptr) return;
     hipEvent_t e = get_event(h);
     if (!e) return;
-    (void)hipEventRecord(e, h->stream);
+    (void)hipEventRecord(e, st);
     std::get<2>(last) = e;
   }
 };
@@ -294,11 +299,11 @@ grand_status run_medoid(grand_index *h, const uint8_t *in_batch, int force) {
 // The reverse graph of the current graph: rows of every id (full) or of the
 // batch positions of the delete batch (by_batch).  The source array is part
 // of the resource pool (capacity x R entries bound every reverse graph).
-grand_status run_reverse(grand_index *h, int by_batch, uint32_t n) {
-  Phase ph(h, GRAND_PH_REVERSE);
+grand_status run_reverse(grand_index *h, int by_batch, uint32_t n, hipStream_t st = nullptr) {
+  Phase ph(h, GRAND_PH_REVERSE, st);
   const uint32_t nrows = by_batch ? n : h->p.capacity;
   HCHK(h, launch_reverse(h->pool, by_batch, h->in_batch, h->bidx, nrows, h->cnt, h->rev_off, h->scan_tmp, h->rev_src,
-                         h->rev, h->ds, h->stream));
+                         h->rev, h->ds, st ? st : h->stream));
   return GRAND_OK;
 }
 
@@ -420,6 +425,14 @@ grand_status cagra_insert(grand_index *h, uint32_t n, uint64_t n0) {
 grand_status vamana_delete(grand_index *h, uint32_t n) {
   const uint32_t kr = h->p.k_repair;
   const int by_batch = h->p.rev_mode == GRAND_REV_BATCH;
+  // the reverse graph (side stream) and the searches from the deleted
+  // points (main stream) both only read the graph: they run together, and
+  // the repair waits for both
+  HCHK(h, hipEventRecord(h->ev_fork, h->stream));
+  HCHK(h, hipStreamWaitEvent(h->side, h->ev_fork, 0));
+  grand_status s = run_reverse(h, by_batch, n, h->side);
+  if (s != GRAND_OK) return s;
+  HCHK(h, hipEventRecord(h->ev_join, h->side));
   {
     Phase ph(h, GRAND_PH_SEARCH_DELETE);
     SearchArgs a{};
@@ -437,8 +450,7 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
     a.ds = h->ds;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
-  grand_status s = run_reverse(h, by_batch, n);
-  if (s != GRAND_OK) return s;
+  HCHK(h, hipStreamWaitEvent(h->stream, h->ev_join, 0));
   RepairArgs r{};
   r.pool = h->pool;
   r.ids = h->b_ids;
@@ -546,6 +558,11 @@ void release(grand_index *h) {
   h->hs = nullptr;
   dfree(h->rchunk); dfree(h->coff); dfree(h->cmap);
   if (h->ev_total) (void)hipEventDestroy(h->ev_total);
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+  if (h->side) (void)hipStreamDestroy(h->side);
+  h->ev_fork = h->ev_join = nullptr;
+  h->side = nullptr;
   h->ev_total = nullptr;
   dfree(h->b_ids); dfree(h->v_ids); dfree(h->v_n); dfree(h->c_ids); dfree(h->rcount); dfree(h->rofs);
   dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs);
@@ -646,7 +663,10 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
              dalloc(&h->ds, 1) ||
              hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
              hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess ||
-             hipEventCreateWithFlags(&h->ev_total, hipEventDisableTiming) != hipSuccess;
+             hipEventCreateWithFlags(&h->ev_total, hipEventDisableTiming) != hipSuccess ||
+             hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming) != hipSuccess ||
+             hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming) != hipSuccess ||
+             hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess;
   if (bad) {
     (void)hipGetLastError();
     release(h);
