@@ -426,13 +426,11 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   const uint32_t kr = h->p.k_repair;
   const int by_batch = h->p.rev_mode == GRAND_REV_BATCH;
   // the reverse graph (side stream) and the searches from the deleted
-  // points (main stream) both only read the graph: they run together, and
-  // the repair waits for both
+  // points (main stream) both only read the graph: they run together (the
+  // searches are issued first), and the repair waits for both
   HCHK(h, hipEventRecord(h->ev_fork, h->stream));
   HCHK(h, hipStreamWaitEvent(h->side, h->ev_fork, 0));
-  grand_status s = run_reverse(h, by_batch, n, h->side);
-  if (s != GRAND_OK) return s;
-  HCHK(h, hipEventRecord(h->ev_join, h->side));
+  grand_status s;
   {
     Phase ph(h, GRAND_PH_SEARCH_DELETE);
     SearchArgs a{};
@@ -450,6 +448,9 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
     a.ds = h->ds;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
+  s = run_reverse(h, by_batch, n, h->side);
+  if (s != GRAND_OK) return s;
+  HCHK(h, hipEventRecord(h->ev_join, h->side));
   HCHK(h, hipStreamWaitEvent(h->stream, h->ev_join, 0));
   RepairArgs r{};
   r.pool = h->pool;
