@@ -49,3 +49,18 @@
       return hipErrorInvalidValue;                                                          \
     }                                                                                       \
   } while (0)
+
+namespace gr {
+// Workgroups of 64 lanes of `kern` (no dynamic LDS) that are resident on
+// the current device at once, or 0 if the runtime cannot say.  A persistent
+// loop over a queue split over exactly this many workgroups leaves no
+// workgroup to start after the first ones finish.
+static inline uint32_t resident_blocks(const void *kern) {
+  int dev = 0, ncu = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, 64, 0) != hipSuccess) return 0;
+  return per > 0 && ncu > 0 ? (uint32_t)per * (uint32_t)ncu : 0u;
+}
+static inline uint32_t clamp_resident(uint32_t grid, uint32_t res) { return res && res < grid ? res : grid; }
+}  // namespace gr

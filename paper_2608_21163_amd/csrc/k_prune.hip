@@ -684,7 +684,7 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
 // 64): V_i arrives with D_{p_i} from the search, so the keys are sorted at
 // once and the greedy selection (greedy_u8) needs no gather beforehand.
 template <int NK, int NR>
-__global__ __launch_bounds__(64) void k_fwd_prune_mr(FwdPruneArgs a) {
+__global__ __launch_bounds__(64, 6) void k_fwd_prune_mr(FwdPruneArgs a) {
   __shared__ uint32_t spos[64 * NR];
   __shared__ float dpos[64 * NR];
   const int ln = lane();
@@ -1590,18 +1590,6 @@ hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPrune
   return hipErrorInvalidValue;
 }
 
-// Workgroups of 64 lanes of `kern` (no dynamic LDS) that are resident on
-// the current device at once, or 0 if the runtime cannot say.  A persistent
-// loop over a queue split over exactly this many workgroups leaves no
-// workgroup to start after the first ones finish.
-static uint32_t resident_blocks(const void *kern) {
-  int dev = 0, ncu = 0, per = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, 64, 0) != hipSuccess) return 0;
-  return per > 0 && ncu > 0 ? (uint32_t)per * (uint32_t)ncu : 0u;
-}
-static uint32_t clamp_resident(uint32_t grid, uint32_t res) { return res && res < grid ? res : grid; }
 
 template <int KIND, int LPV, int CPL, int NP, int NC>
 static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st) {

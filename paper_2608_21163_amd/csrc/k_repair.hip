@@ -496,12 +496,17 @@ bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c) {
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
   if (kind == kU8L2 && repair_chunked(kind, a.pool, a.kr, a.c)) {
+    // persistent waves over the chunk map: exactly the resident workgroups
+    static const uint32_t r22 = resident_blocks((const void *)k_repair_mfma<2, 2>);
+    static const uint32_t r24 = resident_blocks((const void *)k_repair_mfma<2, 4>);
+    static const uint32_t r12 = resident_blocks((const void *)k_repair_mfma<1, 2>);
+    static const uint32_t r14 = resident_blocks((const void *)k_repair_mfma<1, 4>);
     if (a.pool.nch == 8) {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(grid), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(grid), dim3(64), 0, st, a);
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(clamp_resident(grid, r22)), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(clamp_resident(grid, r24)), dim3(64), 0, st, a);
     } else {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(grid), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(grid), dim3(64), 0, st, a);
+      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(clamp_resident(grid, r12)), dim3(64), 0, st, a);
+      else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(clamp_resident(grid, r14)), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }
