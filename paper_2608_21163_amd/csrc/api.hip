@@ -780,9 +780,17 @@ grand_status grand_delete_batch(grand_index *h, const uint32_t *ids, uint32_t n)
     HCHK(h, launch_clear_rows(h->pool, h->b_ids, n, h->stream));
   }
   h->n_active -= n;
-  if ((s = run_medoid(h, h->in_batch, 0)) != GRAND_OK) return s;
+  // whether the medoid was deleted reaches the host with the call's final
+  // copy of the device scalars; only then are the medoid kernels launched
+  HCHK(h, launch_medoid_need(h->ds, h->in_batch, 0, h->stream));
   HCHK(h, launch_mark_batch(h->b_ids, n, h->in_batch, nullptr, 0, h->stream));
   h->st.deleted += n;
+  if ((s = finish(h)) != GRAND_OK) return s;
+  if (!h->hs->need_medoid) return GRAND_OK;
+  {
+    Phase ph(h, GRAND_PH_MEDOID);
+    HCHK(h, launch_medoid(h->pool, h->kind, h->p.dim, h->n_active, h->med_tmp, h->ds, h->stream));
+  }
   return finish(h);
 }
 

@@ -210,9 +210,36 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_apply(const uint32_t *in,
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = tsum[nt];
 }
 
+// Inputs of at most kSmallScan values: one workgroup, one launch.
+constexpr int kSmallScanThreads = 1024, kSmallScanPer = 16;
+constexpr size_t kSmallScan = (size_t)kSmallScanThreads * kSmallScanPer;
+__global__ __launch_bounds__(kSmallScanThreads) void k_scan_small(const uint32_t *in, size_t n, uint32_t *out) {
+  __shared__ uint32_t wsum[kSmallScanThreads / 64];
+  const size_t base = (size_t)threadIdx.x * kSmallScanPer;
+  uint32_t v[kSmallScanPer];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int k = 0; k < kSmallScanPer; k++) {
+    v[k] = base + k < n ? in[base + k] : 0u;
+    sum += v[k];
+  }
+  uint32_t total;
+  uint32_t run = block_excl_scan(sum, wsum, total);
+#pragma unroll
+  for (int k = 0; k < kSmallScanPer; k++) {
+    if (base + k < n) out[base + k] = run;
+    run += v[k];
+  }
+  if (threadIdx.x == 0) out[n] = total;
+}
+
 hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tmp, hipStream_t s) {
   const uint32_t nt = (uint32_t)((n + kScanTile - 1) / kScanTile);
   if (nt == 0) return launch_fill_u32(out, 0u, 1, s);
+  if (n <= kSmallScan) {
+    hipLaunchKernelGGL(k_scan_small, dim3(1), dim3(kSmallScanThreads), 0, s, in, n, out);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_scan_tiles, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp);
   hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(1024), 0, s, tmp, nt);
   hipLaunchKernelGGL(k_scan_apply, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp, nt, out);
