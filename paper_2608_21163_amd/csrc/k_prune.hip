@@ -1259,11 +1259,11 @@ __global__ __launch_bounds__(64) void k_rebuild_fast(RebuildArgs a) {
 // same address.
 constexpr int kVecSlice = 64;
 
-// st[k][0..kVecSlice) <- floats [d0, d0 + kVecSlice) of pool row ids[k]
-// (k < ns; zeros past the row or for an invalid id).  Lane (k, part) copies
-// 16 floats.
+// st[k][0..kVecSlice) <- floats [d0, d0 + kVecSlice) of pool row ids[k],
+// widened to fp64 once here rather than at every use (k < ns; zeros past
+// the row or for an invalid id).  Lane (k, part) copies 16 floats.
 __device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids, int ns, int d0, int nfl,
-                                          float (*st)[kVecSlice]) {
+                                          double (*st)[kVecSlice]) {
   const int ln = lane(), k = ln >> 2, part = ln & 3;
   if (k >= ns) return;
   const uint32_t id = ids[k];
@@ -1272,7 +1272,9 @@ __device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids
   for (int h = 0; h < 4; h++) {
     const int f = d0 + 16 * part + 4 * h;
     const uint4 v = (kvalid(id) && f < nfl) ? *reinterpret_cast<const uint4 *>(row + f) : make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4 *>(&st[k][16 * part + 4 * h]) = v;
+    double2 *dst = reinterpret_cast<double2 *>(&st[k][16 * part + 4 * h]);
+    dst[0] = make_double2((double)__uint_as_float(v.x), (double)__uint_as_float(v.y));
+    dst[1] = make_double2((double)__uint_as_float(v.z), (double)__uint_as_float(v.w));
   }
 }
 
@@ -1280,7 +1282,7 @@ __device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids
 // row own[r] and staged row k, for every register row r with work (act[r],
 // uniform).
 template <int KIND, int NCL, int NS>
-__device__ __forceinline__ void vec_accumulate(const float (*st)[kVecSlice], const float *const (&own)[NCL],
+__device__ __forceinline__ void vec_accumulate(const double (*st)[kVecSlice], const float *const (&own)[NCL],
                                                const bool (&act)[NCL], int d0, int nfl,
                                                double (&acc)[NCL][NS]) {
   for (int pc = 0; pc < kVecSlice && d0 + pc < nfl; pc += 16) {
@@ -1302,9 +1304,9 @@ __device__ __forceinline__ void vec_accumulate(const float (*st)[kVecSlice], con
 #pragma unroll
         for (int t = 0; t < 16; t++) {
           if (KIND == kF32IP) {
-            acc[r][k] = __builtin_fma((double)xv[t], (double)st[k][pc + t], acc[r][k]);
+            acc[r][k] = __builtin_fma((double)xv[t], st[k][pc + t], acc[r][k]);
           } else {
-            const double df = (double)st[k][pc + t] - (double)xv[t];
+            const double df = st[k][pc + t] - (double)xv[t];
             acc[r][k] = __builtin_fma(df, df, acc[r][k]);
           }
         }
@@ -1321,7 +1323,7 @@ __device__ __forceinline__ void vec_accumulate(const float (*st)[kVecSlice], con
 // The selections go to oid/od (LDS) in order; returns their number.
 template <int KIND, int NCL, int NPB>
 __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
-                         const float *dpos, float (*st)[kVecSlice], uint32_t *oid, float *od, uint32_t &evals) {
+                         const float *dpos, double (*st)[kVecSlice], uint32_t *oid, float *od, uint32_t &evals) {
   static_assert(NPB <= 16 && 64 % NPB == 0, "pivot blocks inside one register row");
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const int nfl = P.nch * 4;
@@ -1416,7 +1418,7 @@ __global__ __launch_bounds__(64) void k_rebuild_vec(RebuildArgs a) {
   __shared__ uint32_t cl[64 * NC];
   __shared__ uint32_t spos[64 * NC];
   __shared__ float dpos[64 * NC];
-  __shared__ float st[16][kVecSlice];
+  __shared__ double st[16][kVecSlice];
   __shared__ uint32_t oid[64];
   __shared__ float od[64];
   __shared__ uint32_t uid[1];
@@ -1499,7 +1501,7 @@ __global__ __launch_bounds__(64) void k_fwd_prune_vec(FwdPruneArgs a) {
   constexpr int NPB = NR >= 4 ? 8 : 16;
   __shared__ uint32_t spos[64 * NR];
   __shared__ float dpos[64 * NR];
-  __shared__ float st[16][kVecSlice];
+  __shared__ double st[16][kVecSlice];
   __shared__ uint32_t oid[64];
   __shared__ float od[64];
   const int ln = lane();
