@@ -1316,26 +1316,25 @@ __device__ __forceinline__ void vec_accumulate(const double (*st)[kVecSlice], co
 
 // GrANDRobustPrune over m candidates sorted by (D_p, id) (spos/dpos in LDS,
 // positions e = r*64 + lane, at most 64*NCL).  Positions are taken in blocks
-// of NPB pivots: the block's rows are staged and every lane computes the
-// distances from them to its later positions; the block's own selections
-// come from the parallel fixpoint, and later positions that a selected pivot
-// kills (coef * Dist <= D, in fp64 on the rounded distance) are dropped.
-// The selections go to oid/od (LDS) in order; returns their number.
+// of NPB pivots: the block's rows are staged and the distances from them to
+// every still-live position from the block on are computed, those positions
+// packed onto the lanes (a block rarely leaves more than 64 of them, so the
+// fp64 work follows the live positions, not the register rows); the block's
+// own selections come from the parallel fixpoint, and later positions that a
+// selected pivot kills (coef * Dist <= D, in fp64 on the rounded distance)
+// are dropped.  The selections go to oid/od (LDS) in order; returns their
+// number.
 template <int KIND, int NCL, int NPB>
 __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
                          const float *dpos, double (*st)[kVecSlice], uint32_t *oid, float *od, uint32_t &evals) {
   static_assert(NPB <= 16 && 64 % NPB == 0, "pivot blocks inside one register row");
+  __shared__ uint32_t lpos[64 * NCL];  // live positions of the block, packed
+  __shared__ uint32_t kmL[64 * NCL];   // kill masks by position
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const int nfl = P.nch * 4;
   uint64_t vm[NCL];
 #pragma unroll
   for (int r = 0; r < NCL; r++) vm[r] = ballot(r * 64 + ln < m);
-  const float *own[NCL];
-#pragma unroll
-  for (int r = 0; r < NCL; r++) {
-    const int e = r * 64 + ln;
-    own[r] = reinterpret_cast<const float *>(P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride);
-  }
   int nsel = 0;
   const int nb = (m + NPB - 1) / NPB;
   for (int b = 0; b < nb; b++) {
@@ -1346,9 +1345,27 @@ __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       if (r == (p0 >> 6)) vr = vm[r];
     const uint32_t vb = (uint32_t)(vr >> (p0 & 63)) & ((1u << NPB) - 1u);
     if (!vb) continue;
-    bool act[NCL];
+    // live positions >= p0, in order, packed onto the lanes
+    int nl = 0;
 #pragma unroll
-    for (int r = 0; r < NCL; r++) act[r] = r * 64 + 63 >= p0 && r * 64 < m;
+    for (int r = 0; r < NCL; r++) {
+      const int e = r * 64 + ln;
+      const bool lv = e >= p0 && ((vm[r] >> ln) & 1ull);
+      const uint64_t bm = ballot(lv);
+      if (lv) lpos[nl + mbcnt(bm)] = (uint32_t)e;
+      nl += popc(bm);
+    }
+    __syncthreads();
+    bool act[NCL];
+    const float *own[NCL];
+    int ep[NCL];
+#pragma unroll
+    for (int r = 0; r < NCL; r++) {
+      act[r] = r * 64 < nl;
+      const int c = r * 64 + ln;
+      ep[r] = act[r] && c < nl ? (int)lpos[c] : -1;
+      own[r] = reinterpret_cast<const float *>(P.vecs + (size_t)(ep[r] >= 0 ? spos[ep[r]] : p) * P.stride);
+    }
     double acc[NCL][NPB];
 #pragma unroll
     for (int r = 0; r < NCL; r++)
@@ -1360,22 +1377,29 @@ __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       __syncthreads();
       vec_accumulate<KIND, NCL, NPB>(st, own, act, d0, nfl, acc);
     }
+    // kill masks of the packed positions, scattered back by position
+#pragma unroll
+    for (int r = 0; r < NCL; r++) {
+      const int e = ep[r];
+      if (e < 0) continue;
+      const double De = (double)dpos[e];
+      uint32_t km = 0;
+#pragma unroll
+      for (int k = 0; k < NPB; k++) {
+        const bool kill = e > p0 + k && coef * (double)finalize<KIND>(acc[r][k]) <= De;
+        km |= kill ? (1u << k) : 0u;
+      }
+      kmL[e] = km;
+    }
+    evals += (uint32_t)(NPB * nl);
+    __syncthreads();
     // km[r]: pivots of the block that kill this lane's position
     uint32_t km[NCL];
 #pragma unroll
     for (int r = 0; r < NCL; r++) {
       const int e = r * 64 + ln;
-      km[r] = 0;
-      if (act[r]) {
-        const double De = e < m ? (double)dpos[e] : 0.0;
-#pragma unroll
-        for (int k = 0; k < NPB; k++) {
-          const bool kill = e > p0 + k && e < m && coef * (double)finalize<KIND>(acc[r][k]) <= De;
-          km[r] |= kill ? (1u << k) : 0u;
-        }
-      }
+      km[r] = e >= p0 && ((vm[r] >> ln) & 1ull) ? kmL[e] : 0u;
     }
-    evals += (uint32_t)(NPB * (m - p0));
     // the block's own positions: lanes (p0 & 63) + col of register row p0 >> 6
     uint32_t kbr = 0;
 #pragma unroll
@@ -1403,6 +1427,7 @@ __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       const int e = r * 64 + ln;
       vm[r] &= ~ballot(e >= p0 + NPB && (km[r] & S) != 0u);
     }
+    __syncthreads();
   }
   __syncthreads();
   return nsel;
