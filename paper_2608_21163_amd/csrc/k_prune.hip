@@ -1589,9 +1589,10 @@ hipError_t launch_fwd_prune(int kind, int vc, uint32_t max_iters, const FwdPrune
       return hipGetLastError();
     });
   }
-  // fp32 rows longer than 128 floats: one lane per candidate (the per-pivot
-  // walk of the general kernel costs more there; measured at d = 96 and 960)
-  if (kind != kU8L2 && a.pool.R <= 64 && a.pool.nch > 32) {
+  // fp32 rows longer than 32 floats: one lane per live candidate (the
+  // per-pivot walk of the general kernel costs more there; measured at
+  // d = 96 and 960)
+  if (kind != kU8L2 && a.pool.R <= 64 && a.pool.nch > 8) {
     GR_DISPATCH_N(max_iters, {
       if (kind == kF32L2) hipLaunchKernelGGL((k_fwd_prune_vec<kF32L2, NR>), dim3(a.n), dim3(64), 0, st, a);
       else hipLaunchKernelGGL((k_fwd_prune_vec<kF32IP, NR>), dim3(a.n), dim3(64), 0, st, a);

@@ -346,7 +346,7 @@ __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
 template <int KIND, int K>
 __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
   constexpr int GC = 16, SL = 64;
-  __shared__ float cs[GC][SL];
+  __shared__ double cs[GC][SL];  // candidate slices, widened to fp64 once when staged
   __shared__ uint32_t cidL[64];
   const int ln = lane();
   const PoolView &P = a.pool;
@@ -403,7 +403,9 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
           for (int h = 0; h < 4; h++) {
             const int f = d0 + 16 * part + 4 * h;
             const uint4 v = (kvalid(cv) && f < nfl) ? *reinterpret_cast<const uint4 *>(crow + f) : make_uint4(0, 0, 0, 0);
-            *reinterpret_cast<uint4 *>(&cs[cand][16 * part + 4 * h]) = v;
+            double2 *dst = reinterpret_cast<double2 *>(&cs[cand][16 * part + 4 * h]);
+            dst[0] = make_double2((double)__uint_as_float(v.x), (double)__uint_as_float(v.y));
+            dst[1] = make_double2((double)__uint_as_float(v.z), (double)__uint_as_float(v.w));
           }
         }
         __syncthreads();
@@ -423,10 +425,10 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
 #pragma unroll
             for (int t = 0; t < 16; t++) {
               if (KIND == kF32L2) {
-                const double df = (double)cs[k][pc + t] - (double)xv[t];
+                const double df = cs[k][pc + t] - (double)xv[t];
                 acc[k] = __builtin_fma(df, df, acc[k]);
               } else {
-                acc[k] = __builtin_fma((double)xv[t], (double)cs[k][pc + t], acc[k]);
+                acc[k] = __builtin_fma((double)xv[t], cs[k][pc + t], acc[k]);
               }
             }
         }
