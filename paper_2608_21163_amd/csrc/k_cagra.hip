@@ -217,6 +217,7 @@ hipError_t launch_cagra_affected(const uint32_t *ids, uint32_t n, const uint8_t 
 
 __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   __shared__ uint32_t lc[64];
+  __shared__ uint4 uL[16];  // u's current row, for the membership test
   const int ln = lane();
   const PoolView &P = a.pool;
   const bool inrow = ln < (int)P.R;
@@ -225,6 +226,7 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
     const uint32_t u = a.list[it];
     uint32_t rv = inrow ? P.adj[(size_t)u * P.R + ln] : kInvalid;
+    reinterpret_cast<uint32_t *>(uL)[ln] = rv;
     // slots holding a deleted out-neighbour, found with one parallel lookup;
     // they are then handled in slot order (replacements only ever put
     // non-deleted ids into the row, so the set does not change)
@@ -255,9 +257,12 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
           r = lc[(start + (uint32_t)ln) % (uint32_t)nl];
           ok = !a.in_batch[r] && r != u;
         }
-        for (uint32_t t = 0; t < P.R; t++) {
-          const uint32_t x = rdlane(rv, (int)t);
-          ok = ok && x != r;
+        // r must not already be in u's row (16-byte LDS reads, all lanes
+        // at the same address)
+#pragma unroll 4
+        for (int t = 0; t < 16; t++) {
+          const uint4 q = uL[t];
+          ok = ok & (q.x != r) & (q.y != r) & (q.z != r) & (q.w != r);
         }
         const uint64_t om = ballot(ok);
         if (om) chosen = rdlane(r, ffs64(om));
@@ -265,6 +270,7 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
       if (ln == (int)s) {
         atomicCAS(&P.adj[(size_t)u * P.R + s], p, chosen);
         rv = chosen;
+        reinterpret_cast<uint32_t *>(uL)[ln] = chosen;
       }
       __syncthreads();
     }
