@@ -48,10 +48,11 @@ hipError_t launch_cagra_fwd(PoolView p, const uint32_t *ids, uint32_t n, const u
   return hipGetLastError();
 }
 
-// One reverse edge q -> p against q's row held by lane s in rv.  Returns
-// the new value of this lane's slot.
+// One reverse edge q -> p against q's row held by lane s in rv; fl4 (LDS,
+// 64 ids, INVALID past R) holds N_out(p).  Returns the new value of this
+// lane's slot.
 __device__ __forceinline__ uint32_t detour_one(const CagraArgs &a, uint32_t q, uint32_t p, uint32_t rv,
-                                               uint32_t *fl) {
+                                               const uint4 *fl4) {
   const int ln = lane();
   const PoolView &P = a.pool;
   const bool inrow = ln < (int)P.R;
@@ -65,12 +66,15 @@ __device__ __forceinline__ uint32_t detour_one(const CagraArgs &a, uint32_t q, u
     }
     return rv;
   }
-  const uint32_t bi = a.bidx[p];
-  fl[ln] = inrow ? a.fwd[(size_t)bi * P.R + ln] : kInvalid;
-  __syncthreads();
+  // this lane's entry is in N_out(p): 16-byte LDS reads, all lanes at the
+  // same address
   bool mem = false;
-  for (uint32_t t = 0; t < P.R; t++) mem = mem || (inrow && rv != kInvalid && fl[t] == rv);
-  __syncthreads();
+#pragma unroll 4
+  for (int t = 0; t < 16; t++) {
+    const uint4 f = fl4[t];
+    mem = mem | (f.x == rv) | (f.y == rv) | (f.z == rv) | (f.w == rv);
+  }
+  mem = mem && inrow && rv != kInvalid;
   const uint64_t mm = ballot(mem);
   if (mm) {
     const int s = fls64(mm);
@@ -83,7 +87,8 @@ __device__ __forceinline__ uint32_t detour_one(const CagraArgs &a, uint32_t q, u
 }
 
 __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
-  __shared__ uint32_t fl[64];
+  constexpr int kFwdStage = 4;  // forward lists of records loaded together
+  __shared__ uint4 fl4[kFwdStage][16];
   const int ln = lane();
   const PoolView &P = a.pool;
   const uint32_t nt = a.ds->n_dirty;
@@ -110,9 +115,34 @@ __global__ __launch_bounds__(64) void k_cagra_detour(CagraArgs a) {
       }
       const int nb = popc(ballot(kvalid(ci[0])));
       if (nb == 0) break;
-      for (int t = 0; t < nb; t++) {
-        const uint32_t p = rdlane(ci[0], t);
-        rv = detour_one(a, q, p, rv, fl);
+      for (int t0 = 0; t0 < nb; t0 += kFwdStage) {
+        // N_out of the next kFwdStage records' sources, loaded together:
+        // lane (h, part) copies 4 ids of record t0 + h
+        {
+          const int h = ln >> 4, part = ln & 15;
+          const int t = t0 + h;
+          const uint32_t p = (uint32_t)__shfl((int)ci[0], t < nb ? t : t0, 64);  // per-lane source lane
+          uint4 v = make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+          if (t < nb && 4 * part < (int)P.R) {
+            const uint32_t *row = a.fwd + (size_t)a.bidx[p] * P.R + 4 * part;
+            if ((P.R & 3u) == 0) {
+              v = *reinterpret_cast<const uint4 *>(row);
+            } else {  // rows not 16-byte aligned: word loads, INVALID past R
+              const int e = 4 * part;
+              v.x = row[0];
+              v.y = e + 1 < (int)P.R ? row[1] : kInvalid;
+              v.z = e + 2 < (int)P.R ? row[2] : kInvalid;
+              v.w = e + 3 < (int)P.R ? row[3] : kInvalid;
+            }
+          }
+          fl4[h][part] = v;
+        }
+        __syncthreads();
+        for (int h = 0; h < kFwdStage && t0 + h < nb; h++) {
+          const uint32_t p = rdlane(ci[0], t0 + h);
+          rv = detour_one(a, q, p, rv, fl4[h]);
+        }
+        __syncthreads();
       }
       lastd = rdlane(cd[0], nb - 1);
       lasti = rdlane(ci[0], nb - 1);
