@@ -190,7 +190,7 @@ __device__ __forceinline__ void kl_merge64(uint64_t (&l)[K], const uint64_t (&o)
 }
 
 template <int NK, int K>
-__global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(K <= 2 ? 5 : 4))) void k_repair_mfma(RepairArgs a) {
   constexpr int NT = 4;  // C_i tiles (k_repair <= 64)
   __shared__ uint32_t cidL[64];
   __shared__ int cnrL[64];
@@ -225,6 +225,20 @@ __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
       rbase = a.rofs[i] + nin * (c + 1);
     }
     const bool xok = x != kInvalid && !a.in_batch[x];
+    // The rows of neighbours 16s .. 16s+15 (the B operand of step s): lane
+    // (g, col) loads bytes 16g + 64kk of neighbour 16s + col.  The loads of
+    // step s + 1 are issued before step s is computed.
+    uint4 Xn[NK];
+    uint32_t xsn;
+    bool xsokn;
+    auto load_step = [&](int s) {
+      xsn = __shfl(x, 16 * s + col, 64);
+      xsokn = __shfl((int)xok, 16 * s + col, 64) != 0;
+      const uint8_t *row = P.vecs + (size_t)(xsokn ? xsn : p) * P.stride + goff;
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) Xn[kk] = ld16(row + (size_t)kk * 64);
+    };
+    load_step(0);
     // C_i tiles (A operand: candidate 16t + col, bytes 16g + 64kk)
     v4i Ct[NT][NK];
 #pragma unroll
@@ -250,16 +264,15 @@ __global__ __launch_bounds__(64) void k_repair_mfma(RepairArgs a) {
     rows += (unsigned long long)popc(ballot(xok));
     for (int s = 0; 16 * s < cnt; s++) {
       // neighbours 16s .. 16s+15 as the B operand
-      const uint32_t xs = __shfl(x, 16 * s + col, 64);
-      const bool xsok = __shfl((int)xok, 16 * s + col, 64) != 0;
-      const uint8_t *row = P.vecs + (size_t)(xsok ? xs : p) * P.stride + goff;
+      const uint32_t xs = xsn;
+      const bool xsok = xsokn;
       v4i X[NK];
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) X[kk] = to_i8x16(Xn[kk]);
+      if (16 * (s + 1) < cnt) load_step(s + 1);
       int nx = 0;
 #pragma unroll
-      for (int kk = 0; kk < NK; kk++) {
-        X[kk] = to_i8x16(ld16(row + (size_t)kk * 64));
-        nx = sq_i8x16(X[kk], nx);
-      }
+      for (int kk = 0; kk < NK; kk++) nx = sq_i8x16(X[kk], nx);
       nx += (int)xshfl((uint32_t)nx, 16);
       nx += (int)xshfl((uint32_t)nx, 32);
       uint64_t l[K];
