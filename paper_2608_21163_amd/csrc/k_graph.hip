@@ -175,18 +175,38 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_tiles(const uint32_t *in,
   if (threadIdx.x == 0) tsum[blockIdx.x] = total;
 }
 
-__global__ __launch_bounds__(1024) void k_scan_tsum(uint32_t *tsum, uint32_t nt) {
-  __shared__ uint32_t wsum[16];
+// In-place exclusive scan of the nt tile sums (tsum[nt] <- their total) by
+// one wave: it fits beside a kernel that holds nearly every wave slot of
+// every CU, where a workgroup of many waves waits for one to drain.  Lane l
+// owns 16 consecutive sums of each block of 1024, all loaded before the
+// wave scan of the lane totals.
+constexpr int kTsumPer = 16;
+__global__ __launch_bounds__(64) void k_scan_tsum(uint32_t *tsum, uint32_t nt) {
+  const int ln = lane();
   uint32_t carry = 0;
-  for (uint32_t b0 = 0; b0 < nt; b0 += 1024) {
-    const uint32_t i = b0 + threadIdx.x;
-    const uint32_t v = i < nt ? tsum[i] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_excl_scan(v, wsum, total);
-    if (i < nt) tsum[i] = carry + ex;
-    carry += total;
+  for (uint32_t b0 = 0; b0 < nt; b0 += 64 * kTsumPer) {
+    const uint32_t base = b0 + (uint32_t)ln * kTsumPer;
+    uint32_t v[kTsumPer], sum = 0;
+#pragma unroll
+    for (int k = 0; k < kTsumPer; k++) {
+      v[k] = base + k < nt ? tsum[base + k] : 0u;
+      sum += v[k];
+    }
+    uint32_t x = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(x, o, 64);
+      if (ln >= o) x += y;
+    }
+    uint32_t run = carry + x - sum;
+#pragma unroll
+    for (int k = 0; k < kTsumPer; k++) {
+      if (base + k < nt) tsum[base + k] = run;
+      run += v[k];
+    }
+    carry += __shfl(x, 63, 64);
   }
-  if (threadIdx.x == 0) tsum[nt] = carry;
+  if (ln == 0) tsum[nt] = carry;
 }
 
 __global__ __launch_bounds__(kScanThreads) void k_scan_apply(const uint32_t *in, size_t n, const uint32_t *tsum,
@@ -241,7 +261,7 @@ hipError_t launch_scan(const uint32_t *in, uint32_t *out, size_t n, uint32_t *tm
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_scan_tiles, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp);
-  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(1024), 0, s, tmp, nt);
+  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(64), 0, s, tmp, nt);
   hipLaunchKernelGGL(k_scan_apply, dim3(nt), dim3(kScanThreads), 0, s, in, n, tmp, nt, out);
   return hipGetLastError();
 }
@@ -379,7 +399,7 @@ hipError_t launch_compact_flags(const uint32_t *flags, const uint32_t *items, co
   const uint32_t nt = (uint32_t)((cap + kScanTile - 1) / kScanTile);
   if (nt == 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_cf_tiles, dim3(nt), dim3(kScanThreads), 0, s, flags, n, tmp);
-  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(1024), 0, s, tmp, nt);
+  hipLaunchKernelGGL(k_scan_tsum, dim3(1), dim3(64), 0, s, tmp, nt);
   hipLaunchKernelGGL(k_cf_apply, dim3(nt), dim3(kScanThreads), 0, s, flags, items, n, tmp, nt, out, out_n);
   return hipGetLastError();
 }
