@@ -39,12 +39,30 @@ __global__ void k_repair_plan(RepairArgs a, uint32_t *counts, uint32_t *chunks) 
   chunks[i] = (nin + 63) / 64 + 1;
 }
 
-// cmap[coff[i] + j] = i for every chunk j of deleted node i (one wave each).
-__global__ void k_repair_map(uint32_t n, const uint32_t *coff, uint32_t *cmap) {
+// cmap[coff[i] + j] = i for every chunk j of deleted node i (one wave each),
+// and the chunk's descriptor, so that a repair wave starts a chunk with one
+// pair of loads instead of a chain of dependent ones: chunk j < nci covers
+// in-neighbours 64j .. 64j + 63 of p_i, the last chunk its out-slots.
+__global__ void k_repair_map(RepairArgs a, uint32_t *cmap, uint4 *cdesc) {
   const uint32_t i = blockIdx.x;
-  if (i >= n) return;
-  const uint32_t c0 = coff[i], c1 = coff[i + 1];
-  for (uint32_t q = c0 + threadIdx.x; q < c1; q += blockDim.x) cmap[q] = i;
+  if (i >= a.n) return;
+  const uint32_t c0 = a.coff[i], c1 = a.coff[i + 1];
+  const uint32_t p = a.ids[i];
+  uint32_t b0, b1;
+  rev_row(a, i, p, b0, b1);
+  const uint32_t nin = b1 - b0, nci = (nin + 63) / 64, r0 = a.rofs[i], c = a.c;
+  for (uint32_t q = c0 + threadIdx.x; q < c1; q += blockDim.x) {
+    cmap[q] = i;
+    const uint32_t j = q - c0;
+    if (j < nci) {
+      const uint32_t e0 = j * 64;
+      cdesc[2 * (size_t)q] = make_uint4(i, p, b0 + e0, min(64u, nin - e0));
+      cdesc[2 * (size_t)q + 1] = make_uint4(r0 + e0 * (c + 1), j, 0u, 0u);
+    } else {
+      cdesc[2 * (size_t)q] = make_uint4(i, p, kInvalid, a.pool.R);
+      cdesc[2 * (size_t)q + 1] = make_uint4(r0 + nin * (c + 1), j, 0u, 0u);
+    }
+  }
 }
 
 hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s) {
@@ -52,9 +70,9 @@ hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *c
   hipLaunchKernelGGL(k_repair_plan, dim3((a.n + 255) / 256), dim3(256), 0, s, a, counts, chunks);
   return hipGetLastError();
 }
-hipError_t launch_repair_map(uint32_t n, const uint32_t *coff, uint32_t *cmap, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_repair_map, dim3(n), dim3(64), 0, s, n, coff, cmap);
+hipError_t launch_repair_map(const RepairArgs &a, uint32_t *cmap, uint4 *cdesc, hipStream_t s) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_repair_map, dim3(a.n), dim3(64), 0, s, a, cmap, cdesc);
   return hipGetLastError();
 }
 
@@ -204,26 +222,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(K <= 2 ? 5 :
   const uint32_t total = a.coff[a.n];
   unsigned long long evals = 0, rows = 0, recs = 0;
   for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
-    const uint32_t i = a.cmap[q];
-    const uint32_t j = q - a.coff[i];
-    const uint32_t p = a.ids[i];
-    uint32_t b0, b1;
-    rev_row(a, i, p, b0, b1);
-    const uint32_t nin = b1 - b0, nci = (nin + 63) / 64;
-    const bool inbound = j < nci;
+    const uint4 d0 = a.cdesc[2 * (size_t)q], d1 = a.cdesc[2 * (size_t)q + 1];
+    const uint32_t i = d0.x, p = d0.y, j = d1.y, rbase = d1.x;
+    const bool inbound = d0.z != kInvalid;
     // this chunk's neighbours, lane e holding neighbour e
-    int cnt;
-    uint32_t x, rbase;
-    if (inbound) {
-      const uint32_t e0 = j * 64;
-      cnt = (int)min(64u, nin - e0);
-      x = ln < cnt ? a.rev_src[b0 + e0 + ln] : kInvalid;
-      rbase = a.rofs[i] + e0 * (c + 1);
-    } else {
-      cnt = (int)R;
-      x = ln < cnt ? P.adj[(size_t)p * R + ln] : kInvalid;
-      rbase = a.rofs[i] + nin * (c + 1);
-    }
+    const int cnt = (int)d0.w;
+    const uint32_t x =
+        ln < cnt ? (inbound ? a.rev_src[d0.z + ln] : P.adj[(size_t)p * R + ln]) : kInvalid;
     const bool xok = x != kInvalid && !a.in_batch[x];
     // The rows of neighbours 16s .. 16s+15 (the B operand of step s): lane
     // (g, col) loads bytes 16g + 64kk of neighbour 16s + col.  The loads of
