@@ -40,7 +40,7 @@ struct grand_index {
   // per-batch buffers
   uint32_t bcap = 0;
   uint32_t *b_ids = nullptr, *v_ids = nullptr, *v_n = nullptr, *c_ids = nullptr, *rcount = nullptr,
-           *rofs = nullptr, *rchunk = nullptr, *coff = nullptr, *cmap = nullptr;
+           *rofs = nullptr, *rchunk = nullptr, *coff = nullptr;
   uint4 *cdesc = nullptr;
   hipEvent_t ev_total = nullptr;  // record count of a delete batch copied to the host
   // second stream: a delete batch builds the reverse graph there while its
@@ -193,7 +193,7 @@ grand_status ensure_batch(grand_index *h, uint32_t n) {
   HCHK(h, hipStreamSynchronize(h->stream));
   uint32_t nc = std::max<uint32_t>(n, h->bcap + h->bcap / 2);
   dfree(h->b_ids); dfree(h->v_ids); dfree(h->v_n); dfree(h->c_ids); dfree(h->rcount); dfree(h->rofs);
-  dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs); dfree(h->rchunk); dfree(h->coff); dfree(h->cmap);
+  dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs); dfree(h->rchunk); dfree(h->coff);
   dfree(h->cdesc);
   h->bcap = 0;
   // work chunks of a delete batch: at most (in-edges of the batch) / 64 + 2 per deleted node
@@ -202,7 +202,7 @@ grand_status ensure_batch(grand_index *h, uint32_t n) {
   if (dalloc(&h->b_ids, nc) || dalloc(&h->v_ids, vs) || dalloc(&h->v_d, vs) || dalloc(&h->v_n, nc) ||
       dalloc(&h->c_ids, (size_t)nc * h->c_stride) || dalloc(&h->c_d, (size_t)nc * h->c_stride) ||
       dalloc(&h->rcount, (size_t)nc + 1) || dalloc(&h->rofs, (size_t)nc + 1) ||
-      dalloc(&h->rchunk, (size_t)nc + 1) || dalloc(&h->coff, (size_t)nc + 1) || dalloc(&h->cmap, nchunk) || dalloc(&h->cdesc, 2 * nchunk) ||
+      dalloc(&h->rchunk, (size_t)nc + 1) || dalloc(&h->coff, (size_t)nc + 1) || dalloc(&h->cdesc, 2 * nchunk) ||
       dalloc(&h->b_vecs, (size_t)nc * h->stride)) {
     (void)hipGetLastError();
     return fail(h, GRAND_E_OOM, "device allocation of batch buffers failed");
@@ -467,7 +467,6 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   r.c = h->p.c;
   r.rofs = h->rofs;
   r.coff = h->coff;
-  r.cmap = h->cmap;
   r.cdesc = h->cdesc;
   r.ds = h->ds;
   // record offsets and work chunks; the record count reaches the host
@@ -477,7 +476,7 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   const bool chunked = repair_chunked(h->kind, h->pool, kr, h->p.c);
   if (chunked) {
     HCHK(h, launch_scan(h->rchunk, h->coff, n, h->scan_tmp, h->stream));
-    HCHK(h, launch_repair_map(r, h->cmap, h->cdesc, h->stream));
+    HCHK(h, launch_repair_map(r, h->cdesc, h->stream));
   }
   HCHK(h, hipMemcpyAsync(&h->hs->n_dirty, h->rofs + n, sizeof(uint32_t), hipMemcpyDeviceToHost, h->stream));
   HCHK(h, hipEventRecord(h->ev_total, h->stream));
@@ -560,7 +559,7 @@ void release(grand_index *h) {
   dfree(h->ds);
   if (h->hs) (void)hipHostFree(h->hs);
   h->hs = nullptr;
-  dfree(h->rchunk); dfree(h->coff); dfree(h->cmap); dfree(h->cdesc);
+  dfree(h->rchunk); dfree(h->coff); dfree(h->cdesc);
   if (h->ev_total) (void)hipEventDestroy(h->ev_total);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);

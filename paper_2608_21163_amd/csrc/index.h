@@ -158,7 +158,6 @@ struct RepairArgs {
   uint32_t c;
   const uint32_t *rofs;       // record offsets per deleted node (n + 1)
   const uint32_t *coff;       // work-chunk offsets per deleted node (n + 1)
-  const uint32_t *cmap;       // deleted node of every work chunk
   const uint4 *cdesc;         // two words per work chunk: {node, id, first in-edge or INVALID, count}, {record base, chunk index}
   size_t rcap;                // record capacity: nothing is written when rofs[n] exceeds it
   uint32_t *rec_t, *rec_s;
@@ -192,7 +191,7 @@ hipError_t launch_rebuild(int kind, int vc, uint32_t R, uint32_t P, const Rebuil
                           hipStream_t s);
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t s);
 hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s);
-hipError_t launch_repair_map(const RepairArgs &a, uint32_t *cmap, uint4 *cdesc, hipStream_t s);
+hipError_t launch_repair_map(const RepairArgs &a, uint4 *cdesc, hipStream_t s);
 bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c);
 
 hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s);

@@ -39,11 +39,11 @@ __global__ void k_repair_plan(RepairArgs a, uint32_t *counts, uint32_t *chunks) 
   chunks[i] = (nin + 63) / 64 + 1;
 }
 
-// cmap[coff[i] + j] = i for every chunk j of deleted node i (one wave each),
-// and the chunk's descriptor, so that a repair wave starts a chunk with one
-// pair of loads instead of a chain of dependent ones: chunk j < nci covers
-// in-neighbours 64j .. 64j + 63 of p_i, the last chunk its out-slots.
-__global__ void k_repair_map(RepairArgs a, uint32_t *cmap, uint4 *cdesc) {
+// The descriptor of every work chunk j of deleted node i (one wave per
+// node), so that a repair wave starts a chunk with one pair of loads instead
+// of a chain of dependent ones: chunk j < nci covers in-neighbours
+// 64j .. 64j + 63 of p_i, the last chunk its out-slots.
+__global__ void k_repair_map(RepairArgs a, uint4 *cdesc) {
   const uint32_t i = blockIdx.x;
   if (i >= a.n) return;
   const uint32_t c0 = a.coff[i], c1 = a.coff[i + 1];
@@ -52,7 +52,6 @@ __global__ void k_repair_map(RepairArgs a, uint32_t *cmap, uint4 *cdesc) {
   rev_row(a, i, p, b0, b1);
   const uint32_t nin = b1 - b0, nci = (nin + 63) / 64, r0 = a.rofs[i], c = a.c;
   for (uint32_t q = c0 + threadIdx.x; q < c1; q += blockDim.x) {
-    cmap[q] = i;
     const uint32_t j = q - c0;
     if (j < nci) {
       const uint32_t e0 = j * 64;
@@ -70,9 +69,9 @@ hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *c
   hipLaunchKernelGGL(k_repair_plan, dim3((a.n + 255) / 256), dim3(256), 0, s, a, counts, chunks);
   return hipGetLastError();
 }
-hipError_t launch_repair_map(const RepairArgs &a, uint32_t *cmap, uint4 *cdesc, hipStream_t s) {
+hipError_t launch_repair_map(const RepairArgs &a, uint4 *cdesc, hipStream_t s) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_repair_map, dim3(a.n), dim3(64), 0, s, a, cmap, cdesc);
+  hipLaunchKernelGGL(k_repair_map, dim3(a.n), dim3(64), 0, s, a, cdesc);
   return hipGetLastError();
 }
 
@@ -376,25 +375,12 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
   const uint32_t total = a.coff[a.n];
   unsigned long long evals = 0, rows = 0, recs = 0;
   for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
-    const uint32_t i = a.cmap[q];
-    const uint32_t j = q - a.coff[i];
-    const uint32_t p = a.ids[i];
-    uint32_t b0, b1;
-    rev_row(a, i, p, b0, b1);
-    const uint32_t nin = b1 - b0, nci = (nin + 63) / 64;
-    const bool inbound = j < nci;
-    int cnt;
-    uint32_t x, rbase;
-    if (inbound) {
-      const uint32_t e0 = j * 64;
-      cnt = (int)min(64u, nin - e0);
-      x = ln < cnt ? a.rev_src[b0 + e0 + ln] : kInvalid;
-      rbase = a.rofs[i] + e0 * (c + 1);
-    } else {
-      cnt = (int)R;
-      x = ln < cnt ? P.adj[(size_t)p * R + ln] : kInvalid;
-      rbase = a.rofs[i] + nin * (c + 1);
-    }
+    const uint4 d0 = a.cdesc[2 * (size_t)q], d1 = a.cdesc[2 * (size_t)q + 1];
+    const uint32_t i = d0.x, p = d0.y, j = d1.y, rbase = d1.x;
+    const bool inbound = d0.z != kInvalid;
+    const int cnt = (int)d0.w;
+    const uint32_t x =
+        ln < cnt ? (inbound ? a.rev_src[d0.z + ln] : P.adj[(size_t)p * R + ln]) : kInvalid;
     const bool xok = x != kInvalid && !a.in_batch[x];
     cidL[ln] = ln < kr ? a.ci[(size_t)i * kr + ln] : kInvalid;
     __syncthreads();
