@@ -236,36 +236,57 @@ static uint32_t robust_prune(const oindex *h, uint32_t p, const okey *cand_in, u
 /* ------------------------------------------------------------------------
  * Medoid (Alg. 5 starts from a pre-computed medoid; Section 6.2 notes a new
  * medoid is installed when the medoid is deleted).  Reading: the active id
- * minimising (fp64 squared distance to the centroid, id).  The centroid sums
- * each dimension exactly for uint8, and for fp32 in a fixed order: blocks of
- * 1024 consecutive ids summed in ascending id order, block sums added in
- * block order; it is then divided by the active count.  The distance to the
- * centroid is a fused multiply-add chain in dimension order.
+ * minimising (squared distance to the centroid, id).
+ *   uint8: exact.  With n active points and per-dimension sums S_j, the
+ *     squared distance of x to the centroid S/n is |n x - S|^2 / n^2, so the
+ *     comparison uses the integer key sum_j (n x_j - S_j)^2 (128-bit).
+ *   fp32: the centroid sums each dimension in a fixed order (blocks of 1024
+ *     consecutive ids summed in ascending id order, block sums added in
+ *     block order) and divides by n; the distance to it is a fused
+ *     multiply-add chain in fp64, in dimension order.
  * ---------------------------------------------------------------------- */
 #define O_CENTROID_BLOCK 1024u
+
+static uint32_t medoid_u8(const oindex *h, uint64_t n) {
+    const uint32_t d = h->cfg.dim, cap = h->cfg.capacity;
+    uint64_t *S = calloc(d, sizeof(uint64_t));
+    for (uint32_t i = 0; i < cap; i++) {
+        if (!h->active[i]) continue;
+        const uint8_t *x = vec_of(h, i);
+        for (uint32_t j = 0; j < d; j++) S[j] += x[j];
+    }
+    unsigned __int128 best = 0;
+    uint32_t arg = O_INVALID;
+    for (uint32_t i = 0; i < cap; i++) {
+        if (!h->active[i]) continue;
+        const uint8_t *x = vec_of(h, i);
+        unsigned __int128 key = 0;
+        for (uint32_t j = 0; j < d; j++) {
+            __int128 t = (__int128)n * x[j] - (__int128)S[j];
+            key += (unsigned __int128)(t * t);
+        }
+        if (arg == O_INVALID || key < best) { best = key; arg = i; }  /* ascending ids: ties keep the smaller id */
+    }
+    free(S);
+    return arg;
+}
 
 static uint32_t compute_medoid(const oindex *h) {
     const uint32_t d = h->cfg.dim, cap = h->cfg.capacity;
     uint64_t n = 0;
     for (uint32_t i = 0; i < cap; i++) n += h->active[i] ? 1 : 0;
     if (n == 0) return O_INVALID;
+    if (h->cfg.dtype == O_U8) return medoid_u8(h, n);
     double *c = calloc(d, sizeof(double));
     for (uint32_t j = 0; j < d; j++) {
-        if (h->cfg.dtype == O_U8) {
-            uint64_t s = 0;
-            for (uint32_t i = 0; i < cap; i++)
-                if (h->active[i]) s += ((const uint8_t *)vec_of(h, i))[j];
-            c[j] = (double)s / (double)n;
-        } else {
-            double t = 0.0;
-            for (uint32_t b0 = 0; b0 < cap; b0 += O_CENTROID_BLOCK) {
-                double sb = 0.0;
-                for (uint32_t i = b0; i < cap && i < b0 + O_CENTROID_BLOCK; i++)
-                    if (h->active[i]) sb = sb + (double)((const float *)vec_of(h, i))[j];
-                t = t + sb;
-            }
-            c[j] = t / (double)n;
+        double t = 0.0;
+        for (uint32_t b0 = 0; b0 < cap; b0 += O_CENTROID_BLOCK) {
+            double sb = 0.0;
+            for (uint32_t i = b0; i < cap && i < b0 + O_CENTROID_BLOCK; i++)
+                if (h->active[i]) sb = sb + (double)((const float *)vec_of(h, i))[j];
+            t = t + sb;
         }
+        c[j] = t / (double)n;
     }
     double best = INFINITY;
     uint32_t arg = O_INVALID;
@@ -273,9 +294,7 @@ static uint32_t compute_medoid(const oindex *h) {
         if (!h->active[i]) continue;
         double s = 0.0;
         for (uint32_t j = 0; j < d; j++) {
-            double x = h->cfg.dtype == O_U8 ? (double)((const uint8_t *)vec_of(h, i))[j]
-                                            : (double)((const float *)vec_of(h, i))[j];
-            double t = x - c[j];
+            double t = (double)((const float *)vec_of(h, i))[j] - c[j];
             s = fma(t, t, s);
         }
         if (s < best) { best = s; arg = i; }   /* ascending ids: ties keep the smaller id */
@@ -907,13 +926,23 @@ int32_t oracle_search(void *hv, const void *queries, uint32_t nq, uint32_t k, ui
     return O_OK;
 }
 
-/* Export: lists as stored (slot order), degrees, active map, medoid, and
- * optionally the reverse CSR (offsets: capacity + 1 entries). */
+/* Export: lists (Vamana lists are sets and are returned with each row
+ * ascending, INVALID last; CAGRA lists in slot order), degrees, active map,
+ * medoid, and optionally the reverse CSR (offsets: capacity + 1 entries). */
+static int u32_cmp(const void *pa, const void *pb) {
+    uint32_t a = *(const uint32_t *)pa, b = *(const uint32_t *)pb;
+    return a < b ? -1 : a > b ? 1 : 0;
+}
+
 int32_t oracle_export_graph(void *hv, uint32_t *adj, uint32_t *deg, uint8_t *active, uint32_t *medoid,
                             uint32_t *rev_offsets, uint32_t *rev_srcs, uint64_t *nnz) {
     oindex *h = hv;
     size_t cap = h->cfg.capacity;
-    if (adj) memcpy(adj, h->adj, cap * h->cfg.R * sizeof(uint32_t));
+    if (adj) {
+        memcpy(adj, h->adj, cap * h->cfg.R * sizeof(uint32_t));
+        if (h->cfg.algo == O_VAMANA)
+            for (size_t u = 0; u < cap; u++) qsort(adj + u * h->cfg.R, h->cfg.R, sizeof(uint32_t), u32_cmp);
+    }
     if (deg) memcpy(deg, h->deg, cap * sizeof(uint32_t));
     if (active) memcpy(active, h->active, cap);
     if (medoid) *medoid = h->medoid;

@@ -44,11 +44,27 @@ def test_reverse_csr_ignores_inactive_rows():
 
 
 # ---------------------------------------------------------------- medoid
-def test_medoid_hand_example():
-    o = Oracle(line_config(3, 2))
-    o.import_graph(np.array([[0.0], [1.0], [10.0]], np.float32), np.full((3, 2), INVALID, np.uint32),
-                   np.zeros(3, np.uint32), np.ones(3, np.uint8), INVALID)
-    assert o.medoid() == 1      # centroid 11/3: |1 - 11/3| is the smallest
+def _exact_u8_medoid(X, active):
+    """argmin over active ids of (|x - S/n|^2, id), compared exactly as
+    |n x - S|^2 with Python integers (reading Q13 for uint8)."""
+    ids = np.flatnonzero(active)
+    n = len(ids)
+    S = [int(v) for v in X[ids].astype(np.int64).sum(0)]
+    best = None
+    for i in ids:
+        key = sum((n * int(x) - s) ** 2 for x, s in zip(X[i], S))
+        if best is None or key < best[0]:
+            best = (key, int(i))
+    return best[1]
+
+
+def test_medoid_hand_examples(golden):
+    for case in golden("medoid_examples.json")["cases"]:
+        X = np.array(case["vectors"], np.uint8 if case["dtype"] == "u8" else np.float32)
+        n, d = X.shape
+        o = Oracle(IndexConfig("vamana", case["dtype"], "l2", d, n, 2, 4))
+        o.import_graph(X, np.full((n, 2), INVALID, np.uint32), np.zeros(n, np.uint32), np.ones(n, np.uint8), INVALID)
+        assert o.medoid() == case["expected"], case["name"]
 
 
 @pytest.mark.parametrize("dtype", ["u8", "f32"])
@@ -62,9 +78,12 @@ def test_medoid_matches_brute_force(dtype):
     act = (g.random(cap) < 0.7).astype(np.uint8)
     o.import_graph(X, np.full((cap, 4), INVALID, np.uint32), np.zeros(cap, np.uint32), act, INVALID)
     ids = np.flatnonzero(act)
-    c = X[ids].astype(np.float64).mean(0)
-    dd = ((X[ids].astype(np.float64) - c) ** 2).sum(1)
-    assert o.medoid() == ids[np.argmin(dd)]
+    if dtype == "u8":
+        assert o.medoid() == _exact_u8_medoid(X, act)
+    else:
+        c = X[ids].astype(np.float64).mean(0)
+        dd = ((X[ids].astype(np.float64) - c) ** 2).sum(1)
+        assert o.medoid() == ids[np.argmin(dd)]
 
 
 # ---------------------------------------------------------------- insert
@@ -137,23 +156,158 @@ def test_single_insert_into_complete_graph_prunes_all_points():
     ref.import_graph(X2, adj, deg, np.ones(n + 1, np.uint8), 0)
     D = np.array([ref.dist(X2[n], X2[j]) for j in range(n)], np.float32)
     expect = ref.robust_prune(n, np.arange(n, dtype=np.uint32), D)
-    assert st["adj"][n][: st["deg"][n]].tolist() == expect.tolist()
+    assert st["adj"][n][: st["deg"][n]].tolist() == sorted(expect.tolist())
 
 
-def test_bootstrap_candidates_are_batch_neighbours():
-    """Empty index: each new point's candidates are its nearest other batch
-    points; its list is drawn from them and the medoid is the brute-force one."""
+def _knn_sets_u8(X, k):
+    """Exact k nearest other points of every row, by (distance, id), with
+    int64 arithmetic (numpy brute force)."""
+    Xi = X.astype(np.int64)
+    out = []
+    for i in range(len(X)):
+        d = ((Xi - Xi[i]) ** 2).sum(1)
+        d[i] = np.iinfo(np.int64).max
+        order = np.lexsort((np.arange(len(X)), d))
+        out.append(set(order[:k].tolist()))
+    return out
+
+
+@pytest.mark.parametrize("ell", [3, 5])
+def test_bootstrap_lists_are_the_batch_knn(ell):
+    """Empty index (reading Q14): each new point's candidates are its
+    min(B-1, l) nearest other batch points.  With alpha -> infinity (no
+    pruning between distinct points) and R = l, the forward list is exactly
+    those l nearest; a reverse-edge rebuild keeps the R nearest of a union
+    that contains them, so every final list is the point's exact l-NN in
+    the batch, whatever P is.  Checked against numpy brute force."""
+    g = np.random.default_rng(14)
+    n, d = 60, 6
+    X = np.unique(g.integers(0, 256, (n + 10, d), dtype=np.uint8), axis=0)[:n]
+    X = g.permutation(X)
+    for P in (1, 64):
+        cfg = IndexConfig("vamana", "u8", "l2", d, n, ell, ell, alpha=1e30, P=P)
+        o = Oracle(cfg)
+        assert o.insert(np.arange(n, dtype=np.uint32), X) == 0
+        st = o.export()
+        check_graph_invariants(st, ell)
+        want = _knn_sets_u8(X, ell)
+        for i in range(n):
+            assert set(st["adj"][i][: st["deg"][i]].tolist()) == want[i], (P, i)
+
+
+def test_bootstrap_medoid_is_the_brute_force_medoid():
     g = np.random.default_rng(14)
     n, d = 200, 6
     cfg = IndexConfig("vamana", "u8", "l2", d, n, 8, 20)
     o = Oracle(cfg)
     X = g.integers(0, 256, (n, d), dtype=np.uint8)
-    ids = np.arange(n, dtype=np.uint32)
-    o.insert(ids, X)
+    o.insert(np.arange(n, dtype=np.uint32), X)
     st = o.export()
     check_graph_invariants(st, 8)
-    c = X.astype(np.float64).mean(0)
-    assert st["medoid"] == int(np.argmin(((X - c) ** 2).sum(1)))
+    assert st["medoid"] == _exact_u8_medoid(X, np.ones(n, bool))
+
+
+# ---------------------------------------------------------------- hand examples of Alg. 5 / Alg. 6
+def _line_index(coords, rows, R, medoid, extra=0, **kw):
+    """A 1-D fp32 index holding `coords` (ids 0..n-1) with the given lists,
+    and `extra` inactive slots after them."""
+    n = len(coords)
+    cfg = line_config(n + extra, R, **kw)
+    o = Oracle(cfg)
+    X = np.zeros((n + extra, 1), np.float32)
+    X[:n, 0] = coords
+    adj, deg = rows_to_adj(list(rows) + [[]] * extra, R)
+    act = np.zeros(n + extra, np.uint8)
+    act[:n] = 1
+    o.import_graph(X, adj, deg, act, medoid)
+    return o, X
+
+
+def _delete_cases():
+    from conftest import load_golden
+    return [c["name"] for c in load_golden("delete_repair_examples.json")["cases"]]
+
+
+@pytest.mark.parametrize("name", _delete_cases())
+def test_delete_repair_hand_examples(golden, name):
+    """Alg. 6 on a hand-derived 1-D graph: C_i without the batch, the c
+    closest of C_i for every in-neighbour z, the out-neighbour direction (w
+    enters the lists of its c closest points of C_i), the P cap keeping the
+    smallest (Dist, src) records, the dirty rebuild with and without prune,
+    and a deleted node without in-edges."""
+    fx = golden("delete_repair_examples.json")
+    case = next(c for c in fx["cases"] if c["name"] == name)
+    coords, rows = list(fx["coords"]), [list(r) for r in fx["rows"]]
+    if "extra_node" in case:
+        coords.append(case["extra_node"]["coord"])
+        rows.append(case["extra_node"]["row"])
+    o, _ = _line_index(coords, rows, case["R"], fx["medoid"], ell=fx["ell"], P=case["P"],
+                       k_repair=case["k_repair"], c=case["c"], max_iters=fx["max_iters"], alpha=fx["alpha"])
+    assert o.delete(np.array(case["delete"], np.uint32)) == 0
+    st = o.export()
+    got = [sorted(st["adj"][u][st["adj"][u] != INVALID].tolist()) for u in range(len(coords))]
+    assert got == [sorted(r) for r in case["expected_rows"]]
+    assert st["medoid"] == case["expected_medoid"]
+    assert not st["active"][case["delete"]].any()
+    check_graph_invariants(st, case["R"])
+
+
+@pytest.mark.parametrize("P", [1, 2])
+def test_scratch_cap_hand_examples(golden, P):
+    """Alg. 5 with the scratch capacity P (reading Q6): a target keeps the P
+    records with the smallest (Dist, src); the two new points search the
+    batch-start graph only."""
+    fx = golden("scratch_cap_examples.json")
+    case = next(c for c in fx["cases"] if c["P"] == P)
+    o, _ = _line_index(fx["coords"], fx["rows"], fx["R"], fx["medoid"], extra=2, ell=fx["ell"], P=P,
+                       alpha=fx["alpha"])
+    ids = np.array(fx["insert_ids"], np.uint32)
+    assert o.insert(ids, np.array(fx["insert_coords"], np.float32)[:, None]) == 0
+    st = o.export()
+    got = [sorted(st["adj"][u][st["adj"][u] != INVALID].tolist()) for u in range(4)]
+    assert got == [sorted(r) for r in case["expected_rows"]]
+
+
+def test_delete_without_in_edges_changes_only_out_repair_targets():
+    """Special case of Alg. 6: a deleted node that no list points to has no
+    in-neighbour repair, so the only lists that change are those of the
+    points that receive out-neighbour repair edges: for every surviving
+    out-neighbour w, the c points of C_x (the search's first k_repair
+    results) closest to w.  C_x comes from the pinned BeamSearch; the c
+    closest are picked with numpy."""
+    w = _small_u8(seed=6)
+    o = Oracle(w.cfg)
+    for op in w.base_batches():
+        o.insert(op.ids, op.vecs)
+    st0 = o.export()
+    act = np.flatnonzero(st0["active"])
+    g = np.random.default_rng(7)
+    x = int(np.flatnonzero(st0["active"] == 0)[0])
+    outs = g.choice(act, w.cfg.R // 2, replace=False).astype(np.uint32)
+    adj = st0["adj"].copy()
+    adj[x] = INVALID
+    adj[x, : outs.size] = outs
+    deg = st0["deg"].copy()
+    deg[x] = outs.size
+    active = st0["active"].copy()
+    active[x] = 1
+    vecs = w.vectors.copy()
+    vecs[x] = vecs[int(outs[0])] // 2 + 40
+    o.import_graph(vecs, adj, deg, active, st0["medoid"])
+    C, _, _, _ = o.beam_search(vecs[x], st0["medoid"], w.cfg.L_build, w.cfg.iters)
+    Cx = [int(v) for v in C if v != x][: w.cfg.k_repair]
+    V = vecs.astype(np.int64)
+    targets = set()
+    for wv in outs.tolist():
+        cand = [y for y in Cx if y != wv]
+        d = ((V[cand] - V[wv]) ** 2).sum(1)
+        targets.update(np.array(cand)[np.lexsort((cand, d))][: w.cfg.c].tolist())
+    assert o.delete(np.array([x], np.uint32)) == 0
+    st1 = o.export()
+    changed = set(np.flatnonzero(np.any(canonical_rows(st1["adj"]) != canonical_rows(adj), axis=1)).tolist())
+    assert x in changed
+    assert changed - {x} <= targets
+    assert changed - {x}, "some target gained an edge"
 
 
 @pytest.mark.parametrize("algo", ["vamana", "cagra"])
@@ -223,11 +377,7 @@ def test_delete_medoid_reinstalls_brute_force_medoid():
     med = o.export()["medoid"]
     assert o.delete(np.array([med], np.uint32)) == 0
     st = o.export()
-    act = st["active"].astype(bool)
-    X = w.vectors.astype(np.float64)
-    ids = np.flatnonzero(act)
-    c = X[ids].mean(0)
-    assert st["medoid"] == ids[np.argmin(((X[ids] - c) ** 2).sum(1))]
+    assert st["medoid"] == _exact_u8_medoid(w.vectors, st["active"].astype(bool))
     check_graph_invariants(st, w.cfg.R)
 
 
@@ -286,6 +436,26 @@ def test_cagra_insert_hand_example(golden):
     st = o.export()
     for k, row in fx["expected_rows"].items():
         assert st["adj"][int(k)].tolist() == row, k
+
+
+def test_cagra_insert_fills_an_empty_slot_first(golden):
+    """Reading Q16b: a CAGRA list below the fixed degree takes the new point
+    into its first empty slot; full lists follow the detour rule."""
+    fx = golden("cagra_examples.json")["insert_free_slot"]
+    n = len(fx["coords"])
+    cfg = line_config(n + 1, 3, ell=fx["ell"], algo="cagra")
+    o = Oracle(cfg)
+    X = np.zeros((n + 1, 1), np.float32)
+    X[:n, 0] = fx["coords"]
+    adj, deg = rows_to_adj(fx["rows"] + [[]], 3)
+    act = np.ones(n + 1, np.uint8)
+    act[n] = 0
+    o.import_graph(X, adj, deg, act, fx["medoid"])
+    assert o.insert(np.array([fx["new_id"]], np.uint32), np.array([[fx["new_coord"]]], np.float32)) == 0
+    st = o.export()
+    for k, row in fx["expected_rows"].items():
+        assert st["adj"][int(k)].tolist() == row, k
+    assert st["deg"][0] == 3
 
 
 def test_cagra_delete_hand_example(golden):
