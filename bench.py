@@ -1,6 +1,6 @@
 #!/usr/bin/env python3
-"""Throughput of batched dynamic updates and search of a GrAND-Vamana index
-on one MI355X.
+"""Throughput of batched dynamic updates and search of a GrAND index on one
+MI355X.
 
 Workload (default): 1,000,000 x 128 uint8 vectors from a 256-component
 Gaussian mixture (centres U[0,255], sigma 20, rounded and clipped), L2,
@@ -8,18 +8,26 @@ Vamana R=64, L=128, alpha=1.2.  The base index is built by 100 batched
 inserts of 10,000, then refreshed once: each base batch is deleted and
 re-inserted with the same ids and vectors, so every list is rebuilt against
 the complete base set (the batched counterpart of a static build's second
-pass; untimed).  A step is one round of the streaming
-workload: +10,000 inserts (smallest free ids), -10,000 uniformly random
-deletes, 10,000 queries (k=10, beam 64).  Inputs of every round are staged
-in device memory before timing.  One JSON line is printed:
+pass; untimed).  A step is one round of the streaming workload: +10,000
+inserts (smallest free ids), -10,000 uniformly random deletes, 10,000
+queries (k=10, beam 64).  Inputs of every round are staged in device memory
+before timing.  One JSON line is printed:
   value       = updates/s (inserts + deletes over the time of the insert
                 and delete calls), with search QPS and recall@10 alongside;
   roofline    = achieved algorithmic bandwidth of the dominant kernel (the
                 one with the largest share of GPU time: k_search, whose
                 insert, delete and query launches are summed), from HIP
-                events on the library's stream around each phase; the
-                other phases' figures are listed beside it;
-  cpu_baseline= the CPU oracle timed on a bounded sample of the workload.
+                events on the library's stream around each phase.  A search
+                is charged for the distinct ids whose distance it needs,
+                counted exactly by an untimed rerun of the same rounds on the
+                same state with an exact visited set; the fraction over every
+                evaluation the timed kernel made is given beside it.  The
+                other phases' figures are listed in roofline_other_phases;
+  cpu_baseline= the CPU oracle on the host cores allotted to the job, on the
+                state the timed rounds start from, for the first timed round.
+Other workloads (--workload) are the fp32 sliding window, the CAGRA
+inner-product set, the 960-d set and the tiny set; their lines carry their
+own metric and data labels.
 """
 import argparse
 import json
@@ -31,8 +39,28 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-METRIC = "updates/sec and search QPS at recall@10≥0.95, 1M×128, 1 MI355X"
+HEADLINE_METRIC = "updates/sec and search QPS at recall@10≥0.95, 1M×128, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+
+# what each synthetic workload stands in for (no dataset is available here)
+DATA_LABEL = {
+    "sift1m_u8": "synthetic (seeded 256-component uint8 mixture; stands in for the paper's SIFT-like 128-d set)",
+    "deep1m_window": "synthetic (seeded 512-component mixture, L2-normalised, drifting weights; stands in for the "
+                     "paper's 96-d Euclidean set under the sliding-window pattern)",
+    "glove1m_cagra": "synthetic (seeded 1,000-component Student-t(3) mixture, unit-normalised; stands in for the "
+                     "paper's 100-d angular set)",
+    "gist500k": "synthetic (seeded 128-component mixture, per-dimension scales, clipped at 0; a 960-d stress case)",
+    "tiny": "synthetic (seeded N(0,1), 10,000 x 32)",
+}
+SHAPE = {"sift1m_u8": "1M×128 uint8", "deep1m_window": "1M×96 fp32 sliding window",
+         "glove1m_cagra": "1M×100 fp32 IP, CAGRA degree 64", "gist500k": "500K×960 fp32", "tiny": "10K×32 fp32"}
+
+
+def metric_of(workload, recall_min):
+    if workload == "sift1m_u8":
+        return HEADLINE_METRIC
+    r = "n/a" if recall_min is None else f"{recall_min:.3f}"
+    return f"updates/sec and search QPS at recall@10 (min {r}), {SHAPE.get(workload, workload)}, 1 MI355X"
 
 
 def log(*a):
@@ -56,7 +84,6 @@ def parse():
     ap.add_argument("--rev-mode", choices=["full", "batch"], default="full")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=100_000, help="base size of the oracle's sample index")
     ap.add_argument("--no-recall", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
@@ -116,11 +143,20 @@ class Mirror:
 
 
 # ------------------------------------------------------------------ algorithmic bytes
-def algorithmic_bytes(st, phase, cfg, stride):
+def algorithmic_bytes(st, phase, cfg, stride, distinct=None):
     """Bytes each phase must move over the timed region, from the kernels'
     own work counters (a vector row is `stride` bytes, an adjacency row 4R):
       search : per query one query row; per expanded node one adjacency row;
-               per distance evaluation one vector row; outputs;
+               per distance the search needs one vector row (the distinct
+               ids of a counting rerun when given, else every evaluation the
+               kernel made); outputs;
+      prune_fwd: per new point its row and its |V_i| candidate rows, V_i
+               (8 B an entry), its list (4R) and its records (12 B);
+      group  : every record read (12 B) and written grouped (8 B); per
+               dirty node its offset and its dirty-list entry;
+      reverse: one read of every adjacency row and of the active map, one
+               write of the offsets and of the sources (per launch:
+               capacity x (4R + 1) + 4 (capacity + 1) + 4 nnz);
       rebuild: per dirty node its degree, adjacency row read and written,
                8 B per scratch record; per pruning rebuild the |C| candidate
                rows and u's row (pairwise distances reuse those rows);
@@ -129,10 +165,20 @@ def algorithmic_bytes(st, phase, cfg, stride):
     R = cfg.R
     if phase.startswith("search_"):
         w = phase.split("_")[1]
-        hops, evals = st[f"hops_{w}"], st[f"evals_{w}"]
+        hops = st[f"hops_{w}"]
+        evals = st[f"evals_{w}"] if distinct is None else distinct[w]
         n = {"insert": st["inserted"], "delete": st["deleted"], "query": st["queried"]}[w]
         outb = {"insert": 8 * hops, "delete": 4 * n * cfg.k_repair, "query": 8 * n * 10}[w]
         return n * stride + hops * 4 * R + evals * stride + outb
+    if phase == "prune_fwd":
+        n = st["inserted"]
+        fwd_records = st["records"] - st["repair_records"]
+        return (st["hops_insert"] + n) * stride + 8 * st["hops_insert"] + n * 4 * R + 12 * fwd_records
+    if phase == "group":
+        return 20 * st["records"] + 8 * st["dirty"]
+    if phase == "reverse":
+        launches = st["phase_calls"]["reverse"]
+        return launches * (cfg.capacity * (4 * R + 1) + 4 * (cfg.capacity + 1)) + 4 * st["rev_edges"]
     if phase == "rebuild":
         return st["dirty"] * (8 * R + 4) + 8 * st["rebuild_records"] + st["rebuild_rows"] * stride
     if phase == "repair":
@@ -169,45 +215,63 @@ def profiled_traffic(phase):
 
 
 # ------------------------------------------------------------------ cpu baseline
-def cpu_baseline(args, threads):
-    """The oracle (plain C, OpenMP over batch items) on a bounded sample of the
-    same workload: an index of `cpu_sample` points of the same mixture and
-    parameters built untimed, then one round of the same batch sizes timed."""
+def host_cpu():
+    """CPU model and core counts of this host (lscpu-style, from /proc)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "host_cores": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+def oracle_threads():
+    """Threads for the oracle: the CPU share the job is given (the
+    OMP_NUM_THREADS the environment sets for one GPU's job), else every core
+    this process may run on."""
+    share = os.environ.get("OMP_NUM_THREADS")
+    aff = len(os.sched_getaffinity(0))
+    return min(int(share), aff) if share and share.isdigit() and int(share) > 0 else aff
+
+
+def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
+    """The oracle (plain C, OpenMP over batch items) on the state the timed
+    rounds start from (imported), timed on the first timed round's own
+    batches: the same workload at the same scale, on `threads` host cores."""
     from oracle.oracle import Oracle
-    from workloads import make_workload
-    base = make_workload(args.workload)
-    n_ops = base.spec.n_insert
-    w = make_workload(args.workload, seed=args.seed + 1,
-                      index=dict(capacity=args.cpu_sample + n_ops),
-                      stream=dict(base_n=args.cpu_sample, n_rounds=1))
-    o = Oracle(w.cfg, threads=threads)
+    o = Oracle(cfg, threads=threads)
     t0 = time.perf_counter()
-    for b, op in enumerate(w.base_batches()):
-        o.insert(op.ids, op.vecs)
-        log(f"cpu baseline: sample build batch {b + 1}, {time.perf_counter() - t0:.1f} s")
-    build_s = time.perf_counter() - t0
+    o.import_graph(snap["vecs"], snap["adj"], snap["deg"], snap["active"], snap["medoid"])
+    log(f"cpu baseline: state imported in {time.perf_counter() - t0:.1f} s; oracle on {threads} threads ...")
     t_upd = t_q = 0.0
     n_upd = n_q = 0
-    for _, ops in w.rounds(1):
-        for op in ops:
-            t0 = time.perf_counter()
-            if op.kind == "insert":
-                o.insert(op.ids, op.vecs)
-                t_upd += time.perf_counter() - t0
-                n_upd += len(op.ids)
-            elif op.kind == "delete":
-                o.delete(op.ids)
-                t_upd += time.perf_counter() - t0
-                n_upd += len(op.ids)
-            else:
-                o.search(op.vecs, w.spec.k, w.spec.beam)
-                t_q += time.perf_counter() - t0
-                n_q += len(op.vecs)
-    return {"value": n_upd / t_upd, "unit": "updates/s", "cores": threads, "kind": "oracle",
-            "search_qps": n_q / t_q,
-            "sample": (f"oracle on a {args.cpu_sample:,}-point index of the same mixture and parameters "
-                       f"(built untimed in {build_s:.1f} s), one round of {n_ops:,} inserts + "
-                       f"{w.spec.n_delete:,} deletes + {w.spec.n_query:,} queries")}
+    done = []
+    for kind, ids, vecs in host_round:
+        t0 = time.perf_counter()
+        if kind == "insert":
+            o.insert(ids, vecs)
+            t_upd += time.perf_counter() - t0
+            n_upd += len(ids)
+        elif kind == "delete":
+            o.delete(ids)
+            t_upd += time.perf_counter() - t0
+            n_upd += len(ids)
+        else:
+            o.search(vecs, spec.k, spec.beam)
+            t_q += time.perf_counter() - t0
+            n_q += len(vecs)
+        done.append(f"{len(ids) if ids is not None else len(vecs):,} {kind}s")
+        log(f"cpu baseline: {kind} done, {time.perf_counter() - t0:.1f} s")
+    out = {"value": round(n_upd / t_upd, 1) if t_upd > 0 else None, "unit": "updates/s", "cores": threads,
+           "kind": "oracle", "search_qps": round(n_q / t_q, 1) if t_q > 0 else None,
+           "sample": (f"oracle on the {int(snap['active'].sum()):,}-point index the timed rounds start from "
+                      f"(imported from the GPU), timed on the first timed round: " + ", ".join(done)),
+           "cpu": host_cpu()}
+    return out
 
 
 # ------------------------------------------------------------------ main
@@ -281,11 +345,19 @@ def main():
     build_s = time.perf_counter() - t0
     log(f"build done: {spec.base_n:,} points in {build_s:.1f} s")
 
-    # ---- stage every round's inputs on the device, with exact ground truth
+    # ---- stage every round's inputs on the device, with exact ground truth;
+    # the pool as the timed rounds find it is kept for the counting rerun and
+    # the CPU baseline, and the first timed round's batches on the host
     rounds = []
+    snap_vecs = None
+    host_round = []
     for r in range(W + K):
+        if r == W:
+            snap_vecs = mirror.pool.clone()
         ops = []
         for op in w.round_ops(r):
+            if r == W:
+                host_round.append((op.kind, op.ids, op.vecs))
             if op.kind == "insert":
                 ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
                 mirror.insert(ids, vecs)
@@ -320,6 +392,8 @@ def main():
 
     for r in range(W):
         run_round(rounds[r], [])
+    snap = g.export()     # the state the timed rounds start from
+    snap["vecs"] = snap_vecs
     g.reset_stats()
     g.set_timing(True)
     events = []
@@ -330,6 +404,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = g.stats()
+    g.set_timing(False)
 
     upd_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in events if k != "search")
     upd_n = sum(n for k, n, e0, e1 in events if k != "search")
@@ -348,6 +423,25 @@ def main():
                 hit = (got[:, :, None] == gt[:, None, :]).any(2).sum(1).float()
                 recalls.append(float(hit.mean() / spec.k))
 
+    # ---- counting rerun (untimed): the same rounds from the same state, with
+    # an exact visited set in every search, give the distinct ids whose
+    # distance each search needs.  The path is deterministic, so the rerun
+    # performs the same searches as the timed rounds.
+    distinct = None
+    t0 = time.perf_counter()
+    g.import_graph(snap["vecs"], snap["adj"], snap["deg"], snap["active"], snap["medoid"])
+    g.reset_stats()
+    g.set_counting(True)
+    for r in range(W, W + K):
+        run_round(rounds[r], [])
+    torch.cuda.synchronize()
+    cst = g.stats()
+    g.set_counting(False)
+    same = all(cst[f"hops_{x}"] == 0 for x in ("insert", "delete", "query"))
+    distinct = {x: cst[f"distinct_{x}"] for x in ("insert", "delete", "query")}
+    log(f"counting rerun: {time.perf_counter() - t0:.1f} s; distinct {distinct} (counters of the timed kernels "
+        f"untouched: {same})")
+
     # ---- roofline of the dominant kernel (largest share of the timed region).
     # Phase times come from HIP events on the library stream around each
     # phase.  The three search phases are launches of one kernel (k_search);
@@ -357,21 +451,25 @@ def main():
         calls = st["phase_calls"][ph]
         if calls == 0:
             continue
-        b = algorithmic_bytes(st, ph, cfg, stride)
+        b = algorithmic_bytes(st, ph, cfg, stride, distinct)
         phases[ph] = {"ms_total": round(ms, 3), "launches": int(calls), "ms_per_launch": round(ms / calls, 4)}
         if b is not None:
             phases[ph]["alg_bytes"] = b
             phases[ph]["alg_GB_per_launch"] = round(b / calls / 1e9, 5)
             phases[ph]["achieved_GBps"] = round(b / (ms / 1e3) / 1e9, 1)
+            if ph.startswith("search_"):
+                be = algorithmic_bytes(st, ph, cfg, stride, None)
+                phases[ph]["alg_bytes_all_evals"] = be
     groups = {}
     for ph, v in phases.items():
         if "alg_bytes" not in v:
             continue
         kern = "k_search" if ph.startswith("search_") else ph
-        g_ = groups.setdefault(kern, {"ms": 0.0, "launches": 0, "bytes": 0.0, "phases": []})
+        g_ = groups.setdefault(kern, {"ms": 0.0, "launches": 0, "bytes": 0.0, "bytes_all": 0.0, "phases": []})
         g_["ms"] += v["ms_total"]
         g_["launches"] += v["launches"]
         g_["bytes"] += v["alg_bytes"]
+        g_["bytes_all"] += v.get("alg_bytes_all_evals", v["alg_bytes"])
         g_["phases"].append(ph)
     profiled_ok = args.workload == "sift1m_u8" and not args.base and not args.build_batch
 
@@ -384,33 +482,51 @@ def main():
             if all(x is not None for x in per):
                 # per-launch traffic of each phase, weighted by its launches
                 tb = sum(x * phases[ph]["launches"] for x, ph in zip(per, g_["phases"])) / g_["launches"]
-        return {"bound": "hbm", "kernel": kern, "phases": g_["phases"], "achieved": round(ach, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                "traffic": None if tb is None else round(tb / 1e9, 5),
-                "traffic_unit": "GB per launch, HBM read + write (rocprofv3 FETCH_SIZE and WRITE_SIZE, "
-                                "calibrated on a 1 GiB copy; profiles/traffic_sift1m_u8.md)",
-                "ms_per_launch": round(g_["ms"] / g_["launches"], 4),
-                "alg_GB_per_launch": round(g_["bytes"] / g_["launches"] / 1e9, 5),
-                "ms_total": round(g_["ms"], 3)}
+        out = {"bound": "hbm", "kernel": kern, "phases": g_["phases"], "achieved": round(ach, 1),
+               "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+               "traffic": None if tb is None else round(tb / 1e9, 5),
+               "traffic_unit": "GB per launch, HBM read + write (rocprofv3 FETCH_SIZE and WRITE_SIZE, "
+                               "calibrated on a 1 GiB copy; profiles/traffic_sift1m_u8.md)",
+               "ms_per_launch": round(g_["ms"] / g_["launches"], 4),
+               "alg_GB_per_launch": round(g_["bytes"] / g_["launches"] / 1e9, 5),
+               "ms_total": round(g_["ms"], 3)}
+        if kern == "k_search":
+            ach_all = g_["bytes_all"] / (g_["ms"] / 1e3) / 1e9
+            out["bytes_basis"] = "distinct distance evaluations (counting rerun)"
+            out["frac_all_evaluations"] = round(ach_all / HBM_PEAK_GBS, 4)
+            out["alg_GB_per_launch_all_evaluations"] = round(g_["bytes_all"] / g_["launches"] / 1e9, 5)
+        return out
 
     dom = max(groups, key=lambda k: groups[k]["ms"]) if groups else None
     roofline = roof(dom) if dom else None
     others = {k: roof(k) for k in groups if k != dom}
     for v in phases.values():
         v.pop("alg_bytes", None)
+        v.pop("alg_bytes_all_evals", None)
+
+    searches = {"insert": st["inserted"], "delete": st["deleted"], "query": st["queried"]}
+    search_stats = {x: {"searches": int(searches[x]), "hops": int(st[f"hops_{x}"]),
+                        "evaluations": int(st[f"evals_{x}"]), "distinct": int(distinct[x]),
+                        "repeat_frac": round(1.0 - distinct[x] / max(st[f"evals_{x}"], 1), 4),
+                        "max_iters_hits": int(st[f"capped_{x}"]),
+                        "max_iters_hit_rate": round(st[f"capped_{x}"] / max(searches[x], 1), 5)}
+                    for x in ("insert", "delete", "query") if searches[x]}
 
     cpu = None
     if not args.no_cpu_baseline:
-        threads = min(16, os.cpu_count() or 1)
-        log(f"cpu baseline: oracle on {threads} threads ...")
-        cpu = cpu_baseline(args, threads)
+        snap_host = dict(snap)
+        snap_host["vecs"] = snap["vecs"].cpu().numpy()
+        cpu = cpu_baseline(cfg, spec, snap_host, host_round, oracle_threads())
+        if args.workload == "tiny":
+            cpu["one_core"] = cpu_baseline(cfg, spec, snap_host, host_round, 1)
 
     value = upd_n / (upd_ms / 1e3)
+    rmin = round(min(recalls), 4) if recalls else None
     res = {
-        "metric": METRIC, "value": round(value, 1), "unit": "updates/s", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": round(wall * 1e3 / K, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "u8" if cfg.dtype == "u8" else "f32",
-        "data": "synthetic (seeded mixture; stands in for the paper's SIFT-like 128-d dataset)",
+        "metric": metric_of(args.workload, rmin), "value": round(value, 1), "unit": "updates/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(wall * 1e3 / K, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8" if cfg.dtype == "u8" else "f32",
+        "data": DATA_LABEL.get(args.workload, "synthetic"),
         "config": {"workload": w.wdef.description, "base_points": spec.base_n, "insert_batch": spec.n_insert,
                    "delete_batch": spec.n_delete, "queries": spec.n_query, "k": spec.k, "beam": spec.beam,
                    "R": cfg.R, "L": cfg.L_build, "alpha": cfg.alpha, "P": cfg.P, "c": cfg.c,
@@ -420,13 +536,14 @@ def main():
         "search_qps": round(q_n / (q_ms / 1e3), 1),
         "insert_per_s": round(spec.n_insert * K / (ins_ms / 1e3), 1),
         "delete_per_s": round(spec.n_delete * K / (del_ms / 1e3), 1),
-        "recall_at_10_min": round(min(recalls), 4) if recalls else None,
+        "recall_at_10_min": rmin,
         "recall_at_10_mean": round(float(np.mean(recalls)), 4) if recalls else None,
         "recall_at_10_per_round": [round(x, 4) for x in recalls],
         "build_s": round(build_s, 2),
         "roofline": roofline,
         "roofline_other_phases": others,
         "cpu_baseline": cpu,
+        "searches": search_stats,
         "phases": phases,
         "counters": {k: v for k, v in st.items() if isinstance(v, int)},
     }

@@ -130,8 +130,11 @@ grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint
                           uint32_t *out_ids, float *out_dists);
 
 /* Copies the index state out.  Any output pointer may be NULL.
- *   adj: capacity x R lists as stored (Vamana lists are sets; CAGRA slot
- *        order is meaningful), GRAND_INVALID padding;  deg: capacity;
+ *   adj: capacity x R lists, GRAND_INVALID padding.  Vamana lists are sets
+ *        (their order carries no meaning) and are returned canonically:
+ *        each row's ids ascending, padding last.  CAGRA lists are returned
+ *        in slot order, which the find-and-replace rules depend on;
+ *   deg: capacity;
  *   active: capacity bytes (0/1);  medoid: 1 id (GRAND_INVALID if empty).
  *   rev_offsets (capacity + 1) / rev_srcs: the reverse graph of the current
  *        graph in CSR form, rows ascending by source id (Alg. 8).  With
@@ -173,6 +176,9 @@ typedef struct {
   uint64_t rebuild_rows;           /* vector rows pruning rebuilds need (|C| + 1 each) */
   uint64_t repair_rows;            /* vector rows repairs need (neighbours + |C_i|) */
   uint64_t repair_records;         /* records written by repairs */
+  uint64_t search_distinct[3];     /* distinct ids whose distance a search needs: {start} and every
+                                      neighbour of an expanded node (counting runs only) */
+  uint64_t search_capped[3];       /* searches stopped by max_iters with unexpanded candidates left */
   double phase_ms[GRAND_NPHASE];   /* summed kernel time per phase (timing enabled) */
   uint64_t phase_calls[GRAND_NPHASE];
 } grand_stats_t;
@@ -182,7 +188,21 @@ typedef struct {
  * timed, since each recorded event adds a short gap on the stream; their
  * phase_ms stay 0. */
 grand_status grand_set_timing(grand_index *h, int enable);
-grand_status grand_get_stats(grand_index *h, grand_stats_t *out);
+
+/* Enables (1) or disables (0) counting runs, a measurement mode: every
+ * search then uses an exact visited bitmap of one bit per pool id in device
+ * memory (capacity/8 bytes per search of a launch, allocated on demand)
+ * instead of its lossy visited hash, so that each needed distance is
+ * evaluated once and search_distinct counts the method's own distance
+ * evaluations (Alg. 1 needs Dist for the start and for every neighbour of
+ * an expanded node).  Results are the same as without counting; searches
+ * are slower.  Errors: GRAND_E_OOM when the bitmap cannot be allocated. */
+grand_status grand_set_counting(grand_index *h, int enable);
+
+/* Copies the counters into out, which must point to at least `size` >=
+ * sizeof(grand_stats_t) bytes laid out as grand_stats_t (its struct_size
+ * is set).  Errors: GRAND_E_ARG for a null or smaller buffer. */
+grand_status grand_stats(grand_index *h, void *out, size_t size);
 grand_status grand_reset_stats(grand_index *h);
 
 /* Text of the last error on this handle ("" if none). */

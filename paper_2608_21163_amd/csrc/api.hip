@@ -15,6 +15,7 @@
 
 using namespace gr;
 
+
 struct grand_index {
   grand_params p{};
   hipStream_t stream = nullptr;
@@ -58,6 +59,10 @@ struct grand_index {
   uint8_t *q_vecs = nullptr;
   uint32_t *q_ids = nullptr;
   float *q_d = nullptr;
+  // counting runs: an exact visited bitmap per search (measurement only)
+  bool counting = false;
+  uint32_t *vis = nullptr;
+  size_t vis_cap = 0;  // words
   // timing and stats
   bool timing = false;
   std::vector<std::tuple<int, hipEvent_t, hipEvent_t>> pending;
@@ -184,7 +189,7 @@ grand_status read_validation(grand_index *h) {
 }
 
 grand_status clear_errors(grand_index *h) {
-  HCHK(h, hipMemsetAsync(&h->ds->err_code, 0, 2 * sizeof(uint32_t), h->stream));
+  HCHK(h, launch_fill_u32(&h->ds->err_code, 0u, 2, h->stream));  // err_code and err_id
   return GRAND_OK;
 }
 
@@ -298,6 +303,28 @@ grand_status run_medoid(grand_index *h, const uint8_t *in_batch, int force) {
   return GRAND_OK;
 }
 
+// Counting runs: gives a search launch a cleared visited bitmap of one bit
+// per pool id for each of its nq searches (grown on demand).
+grand_status prep_counting(grand_index *h, SearchArgs &a) {
+  if (!h->counting || a.nq == 0) return GRAND_OK;
+  const size_t words = ((size_t)h->p.capacity + 31) / 32;
+  const size_t need = words * a.nq;
+  if (need > h->vis_cap) {
+    HCHK(h, hipStreamSynchronize(h->stream));
+    dfree(h->vis);
+    h->vis_cap = 0;
+    if (dalloc(&h->vis, need)) {
+      (void)hipGetLastError();
+      return fail(h, GRAND_E_OOM, "device allocation of the counting bitmap failed");
+    }
+    h->vis_cap = need;
+  }
+  HCHK(h, launch_fill_u32(h->vis, 0u, need, h->stream));
+  a.vis = h->vis;
+  a.vis_words = (uint32_t)words;
+  return GRAND_OK;
+}
+
 // The reverse graph of the current graph: rows of every id (full) or of the
 // batch positions of the delete batch (by_batch).  The source array is part
 // of the resource pool (capacity x R entries bound every reverse graph).
@@ -338,6 +365,7 @@ grand_status vamana_insert(grand_index *h, uint32_t n, uint64_t n0) {
     a.v_n = h->v_n;
     a.v_stride = h->iters;
     a.ds = h->ds;
+    if (grand_status s_ = prep_counting(h, a)) return s_;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
   grand_status s = ensure_records(h, (size_t)n * R);
@@ -392,6 +420,7 @@ grand_status cagra_insert(grand_index *h, uint32_t n, uint64_t n0) {
     a.c_d = h->c_d;
     a.c_out = R;
     a.ds = h->ds;
+    if (grand_status s_ = prep_counting(h, a)) return s_;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
   grand_status s = ensure_records(h, (size_t)n * R);
@@ -448,6 +477,7 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
     a.c_out = kr;
     a.c_filter = h->in_batch;
     a.ds = h->ds;
+    if (grand_status s_ = prep_counting(h, a)) return s_;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
   s = run_reverse(h, by_batch, n, h->side);
@@ -573,6 +603,7 @@ void release(grand_index *h) {
   dfree(h->grp.pt); dfree(h->grp.ps); dfree(h->grp.pd); dfree(h->grp.mat); dfree(h->grp.mato); dfree(h->grp.tmp);
   dfree(h->grp.dpad); dfree(h->grp.dcnt);
   dfree(h->q_vecs); dfree(h->q_ids); dfree(h->q_d);
+  dfree(h->vis);
   for (auto &t : h->pending) {
     if (std::get<1>(t)) (void)hipEventDestroy(std::get<1>(t));
     if (std::get<2>(t)) (void)hipEventDestroy(std::get<2>(t));
@@ -834,6 +865,7 @@ grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint
     a.c_d = h->q_d;
     a.c_out = k;
     a.ds = h->ds;
+    if (grand_status s_ = prep_counting(h, a)) return s_;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
   }
   HCHK(h, hipMemcpyAsync(out_ids, h->q_ids, (size_t)nq * k * 4, hipMemcpyDefault, h->stream));
@@ -848,7 +880,14 @@ grand_status grand_export_graph(grand_index *h, uint32_t *adj, uint32_t *deg, ui
   if (s != GRAND_OK) return s;
   HCHK(h, hipSetDevice(h->p.device));
   const size_t cap = h->p.capacity;
-  if (adj) HCHK(h, hipMemcpyAsync(adj, h->pool.adj, cap * h->p.R * 4, hipMemcpyDefault, h->stream));
+  if (adj && h->p.algo == GRAND_VAMANA) {
+    // Vamana lists are sets: returned with each row ascending (the reverse
+    // graph's source array is free scratch between delete batches)
+    HCHK(h, launch_sort_adj_rows(h->pool.adj, (uint32_t)cap, h->p.R, h->rev_src, h->stream));
+    HCHK(h, hipMemcpyAsync(adj, h->rev_src, cap * h->p.R * 4, hipMemcpyDefault, h->stream));
+  } else if (adj) {
+    HCHK(h, hipMemcpyAsync(adj, h->pool.adj, cap * h->p.R * 4, hipMemcpyDefault, h->stream));
+  }
   if (deg) HCHK(h, hipMemcpyAsync(deg, h->pool.deg, cap * 4, hipMemcpyDefault, h->stream));
   if (active) HCHK(h, hipMemcpyAsync(active, h->pool.active, cap, hipMemcpyDefault, h->stream));
   if (rev_offsets || rev_srcs || nnz) {
@@ -953,10 +992,23 @@ grand_status grand_set_timing(grand_index *h, int enable) {
   return GRAND_OK;
 }
 
-grand_status grand_get_stats(grand_index *h, grand_stats_t *out) {
+grand_status grand_set_counting(grand_index *h, int enable) {
   grand_status s = check_usable(h);
   if (s != GRAND_OK) return s;
-  if (!out || out->struct_size != sizeof(grand_stats_t)) return fail(h, GRAND_E_ARG, "bad stats struct");
+  HCHK(h, hipStreamSynchronize(h->stream));
+  h->counting = enable != 0;
+  if (!h->counting) {
+    dfree(h->vis);
+    h->vis_cap = 0;
+  }
+  return GRAND_OK;
+}
+
+grand_status grand_stats(grand_index *h, void *out_v, size_t size) {
+  grand_status s = check_usable(h);
+  if (s != GRAND_OK) return s;
+  if (!out_v || size < sizeof(grand_stats_t)) return fail(h, GRAND_E_ARG, "stats buffer smaller than grand_stats_t");
+  grand_stats_t *out = static_cast<grand_stats_t *>(out_v);
   if ((s = finish(h)) != GRAND_OK) return s;
   HCHK(h, hipMemcpyAsync(h->hs->stat, h->ds->stat, sizeof(h->hs->stat), hipMemcpyDeviceToHost, h->stream));
   HCHK(h, hipStreamSynchronize(h->stream));
@@ -980,6 +1032,11 @@ grand_status grand_get_stats(grand_index *h, grand_stats_t *out) {
   r.rebuild_rows = c[kStRbCand];
   r.repair_rows = c[kStRepRows];
   r.repair_records = c[kStRepRecs];
+  for (int i = 0; i < 3; i++) {
+    r.search_distinct[i] = c[kStDistinct + i];
+    r.search_capped[i] = c[kStCapped + i];
+  }
+  r.struct_size = sizeof(grand_stats_t);
   *out = r;
   return GRAND_OK;
 }

@@ -32,7 +32,9 @@ enum StatId {
   kStRbCand,       // vector rows a pruning rebuild needs: |C| + 1
   kStRepRows,      // vector rows a repair needs: neighbours + |C_i|
   kStRepRecs,      // records written by repairs
-  kStatCount
+  kStDistinct,     // distinct distance evaluations of [insert, delete, query] searches (counting runs) (3)
+  kStCapped = kStDistinct + 3,  // searches stopped by the expansion cap with candidates left (3)
+  kStatCount = kStCapped + 3
 };
 constexpr int kStatWords = 32;
 constexpr int kStatSlots = 256;
@@ -47,7 +49,9 @@ struct DevScalars {
   uint32_t n_queue;                 // dirty nodes left by the fast rebuild for the general one
   uint32_t medoid;
   uint32_t best_id;
-  unsigned long long best_bits;     // medoid search: smallest squared distance (bit pattern)
+  unsigned long long best_bits;     // medoid search: smallest squared distance (fp32 data: bit pattern;
+                                    // uint8 data: low 64 bits of the exact integer key)
+  unsigned long long best_hi;       // uint8 medoid search: high 64 bits of the smallest key
   uint32_t need_medoid;             // medoid kernels run only when set
   uint32_t pad_;
   unsigned long long n_count;       // scratch counter (active ids at import)
@@ -97,6 +101,10 @@ struct SearchArgs {
   float *c_d;
   uint32_t c_out;
   const uint8_t *c_filter;
+  // counting runs only: an exact visited bitmap of vis_words words per
+  // search (cleared by the caller) replaces the lossy hash
+  uint32_t *vis;
+  uint32_t vis_words;
   DevScalars *ds;
 };
 
@@ -271,6 +279,7 @@ struct RevBufs {
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
                           uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,
                           DevScalars *ds, hipStream_t s);
+hipError_t launch_sort_adj_rows(const uint32_t *adj, uint32_t cap, uint32_t R, uint32_t *dst, hipStream_t s);
 hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst,
                             hipStream_t s);
 hipError_t launch_medoid(PoolView p, int kind, uint32_t dim, uint64_t n_active, void *tmp, DevScalars *ds,

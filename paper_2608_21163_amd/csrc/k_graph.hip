@@ -1137,14 +1137,39 @@ hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t 
   return hipGetLastError();
 }
 
+// Copies the fixed-width lists of every node with each row sorted ascending
+// (INVALID, the largest value, last): the canonical form of Vamana lists,
+// whose order carries no meaning.  One wave per row, R <= 64.
+__global__ __launch_bounds__(64) void k_sort_adj_rows(const uint32_t *adj, uint32_t cap, uint32_t R, uint32_t *dst) {
+  const int ln = lane();
+  for (uint32_t u = blockIdx.x; u < cap; u += gridDim.x) {
+    float d[1] = {0.0f};
+    uint32_t v[1] = {ln < (int)R ? adj[(size_t)u * R + ln] : kInvalid};
+    wave_sort<1>(d, v);
+    if (ln < (int)R) dst[(size_t)u * R + ln] = v[0];
+  }
+}
+hipError_t launch_sort_adj_rows(const uint32_t *adj, uint32_t cap, uint32_t R, uint32_t *dst, hipStream_t s) {
+  if (cap == 0) return hipSuccess;
+  const uint32_t g = cap < 65536 ? cap : 65536;
+  hipLaunchKernelGGL(k_sort_adj_rows, dim3(g), dim3(64), 0, s, adj, cap, R, dst);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- medoid
-// The active id minimising (fp64 squared distance to the centroid, id).
-// Centroid: exact integer sums for uint8; for fp32, blocks of 1024
-// consecutive ids summed in id order, block sums added in block order;
-// divided by the active count.  Distance: fused multiply-add chain in
-// dimension order.  The smallest distance is found with a 64-bit atomic min
-// on its bit pattern (non-negative doubles order like their bits), then the
-// smallest id with exactly that distance.
+// The active id minimising (squared distance to the centroid, id).
+//  uint8: exact.  With n active ids and per-dimension sums S_j, the squared
+//    distance of x to S/n is |n x - S|^2 / n^2, so ids are compared by the
+//    integer key sum_j (n x_j - S_j)^2, held in 128 bits (each term is below
+//    2^78).  Three passes over the active ids find the smallest high word,
+//    then the smallest low word among those, then the smallest id with
+//    exactly that key.
+//  fp32: blocks of 1024 consecutive ids summed in id order, block sums added
+//    in block order, divided by the active count; the distance to it is a
+//    fused multiply-add chain in fp64 in dimension order.  The smallest
+//    distance is found with a 64-bit atomic min on its bit pattern
+//    (non-negative doubles order like their bits), then the smallest id with
+//    exactly that distance.
 constexpr uint32_t kCentroidBlock = 1024;
 
 size_t medoid_tmp_bytes(uint32_t cap, uint32_t dim) {
@@ -1163,7 +1188,7 @@ __global__ void k_centroid_part(PoolView P, int kind, uint32_t dim, double *part
     unsigned long long s = 0;
     for (uint32_t i = i0; i < i1; i++)
       if (P.active[i]) s += P.vecs[(size_t)i * P.stride + j];
-    part[(size_t)b * dim + j] = (double)s;  // < 2^53: exact
+    reinterpret_cast<unsigned long long *>(part)[(size_t)b * dim + j] = s;
   } else {
     double s = 0.0;
     for (uint32_t i = i0; i < i1; i++)
@@ -1171,49 +1196,68 @@ __global__ void k_centroid_part(PoolView P, int kind, uint32_t dim, double *part
     part[(size_t)b * dim + j] = s;
   }
 }
+// fp32: cent[j] = the centroid coordinate; uint8: cent[j] holds S_j as a
+// 64-bit integer.
 __global__ void k_centroid_sum(int kind, uint32_t dim, uint32_t nb, const double *part, double *cent,
                                unsigned long long n, DevScalars *ds) {
   if (!ds->need_medoid) return;
   const uint32_t j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j == 0) {
     ds->best_bits = ~0ull;
+    ds->best_hi = ~0ull;
     ds->best_id = kInvalid;
   }
   if (j >= dim) return;
   if (kind == kU8L2) {
+    const unsigned long long *pi = reinterpret_cast<const unsigned long long *>(part);
     unsigned long long s = 0;
-    for (uint32_t b = 0; b < nb; b++) s += (unsigned long long)part[(size_t)b * dim + j];
-    cent[j] = (double)s / (double)n;
+    for (uint32_t b = 0; b < nb; b++) s += pi[(size_t)b * dim + j];
+    reinterpret_cast<unsigned long long *>(cent)[j] = s;
   } else {
     double t = 0.0;
     for (uint32_t b = 0; b < nb; b++) t = t + part[(size_t)b * dim + j];
     cent[j] = t / (double)n;
   }
 }
-__device__ __forceinline__ double dist_to_centroid(const PoolView &P, int kind, uint32_t dim, uint32_t i,
-                                                   const double *cent) {
+__device__ __forceinline__ double dist_to_centroid(const PoolView &P, uint32_t dim, uint32_t i, const double *cent) {
   double s = 0.0;
-  const uint8_t *row = P.vecs + (size_t)i * P.stride;
+  const float *row = reinterpret_cast<const float *>(P.vecs + (size_t)i * P.stride);
   for (uint32_t j = 0; j < dim; j++) {
-    const double x = kind == kU8L2 ? (double)row[j] : (double)reinterpret_cast<const float *>(row)[j];
-    const double t = x - cent[j];
+    const double t = (double)row[j] - cent[j];
     s = __builtin_fma(t, t, s);
   }
   return s;
 }
-__global__ void k_medoid_min(PoolView P, int kind, uint32_t dim, const double *cent, DevScalars *ds) {
-  if (!ds->need_medoid) return;
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= P.cap || !P.active[i]) return;
-  const double s = dist_to_centroid(P, kind, dim, i, cent);
-  atomicMin(&ds->best_bits, (unsigned long long)__double_as_longlong(s));
+__device__ __forceinline__ unsigned __int128 u8_centroid_key(const PoolView &P, uint32_t dim, uint32_t i,
+                                                            const double *cent, unsigned long long n) {
+  const unsigned long long *S = reinterpret_cast<const unsigned long long *>(cent);
+  const uint8_t *row = P.vecs + (size_t)i * P.stride;
+  unsigned __int128 key = 0;
+  for (uint32_t j = 0; j < dim; j++) {
+    const __int128 t = (__int128)n * row[j] - (__int128)S[j];
+    key += (unsigned __int128)(t * t);
+  }
+  return key;
 }
-__global__ void k_medoid_arg(PoolView P, int kind, uint32_t dim, const double *cent, DevScalars *ds) {
+// pass 0: smallest high word (uint8) or smallest distance (fp32); pass 1
+// (uint8 only): smallest low word among keys with the smallest high word;
+// pass 2: smallest id with exactly the smallest key.
+__global__ void k_medoid_pass(PoolView P, int kind, uint32_t dim, const double *cent, unsigned long long n,
+                              int pass, DevScalars *ds) {
   if (!ds->need_medoid) return;
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= P.cap || !P.active[i]) return;
-  const double s = dist_to_centroid(P, kind, dim, i, cent);
-  if ((unsigned long long)__double_as_longlong(s) == ds->best_bits) atomicMin(&ds->best_id, i);
+  if (kind == kU8L2) {
+    const unsigned __int128 key = u8_centroid_key(P, dim, i, cent, n);
+    const unsigned long long hi = (unsigned long long)(key >> 64), lo = (unsigned long long)key;
+    if (pass == 0) atomicMin(&ds->best_hi, hi);
+    else if (pass == 1) { if (hi == ds->best_hi) atomicMin(&ds->best_bits, lo); }
+    else if (hi == ds->best_hi && lo == ds->best_bits) atomicMin(&ds->best_id, i);
+  } else {
+    const unsigned long long bits = (unsigned long long)__double_as_longlong(dist_to_centroid(P, dim, i, cent));
+    if (pass == 0) atomicMin(&ds->best_bits, bits);
+    else if (pass == 2 && bits == ds->best_bits) atomicMin(&ds->best_id, i);
+  }
 }
 __global__ void k_medoid_store(DevScalars *ds) {
   if (ds->need_medoid) ds->medoid = ds->best_id;
@@ -1244,8 +1288,11 @@ hipError_t launch_medoid(PoolView p, int kind, uint32_t dim, uint64_t n_active, 
                      (const DevScalars *)ds);
   hipLaunchKernelGGL(k_centroid_sum, dim3((dim + 63) / 64), dim3(64), 0, s, kind, dim, nb, part, cent,
                      (unsigned long long)n_active, ds);
-  hipLaunchKernelGGL(k_medoid_min, dim3(blocks_for(p.cap, 256)), dim3(256), 0, s, p, kind, dim, cent, ds);
-  hipLaunchKernelGGL(k_medoid_arg, dim3(blocks_for(p.cap, 256)), dim3(256), 0, s, p, kind, dim, cent, ds);
+  for (int pass = 0; pass < 3; pass++) {
+    if (pass == 1 && kind != kU8L2) continue;
+    hipLaunchKernelGGL(k_medoid_pass, dim3(blocks_for(p.cap, 256)), dim3(256), 0, s, p, kind, dim,
+                       (const double *)cent, (unsigned long long)n_active, pass, ds);
+  }
   hipLaunchKernelGGL(k_medoid_store, dim3(1), dim3(1), 0, s, ds);
   return hipGetLastError();
 }

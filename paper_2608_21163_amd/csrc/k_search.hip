@@ -15,6 +15,14 @@
 // Each hop expands the smallest unexpanded key u, reads u's list (one slot
 // per lane), drops ids found in the hash, gathers the remaining rows
 // LPV lanes per row, and merges the new keys into C keeping the l smallest.
+//
+// Counting variant (EXACT): the hash is replaced by an exact visited bitmap
+// per search in device memory, so every id is evaluated once and the
+// evaluation count is the number of distinct ids whose distance the search
+// needs ({start} and every neighbour of an expanded node).  The expansion
+// order, and so C and V, are the same as with the hash (the hash only skips
+// recomputation), which makes this variant a measurement of the method's
+// own work.  It is launched only when counting is enabled.
 #include "dispatch.h"
 
 namespace gr {
@@ -56,7 +64,7 @@ template <> struct IdHash<uint32_t> {
 bool hash16_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFFFu << kHashBits); }
 bool hash8_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFu << kHashBits8); }
 
-template <int KIND, int LPV, int CPL, int NR, class HW>
+template <int KIND, int LPV, int CPL, int NR, class HW, bool EXACT>
 __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   typedef IdHash<HW> H;
   constexpr int kSlots = 1 << H::kBits;
@@ -72,7 +80,9 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
   const uint8_t *qrow = a.qids ? P.vecs + (size_t)a.qids[qi] * P.stride : a.qbase + (size_t)qi * P.stride;
   Slice<KIND, LPV, CPL> s;
   load_slice<KIND, LPV, CPL>(s, qrow, P.nch);
-  for (int i = ln; i < kSlots; i += 64) hsh[i] = H::kEmpty;
+  uint32_t *vrow = EXACT ? a.vis + (size_t)qi * a.vis_words : nullptr;
+  if (!EXACT)
+    for (int i = ln; i < kSlots; i += 64) hsh[i] = H::kEmpty;
 
   float cd[NR];
   uint32_t ci[NR];
@@ -83,7 +93,10 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     if (ln == 0) { cd[0] = d0; ci[0] = a.start; }
   }
   __syncthreads();
-  if (ln == 0 && a.start < P.cap) hsh[H::slot(a.start)] = H::word(a.start);
+  if (ln == 0 && a.start < P.cap) {
+    if (EXACT) atomicOr(&vrow[a.start >> 5], 1u << (a.start & 31));
+    else hsh[H::slot(a.start)] = H::word(a.start);
+  }
   __syncthreads();
   uint32_t nv = 0, evals = 1;
 
@@ -113,11 +126,21 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
     nv++;
     // C <- C u N_out(u), skipping ids already evaluated
     const uint32_t v = ln < (int)P.R ? P.adj[(size_t)u * P.R + ln] : kInvalid;
-    const uint32_t hs = H::slot(v);
-    const HW hw = H::word(v);
-    bool need = v != kInvalid && hsh[hs] != hw;
-    __syncthreads();
-    if (need) hsh[hs] = hw;
+    bool need;
+    if (EXACT) {
+      need = false;
+      if (v != kInvalid) {
+        const uint32_t bit = 1u << (v & 31);
+        need = !(atomicOr(&vrow[v >> 5], bit) & bit);
+      }
+      __syncthreads();
+    } else {
+      const uint32_t hs = H::slot(v);
+      const HW hw = H::word(v);
+      need = v != kInvalid && hsh[hs] != hw;
+      __syncthreads();
+      if (need) hsh[hs] = hw;
+    }
     const uint64_t m = ballot(need);
     const int cnt = popc(m);
     if (cnt == 0) continue;
@@ -152,9 +175,18 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
       a.c_d[(size_t)qi * a.c_out + t] = finf();
     }
   }
+  // stopped by the expansion cap with unexpanded keys left in C
+  bool open = false;
+#pragma unroll
+  for (int r = 0; r < NR; r++) open |= ballot(kvalid(ci[r]) && !(ci[r] & kVisit)) != 0;
   if (ln == 0) {
-    stat_add(a.ds, kStHops + a.which, (unsigned long long)nv);
-    stat_add(a.ds, kStEvals + a.which, (unsigned long long)evals);
+    if (EXACT) {
+      stat_add(a.ds, kStDistinct + a.which, (unsigned long long)evals);
+    } else {
+      stat_add(a.ds, kStHops + a.which, (unsigned long long)nv);
+      stat_add(a.ds, kStEvals + a.which, (unsigned long long)evals);
+      if (open && nv >= a.max_iters) stat_add(a.ds, kStCapped + a.which, 1ull);
+    }
   }
 }
 
@@ -214,9 +246,10 @@ hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t st) 
   if (a.nq == 0) return hipSuccess;
   const bool h8 = hash8_ok(a.pool.cap), h16 = hash16_ok(a.pool.cap);
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.ell, {
-    if (h8) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t>), dim3(a.nq), dim3(64), 0, st, a);
-    else if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t>), dim3(a.nq), dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint32_t>), dim3(a.nq), dim3(64), 0, st, a);
+    if (a.vis) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t, true>), dim3(a.nq), dim3(64), 0, st, a);
+    else if (h8) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t, false>), dim3(a.nq), dim3(64), 0, st, a);
+    else if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t, false>), dim3(a.nq), dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint32_t, false>), dim3(a.nq), dim3(64), 0, st, a);
     return hipGetLastError();
   }));
   return hipErrorInvalidValue;

@@ -30,7 +30,7 @@ PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group
 
 EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
             "grand_delete_batch", "grand_search", "grand_export_graph", "grand_import_graph", "grand_set_timing",
-            "grand_get_stats", "grand_reset_stats", "grand_last_error"]
+            "grand_set_counting", "grand_stats", "grand_reset_stats", "grand_last_error"]
 
 
 class GrandError(RuntimeError):
@@ -58,6 +58,7 @@ class Stats(ctypes.Structure):
                 ("rebuild_records", ctypes.c_uint64), ("records", ctypes.c_uint64), ("rev_edges", ctypes.c_uint64),
                 ("repair_evals", ctypes.c_uint64), ("rebuild_rows", ctypes.c_uint64),
                 ("repair_rows", ctypes.c_uint64), ("repair_records", ctypes.c_uint64),
+                ("search_distinct", ctypes.c_uint64 * 3), ("search_capped", ctypes.c_uint64 * 3),
                 ("phase_ms", ctypes.c_double * len(PHASES)), ("phase_calls", ctypes.c_uint64 * len(PHASES))]
 
 
@@ -72,6 +73,14 @@ def load_library(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with paper_2608_21163_amd/build.py")
+    # One HIP runtime per process: torch ships its own libamdhip64 with the
+    # same soname as the system one libgrand.so links.  Loading torch first
+    # makes libgrand bind to torch's copy; loading libgrand first would pull
+    # in the system copy, and torch's later initialisation then finds no GPU.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     P, U32, I32, U64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64
     lib.grand_default_params.argtypes = [P]
@@ -84,7 +93,8 @@ def load_library(path: str = LIB_PATH):
     lib.grand_export_graph.argtypes = [P, P, P, P, P, P, P, P]
     lib.grand_import_graph.argtypes = [P, P, P, P, P, U32]
     lib.grand_set_timing.argtypes = [P, I32]
-    lib.grand_get_stats.argtypes = [P, P]
+    lib.grand_set_counting.argtypes = [P, I32]
+    lib.grand_stats.argtypes = [P, P, ctypes.c_size_t]
     lib.grand_reset_stats.argtypes = [P]
     lib.grand_last_error.argtypes = [P]
     lib.grand_last_error.restype = ctypes.c_char_p
@@ -232,7 +242,8 @@ class GrandIndex:
         return out
 
     def import_graph(self, vecs, adj, deg, active, medoid: int):
-        vecs = _np(vecs, self.np_dtype)
+        if not _is_torch(vecs):
+            vecs = _np(vecs, self.np_dtype)
         self._check(self.lib.grand_import_graph(self.h, _ptr(vecs), _ptr(_np(adj, np.uint32)),
                                                 _ptr(_np(deg, np.uint32)), _ptr(_np(active, np.uint8)),
                                                 int(medoid)))
@@ -240,18 +251,22 @@ class GrandIndex:
     def set_timing(self, on: bool = True):
         self._check(self.lib.grand_set_timing(self.h, 1 if on else 0))
 
+    def set_counting(self, on: bool = True):
+        self._check(self.lib.grand_set_counting(self.h, 1 if on else 0))
+
     def reset_stats(self):
         self._check(self.lib.grand_reset_stats(self.h))
 
     def stats(self) -> dict:
         s = Stats()
-        s.struct_size = ctypes.sizeof(Stats)
-        self._check(self.lib.grand_get_stats(self.h, ctypes.byref(s)))
-        out = {n: getattr(s, n) for n, _ in Stats._fields_ if n not in
-               ("search_hops", "search_evals", "phase_ms", "phase_calls")}
+        self._check(self.lib.grand_stats(self.h, ctypes.byref(s), ctypes.sizeof(Stats)))
+        arrays = ("search_hops", "search_evals", "search_distinct", "search_capped", "phase_ms", "phase_calls")
+        out = {n: getattr(s, n) for n, _ in Stats._fields_ if n not in arrays}
         for i, w in enumerate(("insert", "delete", "query")):
             out[f"hops_{w}"] = s.search_hops[i]
             out[f"evals_{w}"] = s.search_evals[i]
+            out[f"distinct_{w}"] = s.search_distinct[i]
+            out[f"capped_{w}"] = s.search_capped[i]
         out["phase_ms"] = {n: s.phase_ms[i] for i, n in enumerate(PHASES)}
         out["phase_calls"] = {n: s.phase_calls[i] for i, n in enumerate(PHASES)}
         return out

@@ -31,20 +31,117 @@ def to_gpu(o, g, w):
     return st
 
 
-def compare_states(gst, ost, algo, allow_frac=0.0):
-    """Returns the number of differing rows; asserts the integer state
-    (active map, medoid) is identical and the differing fraction small."""
+def _row_sets(st, algo):
+    adj = st["adj"]
+    return adj if algo == "cagra" else canonical_rows(adj)
+
+
+def differing_rows(gst, ost, algo):
+    a, b = _row_sets(gst, algo), _row_sets(ost, algo)
+    return np.flatnonzero(np.any(a != b, axis=1) | (gst["deg"] != ost["deg"]))
+
+
+def _near(x, y, tol=DIST_RTOL):
+    return abs(x - y) <= tol * max(abs(x), abs(y), 1e-30)
+
+
+def _search_has_tie(o_pre, vec, start, ell, iters):
+    """True when the oracle's search from `vec` on the pre-batch state meets
+    two keys whose distances agree within the tolerance (a tie that can
+    order the keys differently on the two sides)."""
+    C_ids, C_d, V_ids, V_d = o_pre.beam_search(vec, start, ell, iters)
+    d = np.sort(np.concatenate([C_d, V_d]).astype(np.float64))
+    d = np.unique(d)
+    if len(d) < 2:
+        return False
+    gap = np.abs(np.diff(d)) <= DIST_RTOL * np.maximum(np.abs(d[1:]), 1e-30)
+    return bool(gap.any())
+
+
+def explain_differences(gst, ost, rows, ctx):
+    """Traces every differing list to a distance tie within DIST_RTOL of the
+    oracle's own distances (the acceptance rule: each mismatch is explained
+    by a tie).  A list u is explained when
+      (1) two ids of either side's list have Dist(u, .) within the tolerance,
+      (2) an alpha-test of u's prune sits within the tolerance of its
+          boundary: coef * Dist(s, x) ~ Dist(u, x) for s, x in the lists,
+      (3) it differs by an id x whose own list differs and holds u on one
+          side only (the reverse edge x -> u exists on one side only), or
+      (4) u is a point of the batch whose search on the pre-batch state meets
+          a tie (its forward list, or the repair candidates C_u, follow).
+    Returns the rows left unexplained."""
+    algo, dist, coef = ctx["algo"], ctx["dist"], ctx["coef"]
+    rows_set = set(int(r) for r in rows)
+    G, O = _row_sets(gst, algo), _row_sets(ost, algo)
+
+    def ids(row):
+        return set(int(v) for v in row if v != INVALID)
+
+    batch_tie = {}
+    left = []
+    for u in rows_set:
+        g, o = ids(G[u]), ids(O[u])
+        X = g ^ o
+        every = g | o
+        D = {x: dist(u, x) for x in every}
+        ok = False
+        for x in X:                                              # (1)
+            if any(y != x and _near(D[x], D[y]) for y in every):
+                ok = True
+                break
+        if not ok and coef is not None:                          # (2)
+            ok = any(s != x and _near(coef * dist(s, x), D[x]) for x in X for s in every)
+        if not ok:                                               # (3)
+            for x in X:
+                if x in rows_set and u in (ids(G[x]) ^ ids(O[x])):
+                    ok = True
+                    break
+        if not ok and ctx.get("batch") is not None and u in ctx["batch"]:   # (4)
+            if u not in batch_tie:
+                if ctx["start"] == INVALID:
+                    # empty index: the candidates are the batch points by brute force
+                    d = np.unique(np.array([dist(u, x) for x in ctx["batch"] if x != u], np.float64))
+                    batch_tie[u] = bool(len(d) > 1 and (np.diff(d) <= DIST_RTOL * np.abs(d[1:])).any())
+                else:
+                    batch_tie[u] = _search_has_tie(ctx["pre"], ctx["vecs"][u], ctx["start"], ctx["ell"],
+                                                   ctx["iters"])
+            ok = batch_tie[u]
+        if not ok and algo == "cagra" and not X and g == o:
+            ok = True                                            # same set, slot order only: (4) of a neighbour
+        if not ok:
+            left.append(u)
+    return left
+
+
+def compare_states(gst, ost, algo, allow_frac=0.0, ctx=None):
+    """Returns the number of differing rows.  The integer state (active map,
+    medoid) must be identical; at most allow_frac of the active lists may
+    differ, and with a context (fp32 data) every differing list must be
+    traced to a distance tie within DIST_RTOL (explain_differences)."""
     assert np.array_equal(gst["active"], ost["active"]), "active maps differ"
     assert gst["medoid"] == ost["medoid"], (gst["medoid"], ost["medoid"])
-    if algo == "vamana":
-        a, b = canonical_rows(gst["adj"]), canonical_rows(ost["adj"])
-    else:
-        a, b = gst["adj"], ost["adj"]
-    rows = np.flatnonzero(np.any(a != b, axis=1) | (gst["deg"] != ost["deg"]))
+    rows = differing_rows(gst, ost, algo)
     n_act = max(int(ost["active"].sum()), 1)
     frac = len(rows) / n_act
     assert frac <= allow_frac, f"{len(rows)} of {n_act} lists differ (allowed {allow_frac:.4%}): {rows[:10]}"
+    if len(rows) and ctx is not None:
+        left = explain_differences(gst, ost, rows, ctx)
+        assert not left, f"lists without a distance tie: {left[:10]}"
     return len(rows)
+
+
+def tie_context(o_pre, w, algo, batch_ids, coef):
+    """Context for explain_differences: the oracle of the pre-batch state,
+    the pool vectors, the batch ids and the search parameters."""
+    vecs = w.vectors
+
+    def dist(a, b):
+        return o_pre.dist(vecs[a], vecs[b])
+
+    cfg = w.cfg
+    return dict(algo=algo, dist=dist, coef=coef, pre=o_pre, vecs=vecs,
+                batch=set(int(x) for x in batch_ids), start=o_pre.export()["medoid"],
+                ell=cfg.L_build, iters=cfg.iters)
 
 
 def compare_search(gi, gd, oi, od, allow_frac=0.0):
