@@ -129,6 +129,25 @@ grand_status grand_delete_batch(grand_index *h, const uint32_t *ids, uint32_t n)
 grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
                           uint32_t *out_ids, float *out_dists);
 
+/* Bytes of the fixed device array that grand_search_static works in. */
+#define GRAND_STATIC_SCRATCH_BYTES (8u << 20)
+
+/* grand_search for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, semantics and errors as grand_search, and the same
+ * kernels; the staged query rows and the result lists live in a fixed
+ * device array of GRAND_STATIC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends, so the call allocates
+ * nothing (no phase timing and no counting run apply to it).
+ * Limit: align256(nq * row) + 2 * align256(nq * k * 4) <= that size, where
+ * row is the vector length in bytes rounded up to 16 (for 128-byte rows
+ * and k = 10 about 40,000 queries); larger calls return GRAND_E_CAPACITY
+ * with nothing done.  Every call on one GPU shares that GPU's array: calls
+ * that overlap in time on one GPU (from several threads, or several indexes
+ * on different streams) race on it and must be serialised by the caller. */
+grand_status grand_search_static(grand_index *h, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                                 uint32_t *out_ids, float *out_dists);
+
 /* Copies the index state out.  Any output pointer may be NULL.
  *   adj: capacity x R lists, GRAND_INVALID padding.  Vamana lists are sets
  *        (their order carries no meaning) and are returned canonically:

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <tuple>
 #include <vector>
@@ -15,10 +16,45 @@
 
 using namespace gr;
 
+// Device memory of grand_search_static: the staged query rows and the result
+// lists of one call, in a fixed array that every GPU the library runs on
+// holds from module load until the process ends.  In host code `scratch` is
+// only a symbol; its device address on each GPU comes from
+// hipGetSymbolAddress (scratch_of below) and is the only form passed on.
+constexpr size_t kStaticScratchBytes = GRAND_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch[kMaxDevices] = {};
+
+// Address of this device's `scratch`, looked up once per device with the
+// device current.  Returns null (and the HIP error) when the lookup fails.
+uint8_t *scratch_of(int dev, hipError_t *err) {
+  *err = hipSuccess;
+  if (dev < 0 || dev >= kMaxDevices) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      *err = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    g_scratch[dev] = static_cast<uint8_t *>(ptr);
+  }
+  return g_scratch[dev];
+}
+}  // namespace
 
 struct grand_index {
   grand_params p{};
   hipStream_t stream = nullptr;
+  uint8_t *static_scratch = nullptr;  // this device's address of `scratch`
   int kind = 0, vc = 0;
   size_t esize = 0, row_bytes = 0, stride = 0;
   int nch = 0;
@@ -655,6 +691,16 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
     return GRAND_E_DEVICE;
   }
   h->stream = (hipStream_t)p->stream;
+  {
+    hipError_t e = hipSuccess;
+    h->static_scratch = scratch_of(p->device, &e);
+    if (!h->static_scratch) {
+      (void)hipGetLastError();
+      fprintf(stderr, "grand_create: no address for the static search scratch: %s\n", hipGetErrorString(e));
+      delete h;
+      return GRAND_E_DEVICE;
+    }
+  }
   h->kind = p->dtype == GRAND_U8 ? kU8L2 : (p->metric == GRAND_IP ? kF32IP : kF32L2);
   h->esize = p->dtype == GRAND_U8 ? 1 : 4;
   h->row_bytes = (size_t)p->dim * h->esize;
@@ -870,6 +916,58 @@ grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint
   }
   HCHK(h, hipMemcpyAsync(out_ids, h->q_ids, (size_t)nq * k * 4, hipMemcpyDefault, h->stream));
   HCHK(h, hipMemcpyAsync(out_dists, h->q_d, (size_t)nq * k * 4, hipMemcpyDefault, h->stream));
+  h->st.queried += nq;
+  return finish(h);
+}
+
+grand_status grand_search_static(grand_index *h, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                                 uint32_t *out_ids, float *out_dists) {
+  grand_status s = check_usable(h);
+  if (s != GRAND_OK) return s;
+  if (k == 0 || beam == 0 || k > beam || beam > 256) return fail(h, GRAND_E_ARG, "need 1 <= k <= beam <= 256");
+  if (nq == 0) return GRAND_OK;
+  if (!queries || !out_ids || !out_dists) return fail(h, GRAND_E_ARG, "null argument");
+  // layout in `scratch`: query rows (nq x stride), ids (nq x k), distances
+  // (nq x k), each region 256-byte aligned
+  const size_t qb = ((size_t)nq * h->stride + 255) / 256 * 256;
+  const size_t rb = ((size_t)nq * k * 4 + 255) / 256 * 256;
+  if (qb + 2 * rb > kStaticScratchBytes)
+    return fail(h, GRAND_E_CAPACITY, "queries and results exceed the static search scratch");
+  HCHK(h, hipSetDevice(h->p.device));
+  uint8_t *q_vecs = h->static_scratch;
+  uint32_t *q_ids = reinterpret_cast<uint32_t *>(h->static_scratch + qb);
+  float *q_d = reinterpret_cast<float *>(h->static_scratch + qb + rb);
+  // the array keeps the previous call's contents: zero the rows' padding
+  if (h->stride != h->row_bytes) HCHK(h, launch_fill_u32(reinterpret_cast<uint32_t *>(q_vecs), 0u, qb / 4, h->stream));
+  if ((s = stage_rows(h, q_vecs, queries, nq)) != GRAND_OK) return s;
+  if (h->p.dtype == GRAND_F32) {
+    if ((s = clear_errors(h)) != GRAND_OK) return s;
+    HCHK(h, launch_check_finite(q_vecs, nq, h->stride, h->p.dim, h->ds, h->stream));
+    if ((s = read_validation(h)) != GRAND_OK) {
+      (void)finish(h);
+      return s;
+    }
+  }
+  if (h->n_active == 0) {
+    HCHK(h, launch_fill_u32(q_ids, GRAND_INVALID, (size_t)nq * k, h->stream));
+    HCHK(h, launch_fill_u32(reinterpret_cast<uint32_t *>(q_d), 0x7F800000u, (size_t)nq * k, h->stream));
+  } else {
+    SearchArgs a{};
+    a.pool = h->pool;
+    a.qbase = q_vecs;
+    a.nq = nq;
+    a.start = h->medoid;
+    a.ell = beam;
+    a.max_iters = 2 * beam;
+    a.which = 2;
+    a.c_ids = q_ids;
+    a.c_d = q_d;
+    a.c_out = k;
+    a.ds = h->ds;
+    HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
+  }
+  HCHK(h, hipMemcpyAsync(out_ids, q_ids, (size_t)nq * k * 4, hipMemcpyDefault, h->stream));
+  HCHK(h, hipMemcpyAsync(out_dists, q_d, (size_t)nq * k * 4, hipMemcpyDefault, h->stream));
   h->st.queried += nq;
   return finish(h);
 }

@@ -24,12 +24,13 @@ L2, IP = 0, 1
 ALPHA_ON_DIST, ALPHA_ON_L2 = 0, 1
 CAS_GROUPED, CAS_RACING = 0, 1
 REV_FULL, REV_BATCH = 0, 1
+STATIC_SCRATCH_BYTES = 8 << 20   # GRAND_STATIC_SCRATCH_BYTES
 
 PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group", "rebuild", "search_delete",
           "reverse", "repair", "clear", "medoid", "search_query", "cagra_detour", "cagra_pickone"]
 
 EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
-            "grand_delete_batch", "grand_search", "grand_export_graph", "grand_import_graph", "grand_set_timing",
+            "grand_delete_batch", "grand_search", "grand_search_static", "grand_export_graph", "grand_import_graph", "grand_set_timing",
             "grand_set_counting", "grand_stats", "grand_reset_stats", "grand_last_error"]
 
 
@@ -90,6 +91,7 @@ def load_library(path: str = LIB_PATH):
     lib.grand_insert_batch.argtypes = [P, P, P, U32]
     lib.grand_delete_batch.argtypes = [P, P, U32]
     lib.grand_search.argtypes = [P, P, U32, U32, U32, P, P]
+    lib.grand_search_static.argtypes = [P, P, U32, U32, U32, P, P]
     lib.grand_export_graph.argtypes = [P, P, P, P, P, P, P, P]
     lib.grand_import_graph.argtypes = [P, P, P, P, P, U32]
     lib.grand_set_timing.argtypes = [P, I32]
@@ -209,6 +211,21 @@ class GrandIndex:
             out_ids = np.zeros((nq, k), np.uint32)
             out_dists = np.zeros((nq, k), np.float32)
         self._check(self.lib.grand_search(self.h, _ptr(queries), nq, k, beam, _ptr(out_ids), _ptr(out_dists)))
+        return out_ids, out_dists
+
+    def search_static(self, queries, k: int, beam: int, out_ids=None, out_dists=None, check: bool = True):
+        """grand_search_static: the search without any device allocation.
+        Returns (ids, dists), or the status code when check is False."""
+        if not _is_torch(queries):
+            queries = _np(queries, self.np_dtype)
+        nq = int(queries.shape[0])
+        if out_ids is None:
+            out_ids = np.zeros((nq, k), np.uint32)
+            out_dists = np.zeros((nq, k), np.float32)
+        rc = self.lib.grand_search_static(self.h, _ptr(queries), nq, k, beam, _ptr(out_ids), _ptr(out_dists))
+        if not check:
+            return rc
+        self._check(rc)
         return out_ids, out_dists
 
     def search_rc(self, queries, k: int, beam: int) -> int:
