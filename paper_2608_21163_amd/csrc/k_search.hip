@@ -41,6 +41,7 @@ constexpr int kHashBits8 = 12;  // 8-bit tags: twice the slots in the same bytes
 template <class HW> struct IdHash;
 template <> struct IdHash<uint8_t> {
   static constexpr int kBits = kHashBits8;
+  static constexpr int kSlots = 1 << kBits;
   static __device__ __forceinline__ uint32_t slot(uint32_t v) {
     return (v ^ ((v >> kBits) * 40503u)) & ((1u << kBits) - 1u);
   }
@@ -49,6 +50,7 @@ template <> struct IdHash<uint8_t> {
 };
 template <> struct IdHash<uint16_t> {
   static constexpr int kBits = kHashBits;
+  static constexpr int kSlots = 1 << kBits;
   static __device__ __forceinline__ uint32_t slot(uint32_t v) {
     return (v ^ ((v >> kHashBits) * 40503u)) & (kHashSize - 1);
   }
@@ -57,6 +59,7 @@ template <> struct IdHash<uint16_t> {
 };
 template <> struct IdHash<uint32_t> {
   static constexpr int kBits = kHashBits;
+  static constexpr int kSlots = 1 << kBits;
   static __device__ __forceinline__ uint32_t slot(uint32_t v) { return (v * 0x9E3779B1u) >> (32 - kHashBits); }
   static __device__ __forceinline__ uint32_t word(uint32_t v) { return v; }
   static constexpr uint32_t kEmpty = kInvalid;
@@ -64,11 +67,32 @@ template <> struct IdHash<uint32_t> {
 bool hash16_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFFFu << kHashBits); }
 bool hash8_ok(uint32_t cap) { return (uint64_t)cap <= ((uint64_t)0xFFu << kHashBits8); }
 
+// 8-bit tags in S slots, S not necessarily a power of two: with t = v / S
+// and r = v % S, v goes to slot (r + t * odd) % S and stores t.  Slot and tag
+// determine v; tag 0xFF marks an empty slot, so ids must be below 255 * S.
+// The searches of l <= 128 are held to five or six waves per SIMD by their
+// registers, which leaves LDS for more slots than 4096 at no occupancy
+// cost: 6144 slots for l in (64, 128] (7.5 KB a wave, 21 waves per CU) and
+// 5120 for l <= 64 (6 KB, 26 waves per CU).  At 1M x 128 the 6144 slots cut
+// the rows an insert search evaluates again from 24% to 18%.
+template <int S> struct Slots8 {};
+template <int S> struct IdHash<Slots8<S>> {
+  static constexpr int kSlots = S;
+  static __device__ __forceinline__ uint32_t slot(uint32_t v) {
+    const uint32_t t = v / (uint32_t)S, r = v - t * (uint32_t)S;
+    return (r + t * 2654435u) % (uint32_t)S;
+  }
+  static __device__ __forceinline__ uint8_t word(uint32_t v) { return (uint8_t)(v / (uint32_t)S); }
+  static constexpr uint8_t kEmpty = 0xFFu;
+};
+template <int S> bool slots8_ok(uint32_t cap) { return (uint64_t)cap <= 255ull * S; }
+
 template <int KIND, int LPV, int CPL, int NR, class HW, bool EXACT>
-__global__ __launch_bounds__(64) void k_search(SearchArgs a) {
+__device__ __forceinline__ void search_one(SearchArgs a) {
   typedef IdHash<HW> H;
-  constexpr int kSlots = 1 << H::kBits;
-  __shared__ HW hsh[kSlots];
+  typedef decltype(H::word(0u)) Word;
+  constexpr int kSlots = H::kSlots;
+  __shared__ Word hsh[kSlots];
   __shared__ uint32_t nid[64];
   __shared__ float nkey[64];
   __shared__ uint32_t mid[64 * NR];
@@ -136,7 +160,7 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
       __syncthreads();
     } else {
       const uint32_t hs = H::slot(v);
-      const HW hw = H::word(v);
+      const Word hw = H::word(v);
       need = v != kInvalid && hsh[hs] != hw;
       __syncthreads();
       if (need) hsh[hs] = hw;
@@ -188,6 +212,11 @@ __global__ __launch_bounds__(64) void k_search(SearchArgs a) {
       if (open && nv >= a.max_iters) stat_add(a.ds, kStCapped + a.which, 1ull);
     }
   }
+}
+
+template <int KIND, int LPV, int CPL, int NR, class HW, bool EXACT>
+__global__ __launch_bounds__(64) void k_search(SearchArgs a) {
+  search_one<KIND, LPV, CPL, NR, HW, EXACT>(a);
 }
 
 // Empty index at the start of a batch: the candidates of each new point are
@@ -247,6 +276,10 @@ hipError_t launch_search(int kind, int vc, const SearchArgs &a, hipStream_t st) 
   const bool h8 = hash8_ok(a.pool.cap), h16 = hash16_ok(a.pool.cap);
   GR_DISPATCH_KV(kind, vc, GR_DISPATCH_N(a.ell, {
     if (a.vis) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t, true>), dim3(a.nq), dim3(64), 0, st, a);
+    else if (NR == 2 && slots8_ok<6144>(a.pool.cap))
+      hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, Slots8<6144>, false>), dim3(a.nq), dim3(64), 0, st, a);
+    else if (NR == 1 && slots8_ok<5120>(a.pool.cap))
+      hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, Slots8<5120>, false>), dim3(a.nq), dim3(64), 0, st, a);
     else if (h8) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint8_t, false>), dim3(a.nq), dim3(64), 0, st, a);
     else if (h16) hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint16_t, false>), dim3(a.nq), dim3(64), 0, st, a);
     else hipLaunchKernelGGL((k_search<KIND, LPV, CPL, NR, uint32_t, false>), dim3(a.nq), dim3(64), 0, st, a);
