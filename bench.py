@@ -81,7 +81,7 @@ def parse():
                     help="after the base build, delete and re-insert every base batch this many times (untimed)")
     ap.add_argument("--prune-rule", choices=["alpha_on_sq", "alpha_on_l2"], default=None,
                     help="override the alpha test of GrANDRobustPrune")
-    ap.add_argument("--rev-mode", choices=["full", "batch"], default="full")
+    ap.add_argument("--rev-mode", choices=["full", "batch"], default="batch")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-recall", action="store_true")

@@ -58,9 +58,11 @@ enum { GRAND_ALPHA_ON_DIST = 0, GRAND_ALPHA_ON_L2 = 1 };
  * independent racing compare-and-swap updates as in the paper's lock-free
  * last-writer-wins form. */
 enum { GRAND_CAS_GROUPED = 0, GRAND_CAS_RACING = 1 };
-/* In-neighbour discovery for deletes (Alg. 8): the full reverse graph of
- * every node in CSR form (default), or the reverse lists of the deleted
- * nodes only, built by the same histogram / prefix-scan / scatter pass. */
+/* In-neighbour discovery for deletes (Alg. 8): the reverse lists of the
+ * deleted nodes only (default): one pass over every list that keeps the
+ * edges into the batch, then a histogram, prefix scan and scatter into CSR
+ * rows indexed by batch position; or the full reverse graph of every node in
+ * CSR form (the transpose that grand_export_graph also returns). */
 enum { GRAND_REV_FULL = 0, GRAND_REV_BATCH = 1 };
 
 typedef struct {
@@ -86,7 +88,8 @@ typedef struct {
 } grand_params;
 
 /* Fills p with the defaults (Vamana, f32, L2, R 64, L_build 128, P 64,
- * c 2, k_repair 50, alpha 1.2 -- the parameters of Section 5.4). */
+ * c 2, k_repair 50, alpha 1.2 -- the parameters of Section 5.4; reverse
+ * lists of the delete batch only). */
 void grand_default_params(grand_params *p);
 
 /* Creates an index and allocates its whole resource pool on the device

@@ -367,8 +367,8 @@ grand_status prep_counting(grand_index *h, SearchArgs &a) {
 grand_status run_reverse(grand_index *h, int by_batch, uint32_t n, hipStream_t st = nullptr) {
   Phase ph(h, GRAND_PH_REVERSE, st);
   const uint32_t nrows = by_batch ? n : h->p.capacity;
-  HCHK(h, launch_reverse(h->pool, by_batch, h->in_batch, h->bidx, nrows, h->cnt, h->rev_off, h->scan_tmp, h->rev_src,
-                         h->rev, h->ds, st ? st : h->stream));
+  HCHK(h, launch_reverse(h->pool, by_batch, h->in_batch, h->bidx, by_batch ? h->b_ids : nullptr, nrows, h->cnt,
+                         h->rev_off, h->scan_tmp, h->rev_src, h->rev, h->ds, st ? st : h->stream));
   return GRAND_OK;
 }
 
@@ -669,7 +669,7 @@ void grand_default_params(grand_params *p) {
   p->alpha = 1.2f;
   p->prune_rule = GRAND_ALPHA_ON_DIST;
   p->cas_mode = GRAND_CAS_GROUPED;
-  p->rev_mode = GRAND_REV_FULL;
+  p->rev_mode = GRAND_REV_BATCH;
   p->max_batch = 10000;
   p->device = 0;
   p->stream = nullptr;

@@ -276,9 +276,11 @@ struct RevBufs {
   uint32_t *bh2;    // per (coarse bucket, sub-bucket, chunk) counts, rev_fine_words
   uint32_t *bo2;    // their exclusive scan
 };
-hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx, uint32_t nrows,
-                          uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp, uint32_t *src, const RevBufs &rb,
-                          DevScalars *ds, hipStream_t s);
+// by_batch: rows of the nrows batch positions (ids: the batch's ids; a batch
+// id's position is bidx[id] and in_batch[id] is set), else rows of every id
+hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx,
+                          const uint32_t *ids, uint32_t nrows, uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp,
+                          uint32_t *src, const RevBufs &rb, DevScalars *ds, hipStream_t s);
 hipError_t launch_sort_adj_rows(const uint32_t *adj, uint32_t cap, uint32_t R, uint32_t *dst, hipStream_t s);
 hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst,
                             hipStream_t s);

@@ -126,7 +126,7 @@ def _np(x, dtype):
     return np.ascontiguousarray(x, dtype=dtype)
 
 
-def params_from_config(cfg, device: int = 0, max_batch: int = 10000, rev_mode: int = REV_FULL) -> Params:
+def params_from_config(cfg, device: int = 0, max_batch: int = 10000, rev_mode: int = REV_BATCH) -> Params:
     """grand_params from a workloads.IndexConfig."""
     p = Params()
     load_library().grand_default_params(ctypes.byref(p))
