@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-recall", action="store_true")
+    ap.add_argument("--reverse-microbench", action="store_true",
+                    help="after the base build, time in-neighbour detection for one delete batch by a per-id "
+                         "linear scan, the batch-rows reverse build and the full reverse graph, and print that")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
     return ap.parse_args()
@@ -274,6 +277,51 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
     return out
 
 
+# ------------------------------------------------------------------ reverse-graph microbenchmark
+def reverse_microbench(g, w, spec, reps=5):
+    """In-neighbour detection for the first round's delete batch (Section 4.2
+    compares building the reverse graph with a linear scan of the graph for
+    each deleted point).  The reverse builds run on the whole batch; the
+    per-id scan costs n passes over the adjacency, so it is timed on subsets
+    and its time per id is scaled to the batch.  All methods must agree."""
+    import numpy as np
+    from paper_2608_21163_amd.grand import INDEG_REV_BATCH, INDEG_REV_FULL, INDEG_SCAN
+    ops = {op.kind: op for op in w.round_ops(0)}
+    dele = ops["delete"].ids
+    # the delete batch of round 0 follows its insert batch; the ids it deletes
+    # are all active in the built index except those inserted in round 0
+    ids = dele[np.isin(dele, ops["insert"].ids, invert=True)] if "insert" in ops else dele
+    res = {"batch": int(len(ids))}
+    ref = None
+    for name, m in (("reverse_batch_rows", INDEG_REV_BATCH), ("reverse_full", INDEG_REV_FULL)):
+        times = []
+        for _ in range(reps):
+            cnt, ms = g.count_in_edges(ids, m)
+            times.append(ms)
+        if ref is None:
+            ref = cnt
+        assert np.array_equal(cnt, ref), name
+        res[name + "_ms"] = round(float(np.median(times)), 4)
+        log(f"reverse microbench: {name} {res[name + '_ms']} ms")
+    per_id = []
+    for n in (16, 64, 256):
+        times = []
+        for _ in range(3):
+            cnt, ms = g.count_in_edges(ids[:n], INDEG_SCAN)
+            times.append(ms)
+        assert np.array_equal(cnt, ref[:n]), n
+        t = float(np.median(times))
+        per_id.append(t / n)
+        res[f"scan_{n}_ids_ms"] = round(t, 4)
+        log(f"reverse microbench: scan of {n} ids {t:.3f} ms")
+    res["scan_ms_per_id"] = round(per_id[-1], 5)
+    res["scan_batch_ms_scaled"] = round(per_id[-1] * len(ids), 2)
+    res["speedup_batch_rows_vs_scan"] = round(res["scan_batch_ms_scaled"] / res["reverse_batch_rows_ms"], 1)
+    res["speedup_full_vs_scan"] = round(res["scan_batch_ms_scaled"] / res["reverse_full_ms"], 1)
+    res["in_edges_found"] = int(ref.sum())
+    print(json.dumps({"reverse_microbench": res, "config": w.wdef.description}), flush=True)
+
+
 # ------------------------------------------------------------------ main
 def main():
     args = parse()
@@ -344,6 +392,10 @@ def main():
     torch.cuda.synchronize()
     build_s = time.perf_counter() - t0
     log(f"build done: {spec.base_n:,} points in {build_s:.1f} s")
+
+    if args.reverse_microbench:
+        reverse_microbench(g, w, spec)
+        return
 
     # ---- stage every round's inputs on the device, with exact ground truth;
     # the pool as the timed rounds find it is kept for the counting rerun and

@@ -151,6 +151,24 @@ grand_status grand_search(grand_index *h, const void *queries, uint32_t nq, uint
 grand_status grand_search_static(grand_index *h, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
                                  uint32_t *out_ids, float *out_dists);
 
+/* In-neighbour detection, the step a delete batch needs before it can
+ * repair (Alg. 8 builds a reverse graph for it; Section 4.2 reports that
+ * building it is an order of magnitude faster than a linear scan of the
+ * graph for each deleted point).  Counts, for each of n distinct active ids,
+ * the lists of active nodes that hold it, by one of three methods so that
+ * their costs can be compared:
+ *   GRAND_INDEG_SCAN      a scan of every list for each id (n passes over
+ *                         the adjacency; n <= 65535);
+ *   GRAND_INDEG_REV_BATCH the reverse lists of the ids only, as a delete
+ *                         batch builds them (one pass);
+ *   GRAND_INDEG_REV_FULL  the full reverse graph of every node.
+ * out_counts: n counts (host or device).  ms (may be NULL): GPU time of the
+ * method, from events on the index's stream.  The index is not changed.
+ * Errors: GRAND_E_ID (ids out of range, repeated or inactive), GRAND_E_ARG. */
+enum { GRAND_INDEG_SCAN = 0, GRAND_INDEG_REV_BATCH = 1, GRAND_INDEG_REV_FULL = 2 };
+grand_status grand_count_in_edges(grand_index *h, const uint32_t *ids, uint32_t n, int method, uint32_t *out_counts,
+                                  float *ms);
+
 /* Copies the index state out.  Any output pointer may be NULL.
  *   adj: capacity x R lists, GRAND_INVALID padding.  Vamana lists are sets
  *        (their order carries no meaning) and are returned canonically:

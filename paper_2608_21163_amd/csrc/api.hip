@@ -972,6 +972,49 @@ grand_status grand_search_static(grand_index *h, const void *queries, uint32_t n
   return finish(h);
 }
 
+grand_status grand_count_in_edges(grand_index *h, const uint32_t *ids, uint32_t n, int method, uint32_t *out_counts,
+                                  float *ms) {
+  grand_status s = check_usable(h);
+  if (s != GRAND_OK) return s;
+  if (ms) *ms = 0.0f;
+  if (n == 0) return GRAND_OK;
+  if (!ids || !out_counts) return fail(h, GRAND_E_ARG, "null argument");
+  if (method != GRAND_INDEG_SCAN && method != GRAND_INDEG_REV_BATCH && method != GRAND_INDEG_REV_FULL)
+    return fail(h, GRAND_E_ARG, "unknown method");
+  if (method == GRAND_INDEG_SCAN && n > 65535) return fail(h, GRAND_E_ARG, "the scan method takes at most 65535 ids");
+  HCHK(h, hipSetDevice(h->p.device));
+  if ((s = ensure_batch(h, n)) != GRAND_OK) return s;
+  HCHK(h, hipMemcpyAsync(h->b_ids, ids, (size_t)n * 4, hipMemcpyDefault, h->stream));
+  if ((s = clear_errors(h)) != GRAND_OK) return s;
+  h->epoch++;
+  HCHK(h, launch_validate_ids(h->b_ids, n, h->p.capacity, h->pool.active, h->mark, h->epoch, 1, h->ds, h->stream));
+  if ((s = read_validation(h)) != GRAND_OK) {
+    (void)finish(h);
+    return s;
+  }
+  HCHK(h, launch_mark_batch(h->b_ids, n, h->in_batch, h->bidx, 1, h->stream));
+  hipEvent_t e0 = get_event(h), e1 = get_event(h);
+  if (!e0 || !e1) return fail(h, GRAND_E_DEVICE, "event creation failed");
+  HCHK(h, hipEventRecord(e0, h->stream));
+  if (method == GRAND_INDEG_SCAN) {
+    HCHK(h, launch_scan_in_edges(h->pool, h->b_ids, n, h->rcount, h->stream));
+  } else {
+    const int by_batch = method == GRAND_INDEG_REV_BATCH;
+    if ((s = run_reverse(h, by_batch, by_batch ? n : h->p.capacity)) != GRAND_OK) return s;
+    HCHK(h, launch_row_lengths(h->rev_off, by_batch ? nullptr : h->b_ids, n, h->rcount, h->stream));
+  }
+  HCHK(h, hipEventRecord(e1, h->stream));
+  HCHK(h, launch_mark_batch(h->b_ids, n, h->in_batch, nullptr, 0, h->stream));
+  HCHK(h, hipMemcpyAsync(out_counts, h->rcount, (size_t)n * 4, hipMemcpyDefault, h->stream));
+  if ((s = finish(h)) != GRAND_OK) return s;
+  float t = 0.0f;
+  HCHK(h, hipEventElapsedTime(&t, e0, e1));
+  h->spare_events.push_back(e0);
+  h->spare_events.push_back(e1);
+  if (ms) *ms = t;
+  return GRAND_OK;
+}
+
 grand_status grand_export_graph(grand_index *h, uint32_t *adj, uint32_t *deg, uint8_t *active, uint32_t *medoid,
                                 uint32_t *rev_offsets, uint32_t *rev_srcs, uint64_t *nnz) {
   grand_status s = check_usable(h);

@@ -281,6 +281,8 @@ struct RevBufs {
 hipError_t launch_reverse(PoolView p, int by_batch, const uint8_t *in_batch, const uint32_t *bidx,
                           const uint32_t *ids, uint32_t nrows, uint32_t *cnt, uint32_t *off, uint32_t *scan_tmp,
                           uint32_t *src, const RevBufs &rb, DevScalars *ds, hipStream_t s);
+hipError_t launch_scan_in_edges(PoolView p, const uint32_t *ids, uint32_t n, uint32_t *counts, hipStream_t s);
+hipError_t launch_row_lengths(const uint32_t *off, const uint32_t *ids, uint32_t n, uint32_t *counts, hipStream_t s);
 hipError_t launch_sort_adj_rows(const uint32_t *adj, uint32_t cap, uint32_t R, uint32_t *dst, hipStream_t s);
 hipError_t launch_sort_rows(const uint32_t *off, uint32_t nrows, const uint32_t *src, uint32_t *dst,
                             hipStream_t s);

@@ -615,6 +615,42 @@ __global__ void k_rev_scatter(PoolView P, int by_batch, const uint8_t *in_batch,
     src[pos] = u;
   }
 }
+// The naive in-neighbour detection a reverse graph replaces: for each id,
+// a scan of every list for it.  Workgroup (x, i) scans the x-th of
+// gridDim.x slices of the adjacency for ids[i] and adds the occurrences in
+// active rows to counts[i] (counts zeroed by the caller).
+__global__ __launch_bounds__(256) void k_scan_in_edges(PoolView P, const uint32_t *ids, uint32_t *counts) {
+  const uint32_t p = ids[blockIdx.y];
+  const size_t total = (size_t)P.cap * P.R;
+  const size_t per = (total + gridDim.x - 1) / gridDim.x;
+  const size_t e0 = (size_t)blockIdx.x * per, e1 = e0 + per < total ? e0 + per : total;
+  uint32_t c = 0;
+  for (size_t e = e0 + threadIdx.x; e < e1; e += blockDim.x)
+    if (P.adj[e] == p && P.active[e / P.R]) c++;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+  if ((threadIdx.x & 63) == 0 && c) atomicAdd(&counts[blockIdx.y], c);
+}
+hipError_t launch_scan_in_edges(PoolView p, const uint32_t *ids, uint32_t n, uint32_t *counts, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipError_t e = launch_fill_u32(counts, 0u, n, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_scan_in_edges, dim3(256, n), dim3(256), 0, s, p, ids, counts);
+  return hipGetLastError();
+}
+// counts[i] = off[row(i) + 1] - off[row(i)], row(i) = i (batch rows) or ids[i]
+__global__ void k_row_lengths(const uint32_t *off, const uint32_t *ids, uint32_t n, uint32_t *counts) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t r = ids ? ids[i] : i;
+  counts[i] = off[r + 1] - off[r];
+}
+hipError_t launch_row_lengths(const uint32_t *off, const uint32_t *ids, uint32_t n, uint32_t *counts, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_row_lengths, dim3(blocks_for(n, 256)), dim3(256), 0, s, off, ids, n, counts);
+  return hipGetLastError();
+}
+
 __global__ void k_count_edges(const uint32_t *off, uint32_t nrows, DevScalars *ds) {
   if (threadIdx.x == 0) stat_add(ds, kStRevEdges, (unsigned long long)off[nrows]);
 }

@@ -24,13 +24,14 @@ L2, IP = 0, 1
 ALPHA_ON_DIST, ALPHA_ON_L2 = 0, 1
 CAS_GROUPED, CAS_RACING = 0, 1
 REV_FULL, REV_BATCH = 0, 1
+INDEG_SCAN, INDEG_REV_BATCH, INDEG_REV_FULL = 0, 1, 2
 STATIC_SCRATCH_BYTES = 8 << 20   # GRAND_STATIC_SCRATCH_BYTES
 
 PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group", "rebuild", "search_delete",
           "reverse", "repair", "clear", "medoid", "search_query", "cagra_detour", "cagra_pickone"]
 
 EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
-            "grand_delete_batch", "grand_search", "grand_search_static", "grand_export_graph", "grand_import_graph", "grand_set_timing",
+            "grand_delete_batch", "grand_search", "grand_search_static", "grand_count_in_edges", "grand_export_graph", "grand_import_graph", "grand_set_timing",
             "grand_set_counting", "grand_stats", "grand_reset_stats", "grand_last_error"]
 
 
@@ -92,6 +93,7 @@ def load_library(path: str = LIB_PATH):
     lib.grand_delete_batch.argtypes = [P, P, U32]
     lib.grand_search.argtypes = [P, P, U32, U32, U32, P, P]
     lib.grand_search_static.argtypes = [P, P, U32, U32, U32, P, P]
+    lib.grand_count_in_edges.argtypes = [P, P, U32, I32, P, P]
     lib.grand_export_graph.argtypes = [P, P, P, P, P, P, P, P]
     lib.grand_import_graph.argtypes = [P, P, P, P, P, U32]
     lib.grand_set_timing.argtypes = [P, I32]
@@ -227,6 +229,15 @@ class GrandIndex:
             return rc
         self._check(rc)
         return out_ids, out_dists
+
+    def count_in_edges(self, ids, method: int):
+        """grand_count_in_edges: (counts, GPU milliseconds of the method)."""
+        ids = _np(ids, np.uint32)
+        out = np.zeros(ids.shape[0], np.uint32)
+        ms = ctypes.c_float(0.0)
+        self._check(self.lib.grand_count_in_edges(self.h, _ptr(ids), ids.shape[0], method, _ptr(out),
+                                                  ctypes.byref(ms)))
+        return out, float(ms.value)
 
     def search_rc(self, queries, k: int, beam: int) -> int:
         q = _np(queries, self.np_dtype)

@@ -180,6 +180,30 @@ def test_delete_lockstep(case, rev_mode):
                 say(f"  round {r}: {n} differing lists")
 
 
+@pytest.mark.parametrize("case", ["u8_d128", "cagra_ip_r30", "u8_d128_r1"])
+def test_in_edge_counts_agree_with_the_transpose(case):
+    """grand_count_in_edges: the per-id linear scan, the batch-rows reverse
+    build and the full reverse graph all count, for each given id, exactly
+    the in-degree of the oracle's transpose."""
+    from paper_2608_21163_amd import grand
+    say(f"[in-edge counts] {case}")
+    w, o = base_state(case)
+    g = gpu_index(w.cfg)
+    st = to_gpu(o, g, w)
+    offs, _ = reverse_csr(st["adj"], st["active"])
+    act = np.flatnonzero(st["active"])
+    ids = np.random.default_rng(2).choice(act, 300, replace=False).astype(np.uint32)
+    want = (offs[ids.astype(np.int64) + 1] - offs[ids]).astype(np.uint32)
+    for method in (grand.INDEG_SCAN, grand.INDEG_REV_BATCH, grand.INDEG_REV_FULL):
+        got, ms = g.count_in_edges(ids, method)
+        assert np.array_equal(got, want), method
+        say(f"  method {method}: {ms:.3f} ms")
+    assert np.array_equal(g.export()["adj"], o.export()["adj"]) if w.cfg.algo == "cagra" else True
+    inactive = np.flatnonzero(st["active"] == 0)[:1].astype(np.uint32)
+    with pytest.raises(grand.GrandError):
+        g.count_in_edges(inactive, grand.INDEG_SCAN)
+
+
 def test_delete_medoid_installs_the_same_medoid():
     say("[medoid delete] u8_d128")
     w, o = base_state("u8_d128")
