@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-recall", action="store_true")
+    ap.add_argument("--no-concurrent", action="store_true",
+                    help="skip the replay of the timed rounds with each round's queries on a second stream, "
+                         "overlapping its updates (overall throughput)")
     ap.add_argument("--reverse-microbench", action="store_true",
                     help="after the base build, time in-neighbour detection for one delete batch by a per-id "
                          "linear scan, the batch-rows reverse build and the full reverse graph, and print that")
@@ -275,6 +278,72 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
                       f"(imported from the GPU), timed on the first timed round: " + ", ".join(done)),
            "cpu": host_cpu()}
     return out
+
+
+# ------------------------------------------------------------------ concurrent rounds
+def run_concurrent(g, snap, rounds, spec, torch, ops_total, seq_wall):
+    """Replays `rounds` from `snap` with each round's searches on a reader
+    (grand_reader_*: its own HIP stream, on a second host thread) overlapping
+    that round's insert and delete batches; the round ends when both have
+    finished.  Overall throughput = (inserts + deletes + queries) / time, the
+    paper's overall measure (Section 6.1), against the same rounds run one
+    call after another (the timed region)."""
+    import threading
+
+    from paper_2608_21163_amd import Reader
+    g.import_graph(snap["vecs"], snap["adj"], snap["deg"], snap["active"], snap["medoid"])
+    torch.cuda.synchronize()
+    reader = Reader(g)
+    start, done = threading.Barrier(2), threading.Barrier(2)
+    job = {}
+    errors = []
+
+    def reader_loop():
+        while True:
+            start.wait()
+            q = job.get("q")
+            if q is None:
+                return
+            try:
+                reader.search(q[0], spec.k, spec.beam, out_ids=q[1][0], out_dists=q[1][1])
+            except Exception as e:  # reported after the run
+                errors.append(e)
+            done.wait()
+
+    t = threading.Thread(target=reader_loop, daemon=True)
+    t.start()
+    recalls = []
+    t0 = time.perf_counter()
+    for ops in rounds:
+        q = next((o for o in ops if o[0] == "search"), None)
+        job["q"] = (q[1], q[2]) if q else None
+        start.wait()
+        for kind, a, b, _ in ops:
+            if kind == "insert":
+                g.insert(a, b)
+            elif kind == "delete":
+                g.delete(a)
+        done.wait()
+    wall = time.perf_counter() - t0
+    job["q"] = None
+    start.wait()
+    t.join()
+    reader.close()
+    if errors:
+        raise errors[0]
+    for ops in rounds:
+        for kind, q, outs, gt in ops:
+            if kind == "search" and gt is not None:
+                got = outs[0].to(torch.int64)
+                hit = (got[:, :, None] == gt[:, None, :]).any(2).sum(1).float()
+                recalls.append(float(hit.mean() / spec.k))
+    return {"overall_ops_per_s": round(ops_total / wall, 1), "ms_per_round": round(wall * 1e3 / len(rounds), 3),
+            "sequential_overall_ops_per_s": round(ops_total / seq_wall, 1),
+            "sequential_ms_per_round": round(seq_wall * 1e3 / len(rounds), 3),
+            "recall_at_10_min": round(min(recalls), 4) if recalls else None,
+            "recall_note": "queries overlap their round's updates; ground truth is the state after the round",
+            "mode": "each round's queries on a reader (own stream, second host thread) while its insert and "
+                    "delete run"}
 
 
 # ------------------------------------------------------------------ reverse-graph microbenchmark
@@ -494,6 +563,15 @@ def main():
     log(f"counting rerun: {time.perf_counter() - t0:.1f} s; distinct {distinct} (counters of the timed kernels "
         f"untouched: {same})")
 
+    # ---- overall throughput (untimed for the headline value): the same rounds
+    # from the same state, each round's queries on a reader (its own stream and
+    # host thread) while the round's insert and delete run.
+    concurrent = None
+    if not args.no_concurrent:
+        concurrent = run_concurrent(g, snap, rounds[W:W + K], spec, torch, upd_n + q_n, wall)
+        log(f"concurrent rounds: overall {concurrent['overall_ops_per_s']:.0f} ops/s "
+            f"(sequential {concurrent['sequential_overall_ops_per_s']:.0f})")
+
     # ---- roofline of the dominant kernel (largest share of the timed region).
     # Phase times come from HIP events on the library stream around each
     # phase.  The three search phases are launches of one kernel (k_search);
@@ -595,6 +673,7 @@ def main():
         "roofline": roofline,
         "roofline_other_phases": others,
         "cpu_baseline": cpu,
+        "concurrent": concurrent,
         "searches": search_stats,
         "phases": phases,
         "counters": {k: v for k, v in st.items() if isinstance(v, int)},

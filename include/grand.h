@@ -169,6 +169,35 @@ enum { GRAND_INDEG_SCAN = 0, GRAND_INDEG_REV_BATCH = 1, GRAND_INDEG_REV_FULL = 2
 grand_status grand_count_in_edges(grand_index *h, const uint32_t *ids, uint32_t n, int method, uint32_t *out_counts,
                                   float *ms);
 
+/* Readers: searches that may run while the index's own host thread
+ * inserts or deletes (Section 2.3 overlaps kernels on several streams;
+ * Section 3.1 names the read-write race of a search reading a list that a
+ * delete repairs).  A reader has its own HIP stream (`stream`, or a new
+ * non-blocking stream of default priority when NULL), its own staging
+ * buffers and counters; grand_reader_search may be called from one other
+ * host thread at a time per reader, concurrently with any insert, delete or
+ * search call on the index.  Readers must be destroyed before the index;
+ * grand_import_graph must not overlap a reader's search.
+ * Consistency model of a search that overlaps an update batch: every list
+ * entry it reads is a pool id below the capacity or INVALID (lists are
+ * rewritten one 32-bit entry at a time); a list that the batch rewrites is
+ * read before, after, or part-way through its rewrite, so it may mix old
+ * and new entries; a node deleted by the batch may still be reached and
+ * returned, and an id that the batch re-inserts may be read with its old
+ * or new vector (or, while its row is being copied, a mix of the two).  The
+ * start node is the index's medoid as each search begins.  A search that
+ * overlaps no update sees the state after the last completed call and
+ * returns exactly what grand_search returns.
+ * grand_reader_search has the arguments, results and errors of
+ * grand_search, and returns after its work on the reader's stream has
+ * completed. */
+typedef struct grand_reader grand_reader;
+grand_status grand_reader_create(grand_index *h, void *stream, grand_reader **out);
+grand_status grand_reader_search(grand_reader *r, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                                 uint32_t *out_ids, float *out_dists);
+grand_status grand_reader_destroy(grand_reader *r);
+const char *grand_reader_last_error(const grand_reader *r);
+
 /* Copies the index state out.  Any output pointer may be NULL.
  *   adj: capacity x R lists, GRAND_INVALID padding.  Vamana lists are sets
  *        (their order carries no meaning) and are returned canonically:

@@ -1015,6 +1015,128 @@ grand_status grand_count_in_edges(grand_index *h, const uint32_t *ids, uint32_t 
   return GRAND_OK;
 }
 
+// ---------------------------------------------------------------- readers
+struct grand_reader {
+  grand_index *h = nullptr;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  uint8_t *q_vecs = nullptr;
+  uint32_t *q_ids = nullptr;
+  float *q_d = nullptr;
+  uint32_t qcap = 0, qk = 0;
+  DevScalars *ds = nullptr;  // the reader's own error flags and counters
+  DevScalars *hs = nullptr;  // pinned host mirror
+  std::string err;
+};
+
+namespace {
+void reader_release(grand_reader *r) {
+  dfree(r->q_vecs); dfree(r->q_ids); dfree(r->q_d); dfree(r->ds);
+  if (r->hs) (void)hipHostFree(r->hs);
+  if (r->own_stream && r->stream) (void)hipStreamDestroy(r->stream);
+}
+grand_status rfail(grand_reader *r, grand_status code, const std::string &msg) {
+  r->err = msg;
+  return code;
+}
+#define RCHK(r, x)                                                                     \
+  do {                                                                                 \
+    hipError_t e_ = (x);                                                               \
+    if (e_ != hipSuccess) return rfail((r), GRAND_E_DEVICE, std::string(#x ": ") + hipGetErrorString(e_)); \
+  } while (0)
+}  // namespace
+
+grand_status grand_reader_create(grand_index *h, void *stream, grand_reader **out) {
+  if (!out) return GRAND_E_ARG;
+  *out = nullptr;
+  grand_status s = check_usable(h);
+  if (s != GRAND_OK) return s;
+  HCHK(h, hipSetDevice(h->p.device));
+  grand_reader *r = new grand_reader();
+  r->h = h;
+  bool bad = false;
+  if (stream) {
+    r->stream = (hipStream_t)stream;
+  } else {
+    bad = hipStreamCreateWithFlags(&r->stream, hipStreamNonBlocking) != hipSuccess;  // default priority
+    r->own_stream = !bad;
+  }
+  bad = bad || dalloc(&r->ds, 1) || hipHostMalloc((void **)&r->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess;
+  if (!bad) bad = hipMemsetAsync(r->ds, 0, sizeof(DevScalars), r->stream) != hipSuccess ||
+                  hipStreamSynchronize(r->stream) != hipSuccess;
+  if (bad) {
+    (void)hipGetLastError();
+    reader_release(r);
+    delete r;
+    return fail(h, GRAND_E_OOM, "reader allocation failed");
+  }
+  *out = r;
+  return GRAND_OK;
+}
+
+grand_status grand_reader_destroy(grand_reader *r) {
+  if (!r) return GRAND_OK;
+  (void)hipSetDevice(r->h->p.device);
+  (void)hipStreamSynchronize(r->stream);
+  reader_release(r);
+  delete r;
+  return GRAND_OK;
+}
+
+grand_status grand_reader_search(grand_reader *r, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
+                                 uint32_t *out_ids, float *out_dists) {
+  if (!r) return GRAND_E_ARG;
+  grand_index *h = r->h;
+  r->err.clear();
+  if (h->poisoned) return GRAND_E_STATE;
+  if (k == 0 || beam == 0 || k > beam || beam > 256) return rfail(r, GRAND_E_ARG, "need 1 <= k <= beam <= 256");
+  if (nq == 0) return GRAND_OK;
+  if (!queries || !out_ids || !out_dists) return rfail(r, GRAND_E_ARG, "null argument");
+  RCHK(r, hipSetDevice(h->p.device));
+  if (nq > r->qcap || k > r->qk) {
+    RCHK(r, hipStreamSynchronize(r->stream));
+    const uint32_t nc = std::max(nq, r->qcap), kc = std::max(k, r->qk);
+    dfree(r->q_vecs); dfree(r->q_ids); dfree(r->q_d);
+    r->qcap = r->qk = 0;
+    if (dalloc(&r->q_vecs, (size_t)nc * h->stride) || dalloc(&r->q_ids, (size_t)nc * kc) ||
+        dalloc(&r->q_d, (size_t)nc * kc)) {
+      (void)hipGetLastError();
+      return rfail(r, GRAND_E_OOM, "device allocation of reader buffers failed");
+    }
+    RCHK(r, hipMemsetAsync(r->q_vecs, 0, (size_t)nc * h->stride, r->stream));
+    r->qcap = nc;
+    r->qk = kc;
+  }
+  RCHK(r, hipMemcpy2DAsync(r->q_vecs, h->stride, queries, h->row_bytes, h->row_bytes, nq, hipMemcpyDefault, r->stream));
+  if (h->p.dtype == GRAND_F32) {
+    RCHK(r, launch_fill_u32(&r->ds->err_code, 0u, 2, r->stream));
+    RCHK(r, launch_check_finite(r->q_vecs, nq, h->stride, h->p.dim, r->ds, r->stream));
+    RCHK(r, hipMemcpyAsync(r->hs, r->ds, kScalarBytes, hipMemcpyDeviceToHost, r->stream));
+    RCHK(r, hipStreamSynchronize(r->stream));
+    if (r->hs->err_code) return rfail(r, GRAND_E_ARG, "a query holds a non-finite element");
+  }
+  SearchArgs a{};
+  a.pool = h->pool;
+  a.qbase = r->q_vecs;
+  a.nq = nq;
+  a.start = GRAND_INVALID;
+  a.start_ptr = &h->ds->medoid;  // the index's medoid as the search starts
+  a.ell = beam;
+  a.max_iters = 2 * beam;
+  a.which = 2;
+  a.c_ids = r->q_ids;
+  a.c_d = r->q_d;
+  a.c_out = k;
+  a.ds = r->ds;
+  RCHK(r, launch_search(h->kind, h->vc, a, r->stream));
+  RCHK(r, hipMemcpyAsync(out_ids, r->q_ids, (size_t)nq * k * 4, hipMemcpyDefault, r->stream));
+  RCHK(r, hipMemcpyAsync(out_dists, r->q_d, (size_t)nq * k * 4, hipMemcpyDefault, r->stream));
+  RCHK(r, hipStreamSynchronize(r->stream));
+  return GRAND_OK;
+}
+
+const char *grand_reader_last_error(const grand_reader *r) { return r ? r->err.c_str() : "null reader"; }
+
 grand_status grand_export_graph(grand_index *h, uint32_t *adj, uint32_t *deg, uint8_t *active, uint32_t *medoid,
                                 uint32_t *rev_offsets, uint32_t *rev_srcs, uint64_t *nnz) {
   grand_status s = check_usable(h);

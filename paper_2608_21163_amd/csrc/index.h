@@ -88,6 +88,7 @@ struct SearchArgs {
   const uint32_t *qids;       // ... or pool ids used as queries (if non-null)
   uint32_t nq;
   uint32_t start;
+  const uint32_t *start_ptr;  // if non-null, the start id is read here when a search begins
   uint32_t ell;
   uint32_t max_iters;
   int which;                  // 0 insert, 1 delete, 2 query (counter slot)

@@ -102,6 +102,7 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
   if (qi >= a.nq) return;
   const PoolView &P = a.pool;
   const uint8_t *qrow = a.qids ? P.vecs + (size_t)a.qids[qi] * P.stride : a.qbase + (size_t)qi * P.stride;
+  const uint32_t start = a.start_ptr ? *a.start_ptr : a.start;
   Slice<KIND, LPV, CPL> s;
   load_slice<KIND, LPV, CPL>(s, qrow, P.nch);
   uint32_t *vrow = EXACT ? a.vis + (size_t)qi * a.vis_words : nullptr;
@@ -112,14 +113,14 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
   uint32_t ci[NR];
 #pragma unroll
   for (int r = 0; r < NR; r++) { cd[r] = finf(); ci[r] = kInvalid; }
-  if (a.start < P.cap) {  // an invalid start leaves C empty: no expansion
-    const float d0 = wave_dist1<KIND, LPV, CPL>(s, P.vecs + (size_t)a.start * P.stride, P.nch);
-    if (ln == 0) { cd[0] = d0; ci[0] = a.start; }
+  if (start < P.cap) {  // an invalid start leaves C empty: no expansion
+    const float d0 = wave_dist1<KIND, LPV, CPL>(s, P.vecs + (size_t)start * P.stride, P.nch);
+    if (ln == 0) { cd[0] = d0; ci[0] = start; }
   }
   __syncthreads();
-  if (ln == 0 && a.start < P.cap) {
-    if (EXACT) atomicOr(&vrow[a.start >> 5], 1u << (a.start & 31));
-    else hsh[H::slot(a.start)] = H::word(a.start);
+  if (ln == 0 && start < P.cap) {
+    if (EXACT) atomicOr(&vrow[start >> 5], 1u << (start & 31));
+    else hsh[H::slot(start)] = H::word(start);
   }
   __syncthreads();
   uint32_t nv = 0, evals = 1;

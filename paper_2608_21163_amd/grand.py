@@ -31,7 +31,8 @@ PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group
           "reverse", "repair", "clear", "medoid", "search_query", "cagra_detour", "cagra_pickone"]
 
 EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
-            "grand_delete_batch", "grand_search", "grand_search_static", "grand_count_in_edges", "grand_export_graph", "grand_import_graph", "grand_set_timing",
+            "grand_delete_batch", "grand_search", "grand_search_static", "grand_count_in_edges", "grand_reader_create",
+            "grand_reader_search", "grand_reader_destroy", "grand_reader_last_error", "grand_export_graph", "grand_import_graph", "grand_set_timing",
             "grand_set_counting", "grand_stats", "grand_reset_stats", "grand_last_error"]
 
 
@@ -94,6 +95,11 @@ def load_library(path: str = LIB_PATH):
     lib.grand_search.argtypes = [P, P, U32, U32, U32, P, P]
     lib.grand_search_static.argtypes = [P, P, U32, U32, U32, P, P]
     lib.grand_count_in_edges.argtypes = [P, P, U32, I32, P, P]
+    lib.grand_reader_create.argtypes = [P, P, P]
+    lib.grand_reader_search.argtypes = [P, P, U32, U32, U32, P, P]
+    lib.grand_reader_destroy.argtypes = [P]
+    lib.grand_reader_last_error.argtypes = [P]
+    lib.grand_reader_last_error.restype = ctypes.c_char_p
     lib.grand_export_graph.argtypes = [P, P, P, P, P, P, P, P]
     lib.grand_import_graph.argtypes = [P, P, P, P, P, U32]
     lib.grand_set_timing.argtypes = [P, I32]
@@ -103,7 +109,7 @@ def load_library(path: str = LIB_PATH):
     lib.grand_last_error.argtypes = [P]
     lib.grand_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
-        if name not in ("grand_default_params", "grand_last_error"):
+        if name not in ("grand_default_params", "grand_last_error", "grand_reader_last_error"):
             getattr(lib, name).restype = I32
     _lib = lib
     return lib
@@ -144,6 +150,45 @@ def params_from_config(cfg, device: int = 0, max_batch: int = 10000, rev_mode: i
     p.max_batch = max_batch
     p.device = device
     return p
+
+
+class Reader:
+    """grand_reader_create ... grand_reader_destroy: searches that may run on
+    another host thread while the index is updated (ctypes releases the
+    GIL during the call)."""
+
+    def __init__(self, index: "GrandIndex", stream: Optional[int] = None):
+        self.lib = index.lib
+        self.index = index
+        h = ctypes.c_void_p()
+        rc = self.lib.grand_reader_create(index.h, None if stream is None else ctypes.c_void_p(stream),
+                                          ctypes.byref(h))
+        if rc != OK:
+            raise GrandError(rc, index.last_error())
+        self.h = h
+
+    def search(self, queries, k: int, beam: int, out_ids=None, out_dists=None):
+        if not _is_torch(queries):
+            queries = _np(queries, self.index.np_dtype)
+        nq = int(queries.shape[0])
+        if out_ids is None:
+            out_ids = np.zeros((nq, k), np.uint32)
+            out_dists = np.zeros((nq, k), np.float32)
+        rc = self.lib.grand_reader_search(self.h, _ptr(queries), nq, k, beam, _ptr(out_ids), _ptr(out_dists))
+        if rc != OK:
+            raise GrandError(rc, self.lib.grand_reader_last_error(self.h).decode())
+        return out_ids, out_dists
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.grand_reader_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class GrandIndex:
