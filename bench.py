@@ -88,6 +88,10 @@ def parse():
     ap.add_argument("--no-concurrent", action="store_true",
                     help="skip the replay of the timed rounds with each round's queries on a second stream, "
                          "overlapping its updates (overall throughput)")
+    ap.add_argument("--pattern", default=None,
+                    help="run one streaming pattern of the workload generator (sliding_window, interleaved, "
+                         "expiration, clustered, insert_heavy) over base_n points of the workload's "
+                         "distribution instead of the rounds, and print its line")
     ap.add_argument("--reverse-microbench", action="store_true",
                     help="after the base build, time in-neighbour detection for one delete batch by a per-id "
                          "linear scan, the batch-rows reverse build and the full reverse graph, and print that")
@@ -280,6 +284,103 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
     return out
 
 
+# ------------------------------------------------------------------ streaming patterns
+def run_pattern(args):
+    """One streaming pattern (Section 5.2) over `base_n` points of the
+    workload's distribution, in batches of 1% of them: the starting index is
+    built untimed (batched inserts, then one refresh pass as for the
+    rounds), every batch of the stream is staged on the device with exact
+    ground truth, and the whole stream is timed call by call."""
+    import numpy as np
+    import torch
+
+    from paper_2608_21163_amd import GrandIndex
+    from workloads import PatternStream, make_workload
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    st_over = {"base_n": args.base} if args.base else None
+    w = make_workload(args.workload, seed=args.seed, stream=st_over)
+    cfg, spec = w.cfg, w.spec
+    ps = PatternStream(w, args.pattern, spec.base_n, n_query=spec.n_query, seed=args.seed, batch_frac=0.01,
+                       build_batch=spec.build_batch)
+    g = GrandIndex.from_config(cfg, max_batch=max(spec.build_batch, ps.batch), stream=stream.cuda_stream)
+    mirror = Mirror(torch, cfg, dev)
+    t0 = time.perf_counter()
+    base = []
+    for op in ps.base_ops():
+        ids = torch.from_numpy(op.ids.astype(np.int32)).to(dev)
+        vecs = torch.from_numpy(op.vecs).to(dev)
+        g.insert(ids, vecs)
+        mirror.insert(ids, vecs)
+        base.append((ids, vecs))
+    for ids, vecs in base:
+        g.delete(ids)
+        g.insert(ids, vecs)
+    del base
+    torch.cuda.synchronize()
+    build_s = time.perf_counter() - t0
+    log(f"pattern {args.pattern}: base of {int(mirror.active.sum())} points built in {build_s:.1f} s")
+    staged = []
+    for op in ps.ops():
+        if op.kind == "insert":
+            ids, vecs = torch.from_numpy(op.ids.astype(np.int32)).to(dev), torch.from_numpy(op.vecs).to(dev)
+            mirror.insert(ids, vecs)
+            staged.append(("insert", ids, vecs, None))
+        elif op.kind == "delete":
+            ids = torch.from_numpy(op.ids.astype(np.int32)).to(dev)
+            mirror.delete(ids)
+            staged.append(("delete", ids, None, None))
+        else:
+            q = torch.from_numpy(op.vecs).to(dev)
+            gt = mirror.knn(q, spec.k)
+            outs = (torch.empty((q.shape[0], spec.k), dtype=torch.int32, device=dev),
+                    torch.empty((q.shape[0], spec.k), dtype=torch.float32, device=dev))
+            staged.append(("search", q, outs, gt))
+    torch.cuda.synchronize()
+    log(f"pattern {args.pattern}: {len(staged)} operations staged")
+    ev = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for kind, a, b, _ in staged:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        if kind == "insert":
+            g.insert(a, b)
+        elif kind == "delete":
+            g.delete(a)
+        else:
+            g.search(a, spec.k, spec.beam, out_ids=b[0], out_dists=b[1])
+        e1.record(stream)
+        ev.append((kind, int(a.shape[0]), e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    upd_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in ev if k != "search")
+    upd_n = sum(n for k, n, e0, e1 in ev if k != "search")
+    q_ms = sum(e0.elapsed_time(e1) for k, n, e0, e1 in ev if k == "search")
+    q_n = sum(n for k, n, e0, e1 in ev if k == "search")
+    recalls = []
+    for kind, q, outs, gt in staged:
+        if kind == "search":
+            hit = (outs[0].to(torch.int64)[:, :, None] == gt[:, None, :]).any(2).sum(1).float()
+            recalls.append(float(hit.mean() / spec.k))
+    counts = {k: sum(1 for x in staged if x[0] == k) for k in ("insert", "delete", "search")}
+    rmin = round(min(recalls), 4) if recalls else None
+    res = {"metric": f"updates/sec and search QPS, {args.pattern} pattern, {SHAPE.get(args.workload, args.workload)}, "
+                     f"1 MI355X",
+           "value": round(upd_n / (upd_ms / 1e3), 1) if upd_ms > 0 else None, "unit": "updates/s", "n_gpus": 1,
+           "higher_is_better": True, "dtype": "u8" if cfg.dtype == "u8" else "f32",
+           "data": DATA_LABEL.get(args.workload, "synthetic"),
+           "config": {"workload": w.wdef.description, "pattern": args.pattern, "points": spec.base_n,
+                      "batch": ps.batch, "queries_per_search": spec.n_query, "k": spec.k, "beam": spec.beam,
+                      "operations": counts},
+           "search_qps": round(q_n / (q_ms / 1e3), 1) if q_ms > 0 else None,
+           "overall_ops_per_s": round((upd_n + q_n) / wall, 1),
+           "recall_at_10_min": rmin, "recall_at_10_mean": round(float(np.mean(recalls)), 4) if recalls else None,
+           "wall_s": round(wall, 3), "build_s": round(build_s, 2)}
+    print(json.dumps(res), flush=True)
+
+
 # ------------------------------------------------------------------ concurrent rounds
 def run_concurrent(g, snap, rounds, spec, torch, ops_total, seq_wall):
     """Replays `rounds` from `snap` with each round's searches on a reader
@@ -400,6 +501,9 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe()
+        return
+    if args.pattern:
+        run_pattern(args)
         return
     import numpy as np
     import torch

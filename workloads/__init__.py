@@ -7,7 +7,9 @@ without sharing any code of the method.
 """
 from .generators import (  # noqa: F401
     CONFIGS,
+    PATTERNS,
     IndexConfig,
+    PatternStream,
     Workload,
     make_workload,
 )

@@ -315,3 +315,161 @@ def make_workload(name: str, seed: int = 0, index: Optional[dict] = None,
     idx = dataclasses.replace(w.index, **(index or {}))
     st = dataclasses.replace(w.stream, **(stream or {}))
     return Workload(WorkloadDef(w.name, w.description, idx, st, w.sampler, w.sampler_args), seed)
+
+
+# ---------------------------------------------------------------------------
+# Streaming patterns of the paper's workload generator (Section 5.2), over a
+# fixed synthetic dataset of `n_total` points drawn from a workload's
+# sampler.  Batches are uniform and of a single operation type; searches use
+# fresh queries from the same distribution.  Ids are the smallest free ids at
+# insert time.  The k-means of the clustered pattern is workload generation
+# (it orders the data), not part of the index method.
+PATTERNS = ("sliding_window", "interleaved", "expiration", "clustered", "insert_heavy")
+_P_PAT, _P_PATQ, _P_KM = 6, 7, 8
+
+
+def _kmeans(x: np.ndarray, k: int, seed: int, iters: int = 10, sample: int = 50_000) -> np.ndarray:
+    """Lloyd's k-means on a sample (float32), then every point assigned to
+    its nearest centre; returns the cluster of each point."""
+    g = _rng(seed, _P_KM)
+    xs = x[g.choice(len(x), min(sample, len(x)), replace=False)].astype(np.float32)
+    c = xs[g.choice(len(xs), k, replace=False)].copy()
+
+    def assign(pts):
+        out = np.empty(len(pts), np.int64)
+        cn = (c * c).sum(1)
+        for s in range(0, len(pts), 65536):
+            p = pts[s:s + 65536].astype(np.float32)
+            out[s:s + len(p)] = np.argmin(cn[None, :] - 2.0 * p @ c.T, axis=1)
+        return out
+
+    for _ in range(iters):
+        a = assign(xs)
+        for j in range(k):
+            m = a == j
+            if m.any():
+                c[j] = xs[m].mean(0)
+    return assign(x)
+
+
+class PatternStream:
+    """One streaming pattern over `n_total` points of workload `w`'s
+    distribution.  `base_ops()` builds the starting index; `ops()` yields
+    the operation stream (Op with kind insert / delete / search)."""
+
+    def __init__(self, w: "Workload", pattern: str, n_total: int, n_query: int = 1000, seed: int = 0,
+                 batch_frac: float = 0.01, build_batch: int = 10_000):
+        if pattern not in PATTERNS:
+            raise ValueError(pattern)
+        self.w, self.pattern, self.n, self.nq, self.seed = w, pattern, n_total, n_query, seed
+        self.batch = max(1, int(round(batch_frac * n_total)))
+        self.build_batch = build_batch
+        g = _rng(seed, _P_PAT)
+        self.x = w.sampler.draw(g, n_total, 0.0)[0]
+        self.ids = np.full(n_total, INVALID, np.uint64)   # pool id of each dataset point while active
+        self._q = 0
+        if pattern == "clustered":
+            cl = _kmeans(self.x.astype(np.float32), 64, seed)
+            self.order = np.argsort(cl, kind="stable")
+            self.cluster_bounds = np.searchsorted(cl[self.order], np.arange(65))
+        elif pattern == "expiration":
+            half = n_total // 2
+            life = _rng(seed, _P_PAT, 1).choice(np.array([10, 100, -1]), size=n_total - half,
+                                                  p=np.array([10, 2, 1]) / 13.0)
+            self.lifetime = np.concatenate([np.full(half, -1), life])   # -1: permanent
+
+    # -- helpers
+    def _insert(self, pts: np.ndarray) -> Op:
+        ids = self.w._alloc(len(pts))
+        self.w._apply_insert(ids, self.x[pts], np.zeros(len(pts), np.int32))
+        self.ids[pts] = ids
+        return Op("insert", ids, self.x[pts])
+
+    def _delete(self, pts: np.ndarray) -> Op:
+        ids = self.ids[pts].astype(np.uint32)
+        assert (self.ids[pts] != INVALID).all()
+        self.w._apply_delete(ids)
+        self.ids[pts] = INVALID
+        return Op("delete", ids)
+
+    def _search(self) -> Op:
+        g = _rng(self.seed, _P_PATQ, self._q)
+        self._q += 1
+        return Op("search", None, self.w.sampler.draw(g, self.nq, 0.0)[0])
+
+    def _batches(self, pts):
+        for s in range(0, len(pts), self.batch):
+            yield pts[s:s + self.batch]
+
+    def _base_points(self) -> np.ndarray:
+        n = self.n
+        if self.pattern == "sliding_window":
+            return np.arange(n // 2)                       # the first 50 of 100 segments
+        if self.pattern == "expiration":
+            return np.arange(n // 2)                       # the first half
+        if self.pattern == "clustered":
+            return self.order[:self.cluster_bounds[32]]    # the first 32 clusters
+        return np.arange(n // 10)                          # interleaved, insert-heavy: 10%
+
+    def base_ops(self) -> Iterator[Op]:
+        pts = self._base_points()
+        for s in range(0, len(pts), self.build_batch):
+            yield self._insert(pts[s:s + self.build_batch])
+
+    def ops(self) -> Iterator[Op]:
+        n, p = self.n, self.pattern
+        if p == "sliding_window":
+            seg = n // 100
+            for t in range(50):
+                for b in self._batches(np.arange((t + 50) * seg, (t + 51) * seg)):
+                    yield self._insert(b)
+                for b in self._batches(np.arange(t * seg, (t + 1) * seg)):
+                    yield self._delete(b)
+                yield self._search()
+        elif p == "expiration":
+            half = n // 2
+            seg = (n - half) // 50
+            born = np.full(n, -1)
+            for c in range(50):
+                pts = np.arange(half + c * seg, half + (c + 1) * seg)
+                for b in self._batches(pts):
+                    yield self._insert(b)
+                born[pts] = c
+                exp = np.flatnonzero((born >= 0) & (self.lifetime > 0) & (born + self.lifetime == c) &
+                                     (self.ids != INVALID))
+                for b in self._batches(exp):
+                    yield self._delete(b)
+                yield self._search()
+        elif p == "clustered":
+            for t in range(32):
+                for b in self._batches(self.order[self.cluster_bounds[t + 32]:self.cluster_bounds[t + 33]]):
+                    yield self._insert(b)
+                    yield self._search()
+                for b in self._batches(self.order[self.cluster_bounds[t]:self.cluster_bounds[t + 1]]):
+                    yield self._delete(b)
+                    yield self._search()
+        elif p == "interleaved":
+            g = _rng(self.seed, _P_PAT, 2)
+            nxt = n // 10
+            while nxt < n:
+                kind = g.choice(3, p=[0.5, 0.3, 0.2])
+                if kind == 0:
+                    pts = np.arange(nxt, min(n, nxt + self.batch))
+                    nxt += len(pts)
+                    yield self._insert(pts)
+                elif kind == 1:
+                    yield self._search()
+                else:
+                    act = np.flatnonzero(self.ids != INVALID)
+                    if len(act) > self.batch:
+                        yield self._delete(np.sort(g.choice(act, self.batch, replace=False)))
+        else:  # insert_heavy
+            g = _rng(self.seed, _P_PAT, 3)
+            nxt = n // 10
+            while nxt < n:
+                if g.random() < 0.9:
+                    pts = np.arange(nxt, min(n, nxt + self.batch))
+                    nxt += len(pts)
+                    yield self._insert(pts)
+                else:
+                    yield self._search()
