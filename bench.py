@@ -51,9 +51,12 @@ DATA_LABEL = {
                      "paper's 100-d angular set)",
     "gist500k": "synthetic (seeded 128-component mixture, per-dimension scales, clipped at 0; a 960-d stress case)",
     "tiny": "synthetic (seeded N(0,1), 10,000 x 32)",
+    "ip768_mips": "synthetic (seeded 128-component mixture with varying norms, clipped at 40; stands in for the "
+                  "paper's 768-d inner-product text-embedding sets)",
 }
 SHAPE = {"sift1m_u8": "1M×128 uint8", "deep1m_window": "1M×96 fp32 sliding window",
-         "glove1m_cagra": "1M×100 fp32 IP, CAGRA degree 64", "gist500k": "500K×960 fp32", "tiny": "10K×32 fp32"}
+         "glove1m_cagra": "1M×100 fp32 IP, CAGRA degree 64", "gist500k": "500K×960 fp32", "tiny": "10K×32 fp32",
+         "ip768_mips": "500K×768 fp32 inner product via L2 augmentation"}
 
 
 def metric_of(workload, recall_min):
@@ -530,7 +533,8 @@ def main():
     idx_over = {"prune_rule": args.prune_rule} if args.prune_rule else None
     w = make_workload(args.workload, seed=args.seed, index=idx_over, stream=st_over)
     cfg, spec = w.cfg, w.spec
-    stride = ((cfg.dim * (1 if cfg.dtype == "u8" else 4)) + 15) // 16 * 16
+    sdim = cfg.dim + (1 if cfg.metric == "mips" else 0)   # stored row (the MIPS augmentation adds one)
+    stride = ((sdim * (1 if cfg.dtype == "u8" else 4)) + 15) // 16 * 16
     g = GrandIndex.from_config(cfg, max_batch=max(spec.build_batch, spec.n_insert, spec.n_delete),
                                stream=stream.cuda_stream,
                                rev_mode=REV_BATCH if args.rev_mode == "batch" else REV_FULL)

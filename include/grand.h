@@ -49,7 +49,15 @@ typedef enum {
 
 enum { GRAND_VAMANA = 0, GRAND_CAGRA = 1 };
 enum { GRAND_F32 = 0, GRAND_U8 = 1 };
-enum { GRAND_L2 = 0, GRAND_IP = 1 };
+/* GRAND_MIPS: inner-product (maximum inner product) search through the L2
+ * augmentation of Section 5.4: a stored vector is [x, sqrt(M^2 - |x|^2)]
+ * and a query [q, 0], where M (grand_params.mips_norm) bounds every stored
+ * norm, so that |x' - q'|^2 = M^2 + |q|^2 - 2 <x, q> orders points like
+ * -<x, q>.  Callers pass vectors of `dim` elements; the extra coordinate is
+ * computed as the fp32 rounding of the fp64 square root of M^2 - sum x_j^2
+ * (the sum in dimension order).  Search distances are the squared L2
+ * distances in the augmented space.  fp32 only, Vamana or CAGRA. */
+enum { GRAND_L2 = 0, GRAND_IP = 1, GRAND_MIPS = 2 };
 /* alpha test of GrANDRobustPrune (Alg. 4): alpha * Dist(p*, p') <= D_p[p']
  * on the squared distance (default), or on the Euclidean distance. */
 enum { GRAND_ALPHA_ON_DIST = 0, GRAND_ALPHA_ON_L2 = 1 };
@@ -69,7 +77,7 @@ typedef struct {
   uint32_t struct_size;  /* sizeof(grand_params) */
   int32_t algo;          /* GRAND_VAMANA | GRAND_CAGRA */
   int32_t dtype;         /* GRAND_F32 | GRAND_U8 (U8 requires L2) */
-  int32_t metric;        /* GRAND_L2 | GRAND_IP (IP requires CAGRA and F32) */
+  int32_t metric;        /* GRAND_L2 | GRAND_IP (IP requires CAGRA and F32) | GRAND_MIPS (F32) */
   uint32_t dim;          /* vector length; f32 <= 1024, u8 <= 4096 */
   uint32_t capacity;     /* pool size N (ids in [0, N)), < 2^31 */
   uint32_t R;            /* degree bound (Vamana) / fixed degree (CAGRA), 1..64 */
@@ -83,6 +91,7 @@ typedef struct {
   int32_t cas_mode;      /* GRAND_CAS_GROUPED | GRAND_CAS_RACING */
   int32_t rev_mode;      /* GRAND_REV_FULL | GRAND_REV_BATCH */
   uint32_t max_batch;    /* batch size the per-batch buffers are first sized for (grown on demand) */
+  float mips_norm;       /* GRAND_MIPS: M, at least the norm of every vector inserted or imported */
   int32_t device;        /* HIP device ordinal */
   void *stream;          /* hipStream_t for all work; NULL = the null stream */
 } grand_params;
@@ -112,7 +121,8 @@ grand_status grand_set_stream(grand_index *h, void *stream);
  * target and applied once per target.  An index empty at the start of the
  * batch is bootstrapped from the batch itself (each point's candidates are
  * its nearest other batch points) and its medoid computed.
- * n == 0 is a no-op.  Errors: GRAND_E_ID, GRAND_E_ARG (non-finite element). */
+ * n == 0 is a no-op.  Errors: GRAND_E_ID, GRAND_E_ARG (non-finite element;
+ * with GRAND_MIPS a vector whose norm exceeds mips_norm). */
 grand_status grand_insert_batch(grand_index *h, const void *vecs, const uint32_t *ids, uint32_t n);
 
 /* BatchDelete (Alg. 3; Vamana Alg. 6; CAGRA Alg. 8), in place.

@@ -33,7 +33,7 @@
 enum { O_OK = 0, O_E_ARG = -1, O_E_ID = -2, O_E_CAPACITY = -3, O_E_OOM = -5 };
 enum { O_VAMANA = 0, O_CAGRA = 1 };
 enum { O_F32 = 0, O_U8 = 1 };
-enum { O_L2 = 0, O_IP = 1 };
+enum { O_L2 = 0, O_IP = 1, O_MIPS = 2 };
 enum { O_ALPHA_ON_DIST = 0, O_ALPHA_ON_L2 = 1 };
 
 typedef struct {
@@ -41,6 +41,7 @@ typedef struct {
     uint32_t dim, capacity, R, L_build, P, c, k_repair, max_iters;
     float alpha;
     int32_t threads;
+    float mips_norm;           /* O_MIPS: M, the bound on every stored norm */
 } ocfg;
 
 typedef struct {
@@ -49,6 +50,7 @@ typedef struct {
 
 typedef struct {
     ocfg cfg;
+    uint32_t sdim;             /* stored elements per row: dim, or dim + 1 for O_MIPS */
     size_t esize;              /* bytes per element */
     uint8_t *vecs;             /* capacity x dim */
     uint32_t *adj;             /* capacity x R */
@@ -74,7 +76,34 @@ static int key_cmp(const void *pa, const void *pb) {
 static int nthreads(const oindex *h) { return h->cfg.threads > 0 ? h->cfg.threads : omp_get_max_threads(); }
 
 static const void *vec_of(const oindex *h, uint32_t id) {
-    return h->vecs + (size_t)id * h->cfg.dim * h->esize;
+    return h->vecs + (size_t)id * h->sdim * h->esize;
+}
+
+/* ------------------------------------------------------------------------
+ * MIPS to L2 (Section 5.4): inner-product data are searched as L2 data by
+ * storing x' = [x, sqrt(M^2 - |x|^2)] (M bounds every norm) and querying
+ * with q' = [q, 0]: |x' - q'|^2 = M^2 + |q|^2 - 2 <x, q>, an increasing
+ * function of -<x, q>.  The squared norm is an fp64 sum in dimension order,
+ * the square root is taken in fp64 and rounded once to fp32.  Returns 0, or
+ * -1 when |x|^2 exceeds M^2.
+ * ---------------------------------------------------------------------- */
+static int mips_row(const oindex *h, const float *x, float *out, int is_query) {
+    const uint32_t d = h->cfg.dim;
+    double s = 0.0;
+    for (uint32_t j = 0; j < d; j++) { out[j] = x[j]; s = fma((double)x[j], (double)x[j], s); }
+    if (is_query) { out[d] = 0.0f; return 0; }
+    double M2 = (double)h->cfg.mips_norm * (double)h->cfg.mips_norm;
+    double t = M2 - s;
+    out[d] = (float)sqrt(t > 0.0 ? t : 0.0);
+    return s > M2 ? -1 : 0;
+}
+
+/* A caller row (dim elements) as stored (sdim elements): copied, or
+ * augmented for O_MIPS.  out holds sdim elements. */
+static int store_row(const oindex *h, const void *x, void *out, int is_query) {
+    if (h->cfg.metric == O_MIPS) return mips_row(h, x, out, is_query);
+    memcpy(out, x, (size_t)h->cfg.dim * h->esize);
+    return 0;
 }
 
 /* ------------------------------------------------------------------------
@@ -86,7 +115,7 @@ static const void *vec_of(const oindex *h, uint32_t id) {
  * A zero result is returned as +0.
  * ---------------------------------------------------------------------- */
 static float dist_raw(const oindex *h, const void *a, const void *b) {
-    uint32_t d = h->cfg.dim;
+    uint32_t d = h->sdim;
     float r;
     if (h->cfg.dtype == O_U8) {
         const uint8_t *x = a, *y = b;
@@ -101,7 +130,7 @@ static float dist_raw(const oindex *h, const void *a, const void *b) {
     } else {
         const float *x = a, *y = b;
         double s = 0.0;
-        if (h->cfg.metric == O_L2) {
+        if (h->cfg.metric != O_IP) {
             for (uint32_t j = 0; j < d; j++) { double t = (double)x[j] - (double)y[j]; s = fma(t, t, s); }
             r = (float)s;
         } else {
@@ -248,7 +277,7 @@ static uint32_t robust_prune(const oindex *h, uint32_t p, const okey *cand_in, u
 #define O_CENTROID_BLOCK 1024u
 
 static uint32_t medoid_u8(const oindex *h, uint64_t n) {
-    const uint32_t d = h->cfg.dim, cap = h->cfg.capacity;
+    const uint32_t d = h->sdim, cap = h->cfg.capacity;
     uint64_t *S = calloc(d, sizeof(uint64_t));
     for (uint32_t i = 0; i < cap; i++) {
         if (!h->active[i]) continue;
@@ -272,7 +301,7 @@ static uint32_t medoid_u8(const oindex *h, uint64_t n) {
 }
 
 static uint32_t compute_medoid(const oindex *h) {
-    const uint32_t d = h->cfg.dim, cap = h->cfg.capacity;
+    const uint32_t d = h->sdim, cap = h->cfg.capacity;
     uint64_t n = 0;
     for (uint32_t i = 0; i < cap; i++) n += h->active[i] ? 1 : 0;
     if (n == 0) return O_INVALID;
@@ -467,11 +496,18 @@ static int validate_ids(oindex *h, const uint32_t *ids, uint32_t n, int want_act
     return rc;
 }
 
-static int validate_vectors(oindex *h, const void *vecs, uint32_t n) {
+static int validate_vectors(oindex *h, const void *vecs, uint32_t n, int is_query) {
     if (h->cfg.dtype != O_F32) return O_OK;
     const float *x = vecs;
     for (uint64_t i = 0; i < (uint64_t)n * h->cfg.dim; i++)
         if (!isfinite(x[i])) { snprintf(h->err, sizeof h->err, "non-finite vector element"); return O_E_ARG; }
+    if (h->cfg.metric == O_MIPS && !is_query) {
+        float *tmp = malloc(sizeof(float) * h->sdim);
+        int bad = 0;
+        for (uint32_t i = 0; i < n && !bad; i++) bad = mips_row(h, x + (size_t)i * h->cfg.dim, tmp, 0) != 0;
+        free(tmp);
+        if (bad) { snprintf(h->err, sizeof h->err, "vector norm above mips_norm"); return O_E_ARG; }
+    }
     return O_OK;
 }
 
@@ -485,8 +521,9 @@ void *oracle_create(const ocfg *cfg) {
     h->cfg = *cfg;
     if (h->cfg.max_iters == 0) h->cfg.max_iters = 2 * h->cfg.L_build;
     h->esize = cfg->dtype == O_U8 ? 1 : 4;
+    h->sdim = cfg->dim + (cfg->metric == O_MIPS ? 1 : 0);
     size_t cap = cfg->capacity;
-    h->vecs = calloc(cap * cfg->dim, h->esize);
+    h->vecs = calloc(cap * h->sdim, h->esize);
     h->adj = malloc(cap * cfg->R * sizeof(uint32_t));
     h->deg = calloc(cap, sizeof(uint32_t));
     h->active = calloc(cap, 1);
@@ -511,7 +548,7 @@ void oracle_get_stats(void *hv, ostats *out) { *out = ((oindex *)hv)->st; }
 static void stage(oindex *h, const void *vecs, const uint32_t *ids, uint32_t n) {
     size_t row = (size_t)h->cfg.dim * h->esize;
     for (uint32_t i = 0; i < n; i++) {
-        memcpy(h->vecs + (size_t)ids[i] * row, (const uint8_t *)vecs + (size_t)i * row, row);
+        store_row(h, (const uint8_t *)vecs + (size_t)i * row, h->vecs + (size_t)ids[i] * h->sdim * h->esize, 0);
         for (uint32_t t = 0; t < h->cfg.R; t++) h->adj[(size_t)ids[i] * h->cfg.R + t] = O_INVALID;
         h->deg[ids[i]] = 0;
         h->active[ids[i]] = 1;
@@ -702,7 +739,7 @@ int32_t oracle_insert_batch(void *hv, const void *vecs, const uint32_t *ids, uin
     if (!vecs || !ids) { snprintf(h->err, sizeof h->err, "null argument"); return O_E_ARG; }
     int rc = validate_ids(h, ids, n, 0);
     if (rc) return rc;
-    rc = validate_vectors(h, vecs, n);
+    rc = validate_vectors(h, vecs, n, 0);
     if (rc) return rc;
     return h->cfg.algo == O_CAGRA ? cagra_insert(h, vecs, ids, n) : vamana_insert(h, vecs, ids, n);
 }
@@ -903,7 +940,7 @@ int32_t oracle_search(void *hv, const void *queries, uint32_t nq, uint32_t k, ui
     h->err[0] = 0;
     if (k == 0 || beam == 0 || k > beam) { snprintf(h->err, sizeof h->err, "need 1 <= k <= beam"); return O_E_ARG; }
     if (nq == 0) return O_OK;
-    if (validate_vectors(h, queries, nq)) return O_E_ARG;
+    if (validate_vectors(h, queries, nq, 1)) return O_E_ARG;
     size_t row = (size_t)h->cfg.dim * h->esize;
     uint64_t hops = 0, evals = 0;
     #pragma omp parallel for schedule(dynamic, 4) num_threads(nthreads(h)) reduction(+:hops, evals)
@@ -911,8 +948,11 @@ int32_t oracle_search(void *hv, const void *queries, uint32_t nq, uint32_t k, ui
         uint32_t got = 0;
         if (h->n_active > 0) {
             osearch s;
+            uint8_t *qs = malloc((size_t)h->sdim * h->esize);
+            store_row(h, (const uint8_t *)queries + (size_t)i * row, qs, 1);
             search_alloc(&s, beam, h->cfg.R, 2 * beam);
-            beam_search(h, (const uint8_t *)queries + (size_t)i * row, h->medoid, beam, 2 * beam, &s);
+            beam_search(h, qs, h->medoid, beam, 2 * beam, &s);
+            free(qs);
             for (; got < k && got < s.nC; got++) {
                 out_ids[(size_t)i * k + got] = s.C[got].id;
                 out_d[(size_t)i * k + got] = s.C[got].d;
@@ -959,7 +999,9 @@ int32_t oracle_import_graph(void *hv, const void *vecs, const uint32_t *adj, con
                             const uint8_t *active, uint32_t medoid) {
     oindex *h = hv;
     size_t cap = h->cfg.capacity;
-    memcpy(h->vecs, vecs, cap * h->cfg.dim * h->esize);
+    const size_t row = (size_t)h->cfg.dim * h->esize;
+    for (size_t i = 0; i < cap; i++)
+        store_row(h, (const uint8_t *)vecs + i * row, h->vecs + i * h->sdim * h->esize, 0);
     memcpy(h->adj, adj, cap * h->cfg.R * sizeof(uint32_t));
     memcpy(h->deg, deg, cap * sizeof(uint32_t));
     memcpy(h->active, active, cap);
@@ -970,7 +1012,14 @@ int32_t oracle_import_graph(void *hv, const void *vecs, const uint32_t *adj, con
 }
 
 /* ---- pieces exposed for the pin tests ---------------------------------- */
+/* Dist of two stored rows (sdim elements each). */
 float oracle_dist(void *hv, const void *a, const void *b) { return dist_raw(hv, a, b); }
+
+/* A caller row as stored (sdim elements): is_query selects the query form
+ * of the MIPS augmentation.  Returns -1 for a norm above mips_norm. */
+int32_t oracle_store_row(void *hv, const void *x, void *out, int32_t is_query) {
+    return store_row(hv, x, out, is_query);
+}
 
 /* BeamSearch on the current state from start s; writes C (ids, dists) and V
  * (ids, dists); returns |C| and stores |V| in *nV. */
@@ -978,8 +1027,11 @@ uint32_t oracle_beam_search(void *hv, const void *q, uint32_t s, uint32_t ell, u
                             uint32_t *C_ids, float *C_d, uint32_t *V_ids, float *V_d, uint32_t *nV) {
     oindex *h = hv;
     osearch st;
+    uint8_t *qs = malloc((size_t)h->sdim * h->esize);
+    store_row(h, q, qs, 1);
     search_alloc(&st, ell, h->cfg.R, max_iters);
-    beam_search(h, q, s, ell, max_iters, &st);
+    beam_search(h, qs, s, ell, max_iters, &st);
+    free(qs);
     for (uint32_t i = 0; i < st.nC; i++) { C_ids[i] = st.C[i].id; C_d[i] = st.C[i].d; }
     for (uint32_t i = 0; i < st.nV; i++) { V_ids[i] = st.V[i].id; V_d[i] = st.V[i].d; }
     *nV = st.nV;
@@ -1015,7 +1067,8 @@ int32_t oracle_bruteforce_knn(void *hv, const void *queries, uint32_t nq, uint32
     const uint32_t cap = h->cfg.capacity;
     #pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads(h))
     for (uint32_t i = 0; i < nq; i++) {
-        const void *q = (const uint8_t *)queries + (size_t)i * row;
+        uint8_t *q = malloc((size_t)h->sdim * h->esize);
+        store_row(h, (const uint8_t *)queries + (size_t)i * row, q, 1);
         okey *best = malloc(sizeof(okey) * (k + 1));
         uint32_t nb = 0;
         for (uint32_t v = 0; v < cap; v++) {
@@ -1031,6 +1084,7 @@ int32_t oracle_bruteforce_knn(void *hv, const void *queries, uint32_t nq, uint32
             out_d[(size_t)i * k + j] = j < nb ? best[j].d : INFINITY;
         }
         free(best);
+        free(q);
     }
     return O_OK;
 }

@@ -63,6 +63,8 @@ def _load():
     lib.oracle_dist.argtypes = [P, P, P]
     lib.oracle_beam_search.restype = U32
     lib.oracle_beam_search.argtypes = [P, P, U32, U32, U32, P, P, P, P, P]
+    lib.oracle_store_row.restype = I32
+    lib.oracle_store_row.argtypes = [P, P, P, I32]
     lib.oracle_robust_prune.restype = U32
     lib.oracle_robust_prune.argtypes = [P, U32, P, P, U32, P]
     lib.oracle_medoid.restype = U32
@@ -81,7 +83,7 @@ class _Cfg(ctypes.Structure):
                 ("dim", ctypes.c_uint32), ("capacity", ctypes.c_uint32), ("R", ctypes.c_uint32),
                 ("L_build", ctypes.c_uint32), ("P", ctypes.c_uint32), ("c", ctypes.c_uint32),
                 ("k_repair", ctypes.c_uint32), ("max_iters", ctypes.c_uint32),
-                ("alpha", ctypes.c_float), ("threads", ctypes.c_int32)]
+                ("alpha", ctypes.c_float), ("threads", ctypes.c_int32), ("mips_norm", ctypes.c_float)]
 
 
 class _Stats(ctypes.Structure):
@@ -113,7 +115,7 @@ class Oracle:
         self.lib = _load()
         self.cfg = cfg
         c = _Cfg(algo=1 if cfg.algo == "cagra" else 0, dtype=1 if cfg.dtype == "u8" else 0,
-                 metric=1 if cfg.metric == "ip" else 0,
+                 metric={"l2": 0, "ip": 1, "mips": 2}[cfg.metric], mips_norm=cfg.mips_norm,
                  prune_rule=1 if cfg.prune_rule == "alpha_on_l2" else 0,
                  dim=cfg.dim, capacity=cfg.capacity, R=cfg.R, L_build=cfg.L_build, P=cfg.P,
                  c=cfg.c, k_repair=cfg.k_repair, max_iters=cfg.iters, alpha=cfg.alpha,
@@ -197,6 +199,15 @@ class Oracle:
                                          _ptr(V_ids), _ptr(V_d), _ptr(nV))
         n = int(nV[0])
         return C_ids[:nC], C_d[:nC], V_ids[:n], V_d[:n]
+
+    def store_row(self, x, is_query: bool = False):
+        """A caller row in its stored form (the MIPS augmentation appends one
+        coordinate); returns (row, status)."""
+        x = np.ascontiguousarray(x, self.np_dtype)
+        sdim = self.cfg.dim + (1 if self.cfg.metric == "mips" else 0)
+        out = np.zeros(sdim, self.np_dtype)
+        rc = self.lib.oracle_store_row(self.h, _ptr(x), _ptr(out), 1 if is_query else 0)
+        return out, rc
 
     def robust_prune(self, p: int, ids, D) -> np.ndarray:
         ids = np.ascontiguousarray(ids, np.uint32)

@@ -56,7 +56,9 @@ struct grand_index {
   hipStream_t stream = nullptr;
   uint8_t *static_scratch = nullptr;  // this device's address of `scratch`
   int kind = 0, vc = 0;
-  size_t esize = 0, row_bytes = 0, stride = 0;
+  size_t esize = 0, row_bytes = 0, stride = 0;  // caller row bytes; stored row bytes (16-byte multiple)
+  uint32_t sdim = 0;   // stored elements per row: dim, or dim + 1 with GRAND_MIPS
+  bool mips = false;
   int nch = 0;
   uint32_t iters = 0;
   double coef = 0.0;
@@ -220,6 +222,7 @@ grand_status read_validation(grand_index *h) {
     case kErrRange: snprintf(buf, sizeof buf, "id %u is out of range", id); return fail(h, GRAND_E_ID, buf);
     case kErrRepeat: snprintf(buf, sizeof buf, "id %u is repeated in the batch", id); return fail(h, GRAND_E_ID, buf);
     case kErrState: snprintf(buf, sizeof buf, "id %u is in the wrong active state", id); return fail(h, GRAND_E_ID, buf);
+    case kErrNorm: snprintf(buf, sizeof buf, "row %u has a norm above mips_norm", id); return fail(h, GRAND_E_ARG, buf);
     default: snprintf(buf, sizeof buf, "row %u holds a non-finite element", id); return fail(h, GRAND_E_ARG, buf);
   }
 }
@@ -335,7 +338,7 @@ grand_status run_rebuild(grand_index *h, size_t nrec, const uint8_t *in_batch) {
 grand_status run_medoid(grand_index *h, const uint8_t *in_batch, int force) {
   Phase ph(h, GRAND_PH_MEDOID);
   HCHK(h, launch_medoid_need(h->ds, in_batch, force, h->stream));
-  HCHK(h, launch_medoid(h->pool, h->kind, h->p.dim, h->n_active, h->med_tmp, h->ds, h->stream));
+  HCHK(h, launch_medoid(h->pool, h->kind, h->sdim, h->n_active, h->med_tmp, h->ds, h->stream));
   return GRAND_OK;
 }
 
@@ -593,7 +596,11 @@ bool params_ok(const grand_params *p, std::string &why) {
   if (!p || p->struct_size != sizeof(grand_params)) { why = "grand_params.struct_size mismatch"; return false; }
   if (p->algo != GRAND_VAMANA && p->algo != GRAND_CAGRA) { why = "unknown algo"; return false; }
   if (p->dtype != GRAND_F32 && p->dtype != GRAND_U8) { why = "unknown dtype"; return false; }
-  if (p->metric != GRAND_L2 && p->metric != GRAND_IP) { why = "unknown metric"; return false; }
+  if (p->metric != GRAND_L2 && p->metric != GRAND_IP && p->metric != GRAND_MIPS) { why = "unknown metric"; return false; }
+  if (p->metric == GRAND_MIPS && (p->dtype != GRAND_F32 || !(p->mips_norm > 0.0f) || !isfinite(p->mips_norm))) {
+    why = "GRAND_MIPS needs fp32 data and a finite mips_norm > 0";
+    return false;
+  }
   if (p->metric == GRAND_IP && (p->dtype != GRAND_F32 || p->algo != GRAND_CAGRA)) {
     why = "inner product is supported for fp32 CAGRA indexes (Vamana uses L2)";
     return false;
@@ -703,8 +710,10 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
   }
   h->kind = p->dtype == GRAND_U8 ? kU8L2 : (p->metric == GRAND_IP ? kF32IP : kF32L2);
   h->esize = p->dtype == GRAND_U8 ? 1 : 4;
+  h->mips = p->metric == GRAND_MIPS;
+  h->sdim = p->dim + (h->mips ? 1 : 0);
   h->row_bytes = (size_t)p->dim * h->esize;
-  h->stride = (h->row_bytes + 15) / 16 * 16;
+  h->stride = ((size_t)h->sdim * h->esize + 15) / 16 * 16;
   h->nch = (int)(h->stride / 16);
   h->vc = vec_class(h->nch);
   if (h->vc < 0) {
@@ -741,7 +750,7 @@ grand_status grand_create(const grand_params *p, grand_index **out) {
              (group_two_level(p->capacity) && (dalloc(&h->grp.dpad, group_pad_words(p->capacity)) ||
                                                dalloc(&h->grp.dcnt, group_buckets(p->capacity)))) ||
              dalloc(&h->ds, 1) ||
-             hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim)) != hipSuccess ||
+             hipMalloc(&h->med_tmp, medoid_tmp_bytes(p->capacity, p->dim + 1)) != hipSuccess ||
              hipHostMalloc((void **)&h->hs, sizeof(DevScalars), hipHostMallocDefault) != hipSuccess ||
              hipEventCreateWithFlags(&h->ev_total, hipEventDisableTiming) != hipSuccess ||
              hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming) != hipSuccess ||
@@ -815,6 +824,7 @@ grand_status grand_insert_batch(grand_index *h, const void *vecs, const uint32_t
     HCHK(h, launch_validate_ids(h->b_ids, n, h->p.capacity, h->pool.active, h->mark, h->epoch, 0, h->ds, h->stream));
     if (h->p.dtype == GRAND_F32)
       HCHK(h, launch_check_finite(h->b_vecs, n, h->stride, h->p.dim, h->ds, h->stream));
+    if (h->mips) HCHK(h, launch_mips_augment(h->b_vecs, n, h->stride, h->p.dim, h->p.mips_norm, h->ds, h->stream));
   }
   if ((s = read_validation(h)) != GRAND_OK) {
     (void)finish(h);
@@ -868,7 +878,7 @@ grand_status grand_delete_batch(grand_index *h, const uint32_t *ids, uint32_t n)
   if (!h->hs->need_medoid) return GRAND_OK;
   {
     Phase ph(h, GRAND_PH_MEDOID);
-    HCHK(h, launch_medoid(h->pool, h->kind, h->p.dim, h->n_active, h->med_tmp, h->ds, h->stream));
+    HCHK(h, launch_medoid(h->pool, h->kind, h->sdim, h->n_active, h->med_tmp, h->ds, h->stream));
   }
   return finish(h);
 }
@@ -1217,8 +1227,9 @@ grand_status grand_import_graph(grand_index *h, const void *vecs, const uint32_t
   HCHK(h, hipMemcpyAsync(h->pool.adj, adj, cap * h->p.R * 4, hipMemcpyDefault, h->stream));
   HCHK(h, hipMemcpyAsync(h->pool.deg, deg, cap * 4, hipMemcpyDefault, h->stream));
   HCHK(h, hipMemcpyAsync(h->pool.active, active, cap, hipMemcpyDefault, h->stream));
-  HCHK(h, launch_adj_dists(h->pool, h->stream));
   if ((s = clear_errors(h)) != GRAND_OK) return s;
+  if (h->mips) HCHK(h, launch_mips_augment(h->pool.vecs, cap, h->stride, h->p.dim, h->p.mips_norm, h->ds, h->stream));
+  HCHK(h, launch_adj_dists(h->pool, h->stream));
   HCHK(h, hipMemsetAsync(&h->ds->n_count, 0, sizeof(unsigned long long), h->stream));
   hipLaunchKernelGGL(k_import_check, dim3(4096), dim3(256), 0, h->stream, h->pool, h->ds);
   hipLaunchKernelGGL(k_count_active, dim3(1024), dim3(256), 0, h->stream, h->pool.active, h->p.capacity, h->ds);
@@ -1229,7 +1240,10 @@ grand_status grand_import_graph(grand_index *h, const void *vecs, const uint32_t
   if (h->hs->err_code) {
     // malformed lists: leave an empty index rather than an inconsistent one
     char buf[128];
-    snprintf(buf, sizeof buf, "list of node %u holds an invalid, inactive or self edge", h->hs->err_id);
+    if (h->hs->err_code == kErrNorm)
+      snprintf(buf, sizeof buf, "row %u has a norm above mips_norm", h->hs->err_id);
+    else
+      snprintf(buf, sizeof buf, "list of node %u holds an invalid, inactive or self edge", h->hs->err_id);
     HCHK(h, launch_fill_u32(h->pool.adj, GRAND_INVALID, cap * h->p.R, h->stream));
     HCHK(h, hipMemsetAsync(h->pool.deg, 0, cap * 4, h->stream));
     HCHK(h, hipMemsetAsync(h->pool.active, 0, cap, h->stream));

@@ -63,7 +63,7 @@ __device__ __forceinline__ void stat_add(DevScalars *ds, int id, unsigned long l
   if (v) atomicAdd(&ds->stat[(size_t)(blockIdx.x % kStatSlots) * kStatWords + id], v);
 }
 
-enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4 };
+enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4, kErrNorm = 5 };
 
 // Vector-layout classes: lanes per row (LPV) and 16-byte chunks per lane
 // (CPL) of the distance machinery, chosen from the padded row length.
@@ -207,6 +207,11 @@ hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s);
 hipError_t launch_fill_u8(uint8_t *p, uint8_t v, size_t n, hipStream_t s);
 hipError_t launch_validate_ids(const uint32_t *ids, uint32_t n, uint32_t cap, const uint8_t *active,
                                uint32_t *mark, uint32_t epoch, int want_active, DevScalars *ds, hipStream_t s);
+// Augmentation of inner-product rows into L2 rows (Section 5.4): row[dim] =
+// fp32(sqrt(M^2 - sum_j row[j]^2)), the sum in fp64 in dimension order;
+// rows whose squared norm exceeds M^2 raise kErrNorm.
+hipError_t launch_mips_augment(uint8_t *rows, size_t n, size_t stride, uint32_t dim, float M, DevScalars *ds,
+                               hipStream_t s);
 hipError_t launch_check_finite(const uint8_t *rows, uint32_t n, size_t stride, uint32_t dim, DevScalars *ds,
                                hipStream_t s);
 // Stored list distances apply to Vamana uint8 pools whose list writers are

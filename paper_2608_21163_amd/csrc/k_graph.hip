@@ -77,6 +77,25 @@ hipError_t launch_check_finite(const uint8_t *rows, uint32_t n, size_t stride, u
   return hipGetLastError();
 }
 
+__global__ void k_mips_augment(uint8_t *rows, size_t n, size_t stride, uint32_t dim, double M2, DevScalars *ds) {
+  for (size_t r = blockIdx.x * (size_t)blockDim.x + threadIdx.x; r < n; r += (size_t)gridDim.x * blockDim.x) {
+    float *x = reinterpret_cast<float *>(rows + r * stride);
+    double s = 0.0;
+    for (uint32_t j = 0; j < dim; j++) s = __builtin_fma((double)x[j], (double)x[j], s);
+    if (s > M2) set_error(ds, kErrNorm, (uint32_t)r);
+    const double t = M2 - s;
+    x[dim] = (float)sqrt(t > 0.0 ? t : 0.0);
+  }
+}
+hipError_t launch_mips_augment(uint8_t *rows, size_t n, size_t stride, uint32_t dim, float M, DevScalars *ds,
+                               hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  uint32_t g = blocks_for(n, 64);
+  if (g > 65535) g = 65535;
+  hipLaunchKernelGGL(k_mips_augment, dim3(g), dim3(64), 0, s, rows, n, stride, dim, (double)M * (double)M, ds);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- staging
 // Alg. 5 / Alg. 7 first loop: write x_i into slot p_i, empty its list, mark
 // it active; remember each id's batch position.  One wave per new point.

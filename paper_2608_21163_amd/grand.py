@@ -20,7 +20,7 @@ INVALID = 0xFFFFFFFF
 OK, E_ARG, E_ID, E_CAPACITY, E_DEVICE, E_OOM, E_STATE = 0, -1, -2, -3, -4, -5, -6
 VAMANA, CAGRA = 0, 1
 F32, U8 = 0, 1
-L2, IP = 0, 1
+L2, IP, MIPS = 0, 1, 2
 ALPHA_ON_DIST, ALPHA_ON_L2 = 0, 1
 CAS_GROUPED, CAS_RACING = 0, 1
 REV_FULL, REV_BATCH = 0, 1
@@ -48,7 +48,8 @@ class Params(ctypes.Structure):
                 ("R", ctypes.c_uint32), ("L_build", ctypes.c_uint32), ("P", ctypes.c_uint32),
                 ("c", ctypes.c_uint32), ("k_repair", ctypes.c_uint32), ("max_iters", ctypes.c_uint32),
                 ("alpha", ctypes.c_float), ("prune_rule", ctypes.c_int32), ("cas_mode", ctypes.c_int32),
-                ("rev_mode", ctypes.c_int32), ("max_batch", ctypes.c_uint32), ("device", ctypes.c_int32),
+                ("rev_mode", ctypes.c_int32), ("max_batch", ctypes.c_uint32), ("mips_norm", ctypes.c_float),
+                ("device", ctypes.c_int32),
                 ("stream", ctypes.c_void_p)]
 
 
@@ -140,7 +141,8 @@ def params_from_config(cfg, device: int = 0, max_batch: int = 10000, rev_mode: i
     load_library().grand_default_params(ctypes.byref(p))
     p.algo = CAGRA if cfg.algo == "cagra" else VAMANA
     p.dtype = U8 if cfg.dtype == "u8" else F32
-    p.metric = IP if cfg.metric == "ip" else L2
+    p.metric = {"l2": L2, "ip": IP, "mips": MIPS}[cfg.metric]
+    p.mips_norm = getattr(cfg, "mips_norm", 0.0)
     p.dim, p.capacity, p.R, p.L_build = cfg.dim, cfg.capacity, cfg.R, cfg.L_build
     p.P, p.c, p.k_repair, p.max_iters = cfg.P, cfg.c, cfg.k_repair, cfg.max_iters
     p.alpha = cfg.alpha

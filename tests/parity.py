@@ -134,9 +134,16 @@ def tie_context(o_pre, w, algo, batch_ids, coef):
     """Context for explain_differences: the oracle of the pre-batch state,
     the pool vectors, the batch ids and the search parameters."""
     vecs = w.vectors
+    stored = {}
+
+    def row(i):
+        # the stored form of a point (the MIPS augmentation appends a coordinate)
+        if i not in stored:
+            stored[i] = o_pre.store_row(vecs[i])[0]
+        return stored[i]
 
     def dist(a, b):
-        return o_pre.dist(vecs[a], vecs[b])
+        return o_pre.dist(row(a), row(b))
 
     cfg = w.cfg
     return dict(algo=algo, dist=dist, coef=coef, pre=o_pre, vecs=vecs,

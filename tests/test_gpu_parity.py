@@ -49,6 +49,9 @@ CASES = {
                    dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     "u8_d128_r1": ("sift1m_u8", dict(capacity=12_000, R=1),
                    dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    # inner-product data through the L2 augmentation (Section 5.4)
+    "mips_f32_d64": ("ip768_mips", dict(capacity=9_000, dim=64),
+                     dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.001),
 }
 
 

@@ -39,7 +39,7 @@ class IndexConfig:
     """Index parameters (Section 5.4 names l, alpha, P, k, c; R per workload)."""
     algo: str            # "vamana" | "cagra"
     dtype: str           # "f32" | "u8"
-    metric: str          # "l2" | "ip"
+    metric: str          # "l2" | "ip" | "mips" (inner product through the L2 augmentation)
     dim: int
     capacity: int
     R: int
@@ -51,6 +51,7 @@ class IndexConfig:
     max_iters: int = 0   # expansion cap of build searches; 0 means 2 * L_build
     prune_rule: str = "alpha_on_sq"   # or "alpha_on_l2"
     cas_mode: str = "grouped"         # or "racing" (CAGRA insert only)
+    mips_norm: float = 0.0            # metric "mips": the bound M on every vector norm
 
     @property
     def iters(self) -> int:
@@ -133,6 +134,14 @@ CONFIGS = {
         "mix_t_norm", (1000, 0.3, 3.0)),
     # 500K x 960 fp32, 128-component mixture, per-dimension scale U[0.1,1],
     # clipped at zero; 10 rounds of +5K / -5K / 5K queries (beam 128).
+    # 500K x 768 fp32 inner-product data with varying norms (a Gaussian
+    # mixture, norms clipped at 40), searched through the L2 augmentation
+    # with M = 40; 10 rounds of +5K / -5K / 5K queries (beam 128).
+    "ip768_mips": WorkloadDef(
+        "ip768_mips", "500K x 768 fp32 inner product (MIPS via L2 augmentation), Vamana R=64 L=128",
+        IndexConfig("vamana", "f32", "mips", 768, 505_000, 64, 128, mips_norm=40.0),
+        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128),
+        "mix_ip", (128, 0.35, 40.0)),
     "gist500k": WorkloadDef(
         "gist500k", "500K x 960 fp32 scaled clipped mixture, Vamana R=64 L=128",
         IndexConfig("vamana", "f32", "l2", 960, 505_000, 64, 128),
@@ -165,6 +174,10 @@ class _Sampler:
             self.n_comp, self.sigma = args
             self.dim_scale = g.uniform(0.1, 1.0, size=d)
             self.centres = g.standard_normal((self.n_comp, d))
+        elif kind == "mix_ip":
+            self.n_comp, self.sigma, self.max_norm = args
+            # centres of different lengths, so that norms vary across components
+            self.centres = g.standard_normal((self.n_comp, d)) * g.uniform(0.5, 1.5, size=(self.n_comp, 1))
         else:
             raise ValueError(kind)
 
@@ -186,6 +199,11 @@ class _Sampler:
         if self.kind == "mix_u8":
             x = np.rint(mu + self.sigma * g.standard_normal((n, d)))
             return np.clip(x, 0, 255).astype(np.uint8), comps
+        if self.kind == "mix_ip":
+            x = mu + self.sigma * g.standard_normal((n, d))
+            nrm = np.linalg.norm(x, axis=1, keepdims=True)
+            x = x * np.minimum(1.0, (0.999 * self.max_norm) / np.maximum(nrm, 1e-30))
+            return x.astype(np.float32), comps
         if self.kind == "mix_norm_drift":
             x = mu + self.sigma * g.standard_normal((n, d))
         elif self.kind == "mix_t_norm":
