@@ -277,7 +277,8 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
             o.search(vecs, spec.k, spec.beam)
             t_q += time.perf_counter() - t0
             n_q += len(vecs)
-        done.append(f"{len(ids) if ids is not None else len(vecs):,} {kind}s")
+        plural = {"insert": "inserts", "delete": "deletes", "search": "searches"}.get(kind, kind)
+        done.append(f"{len(ids) if ids is not None else len(vecs):,} {plural}")
         log(f"cpu baseline: {kind} done, {time.perf_counter() - t0:.1f} s")
     out = {"value": round(n_upd / t_upd, 1) if t_upd > 0 else None, "unit": "updates/s", "cores": threads,
            "kind": "oracle", "search_qps": round(n_q / t_q, 1) if t_q > 0 else None,
