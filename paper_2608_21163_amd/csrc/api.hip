@@ -240,7 +240,8 @@ grand_status ensure_batch(grand_index *h, uint32_t n) {
   dfree(h->v_d); dfree(h->c_d); dfree(h->b_vecs); dfree(h->rchunk); dfree(h->coff);
   dfree(h->cdesc);
   h->bcap = 0;
-  // work chunks of a delete batch: at most (in-edges of the batch) / 64 + 2 per deleted node
+  // work chunks of a delete batch (64 or more positions each): at most
+  // (in-edges of the batch) / 64 + 2 per deleted node, as R <= 64 there
   const size_t nchunk = (size_t)h->p.capacity * h->p.R / 64 + 2 * (size_t)nc + 1;
   const size_t vs = (size_t)nc * h->iters;
   if (dalloc(&h->b_ids, nc) || dalloc(&h->v_ids, vs) || dalloc(&h->v_d, vs) || dalloc(&h->v_n, nc) ||
@@ -515,6 +516,7 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
     a.c_d = h->c_d;
     a.c_out = kr;
     a.c_filter = h->in_batch;
+    a.c_by_id = 1;
     a.ds = h->ds;
     if (grand_status s_ = prep_counting(h, a)) return s_;
     HCHK(h, launch_search(h->kind, h->vc, a, h->stream));
@@ -537,6 +539,7 @@ grand_status vamana_delete(grand_index *h, uint32_t n) {
   r.rofs = h->rofs;
   r.coff = h->coff;
   r.cdesc = h->cdesc;
+  r.cw = repair_chunk_width(h->kind, h->pool, kr, h->p.c);
   r.ds = h->ds;
   // record offsets and work chunks; the record count reaches the host
   // through an event while the repair runs, so the stream never drains

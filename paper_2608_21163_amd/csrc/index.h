@@ -102,6 +102,7 @@ struct SearchArgs {
   float *c_d;
   uint32_t c_out;
   const uint8_t *c_filter;
+  int c_by_id;                // write that set in ascending id order instead (c_out <= 64; c_d untouched)
   // counting runs only: an exact visited bitmap of vis_words words per
   // search (cleared by the caller) replaces the lossy hash
   uint32_t *vis;
@@ -159,7 +160,7 @@ struct RepairArgs {
   const uint32_t *ids;
   uint32_t n;
   const uint8_t *in_batch;
-  const uint32_t *ci;         // n x kr repair candidates (INVALID padded)
+  const uint32_t *ci;         // n x kr repair candidates, ascending ids, INVALID padded at the end
   uint32_t kr;
   const uint32_t *rev_off;
   const uint32_t *rev_src;
@@ -167,7 +168,8 @@ struct RepairArgs {
   uint32_t c;
   const uint32_t *rofs;       // record offsets per deleted node (n + 1)
   const uint32_t *coff;       // work-chunk offsets per deleted node (n + 1)
-  const uint4 *cdesc;         // two words per work chunk: {node, id, first in-edge or INVALID, count}, {record base, chunk index}
+  const uint4 *cdesc;         // two words per work chunk: {node, id, reverse-row start, in-degree}, {record base of the node, first position, positions, chunk index}
+  uint32_t cw;                // positions per work chunk (a multiple of 64)
   size_t rcap;                // record capacity: nothing is written when rofs[n] exceeds it
   uint32_t *rec_t, *rec_s;
   float *rec_d;
@@ -202,6 +204,7 @@ hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, h
 hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s);
 hipError_t launch_repair_map(const RepairArgs &a, uint4 *cdesc, hipStream_t s);
 bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c);
+uint32_t repair_chunk_width(int kind, const PoolView &p, uint32_t kr, uint32_t c);
 
 hipError_t launch_fill_u32(uint32_t *p, uint32_t v, size_t n, hipStream_t s);
 hipError_t launch_fill_u8(uint8_t *p, uint8_t v, size_t n, hipStream_t s);

@@ -27,8 +27,13 @@ __device__ __forceinline__ void rev_row(const RepairArgs &a, uint32_t i, uint32_
   b1 = a.rev_off[r + 1];
 }
 
-// Per deleted node: its record count and its work chunks (64 in-neighbours
-// each, plus one chunk for the out-slots).
+// Work positions of deleted node i: its nin in-neighbours (positions
+// 0 .. nin-1, in reverse-row order) followed by its R out-slots.  Position e
+// owns c+1 records from rofs[i] + e*(c+1) when it is an in-neighbour, c
+// records from rofs[i] + nin*(c+1) + (e-nin)*c when it is an out-slot.
+// A work chunk is a run of at most a.cw positions of one node, so most nodes
+// are one chunk (their C_i tiles loaded once) and a node with a long
+// in-neighbour list is spread over several.
 __global__ void k_repair_plan(RepairArgs a, uint32_t *counts, uint32_t *chunks) {
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
@@ -36,13 +41,12 @@ __global__ void k_repair_plan(RepairArgs a, uint32_t *counts, uint32_t *chunks) 
   rev_row(a, i, a.ids[i], b0, b1);
   const uint32_t nin = b1 - b0;
   counts[i] = nin * (a.c + 1) + a.pool.R * a.c;
-  chunks[i] = (nin + 63) / 64 + 1;
+  chunks[i] = (nin + a.pool.R + a.cw - 1) / a.cw;
 }
 
 // The descriptor of every work chunk j of deleted node i (one wave per
 // node), so that a repair wave starts a chunk with one pair of loads instead
-// of a chain of dependent ones: chunk j < nci covers in-neighbours
-// 64j .. 64j + 63 of p_i, the last chunk its out-slots.
+// of a chain of dependent ones.
 __global__ void k_repair_map(RepairArgs a, uint4 *cdesc) {
   const uint32_t i = blockIdx.x;
   if (i >= a.n) return;
@@ -50,18 +54,26 @@ __global__ void k_repair_map(RepairArgs a, uint4 *cdesc) {
   const uint32_t p = a.ids[i];
   uint32_t b0, b1;
   rev_row(a, i, p, b0, b1);
-  const uint32_t nin = b1 - b0, nci = (nin + 63) / 64, r0 = a.rofs[i], c = a.c;
+  const uint32_t nin = b1 - b0, npos = nin + a.pool.R;
   for (uint32_t q = c0 + threadIdx.x; q < c1; q += blockDim.x) {
-    const uint32_t j = q - c0;
-    if (j < nci) {
-      const uint32_t e0 = j * 64;
-      cdesc[2 * (size_t)q] = make_uint4(i, p, b0 + e0, min(64u, nin - e0));
-      cdesc[2 * (size_t)q + 1] = make_uint4(r0 + e0 * (c + 1), j, 0u, 0u);
-    } else {
-      cdesc[2 * (size_t)q] = make_uint4(i, p, kInvalid, a.pool.R);
-      cdesc[2 * (size_t)q + 1] = make_uint4(r0 + nin * (c + 1), j, 0u, 0u);
-    }
+    const uint32_t j = q - c0, e0 = j * a.cw;
+    cdesc[2 * (size_t)q] = make_uint4(i, p, b0, nin);
+    cdesc[2 * (size_t)q + 1] = make_uint4(a.rofs[i], e0, min(a.cw, npos - e0), j);
   }
+}
+
+// Position e of a chunk's node: its neighbour (INVALID when the slot is
+// empty or the neighbour is in the batch) ...
+__device__ __forceinline__ uint32_t repair_nbr(const RepairArgs &a, uint4 d0, uint32_t e) {
+  const uint32_t p = d0.y, b0 = d0.z, nin = d0.w;
+  const uint32_t x = e < nin ? a.rev_src[b0 + e] : a.pool.adj[(size_t)p * a.pool.R + (e - nin)];
+  return (x != kInvalid && !a.in_batch[x]) ? x : kInvalid;
+}
+// ... and its records: c + 1 from `base` for an in-neighbour (the last one
+// the marker), c for an out-slot.
+__device__ __forceinline__ uint32_t repair_base(const RepairArgs &a, uint4 d0, uint32_t rbase, uint32_t e) {
+  const uint32_t nin = d0.w, c = a.c;
+  return rbase + (e < nin ? e * (c + 1) : nin * (c + 1) + (e - nin) * c);
 }
 
 hipError_t launch_repair_plan(const RepairArgs &a, uint32_t *counts, uint32_t *chunks, hipStream_t s) {
@@ -172,104 +184,160 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
 // uint8 repair on the matrix cores, for rows of 64*NK bytes, k_repair <= 64
 // and c <= K.  The c closest points of C_i of each repaired neighbour x are
 // found in one distance block {neighbours} x C_i (exact int32 from int8
-// MFMA on x ^ 0x80).  Work is split in chunks of at most 64 neighbours of
-// one deleted node (persistent waves over the chunk list), so a node with
-// a long in-neighbour list is spread over many waves.  Per chunk the C_i
-// tiles are the MFMA A operand and 16 neighbours at a time the B operand:
-// lane (g, col) then holds 16 candidate distances of neighbour col, keeps
-// its K smallest (distance, id) keys, and the four lanes of a neighbour
-// merge their lists (two exchanges).
+// MFMA on x ^ 0x80).  Work is split in chunks of at most 64*NPL positions of
+// one deleted node (persistent waves over the chunk list).  Per chunk the
+// C_i tiles are the MFMA A operand and 16 neighbours at a time the B
+// operand: lane (g, col) then holds 16 candidate distances of neighbour col,
+// keeps its K smallest keys, and the four lanes of a neighbour merge their
+// lists (two exchanges).
+//
+// C_i arrives in ascending id order (points first), so a candidate's slot
+// is its rank among the ids and 32-bit keys 64 * Dist + slot order like
+// (Dist, id) (Dist < 2^23 for 128 uint8 dimensions).  A slot without a point
+// gets a key of at least 2^30.  The key of x itself (when x is in C_i) is its
+// slot alone, Dist being 0, which is how it is excluded.
 
-// Sorted list of the K smallest 64-bit keys.
+// Sorted list of the K smallest keys.
 template <int K>
-__device__ __forceinline__ void kl_insert64(uint64_t (&l)[K], uint64_t k) {
+__device__ __forceinline__ void kl_insert32(uint32_t (&l)[K], uint32_t k) {
 #pragma unroll
   for (int j = 0; j < K; j++) {
-    const uint64_t lo = k < l[j] ? k : l[j];
-    k = k < l[j] ? l[j] : k;
+    const uint32_t lo = min(k, l[j]);
+    k = max(k, l[j]);
     l[j] = lo;
   }
 }
 // l <- the K smallest of the two sorted lists l and o (bitonic merge).
 template <int K>
-__device__ __forceinline__ void kl_merge64(uint64_t (&l)[K], const uint64_t (&o)[K]) {
+__device__ __forceinline__ void kl_merge32(uint32_t (&l)[K], const uint32_t (&o)[K]) {
 #pragma unroll
-  for (int j = 0; j < K; j++) l[j] = o[K - 1 - j] < l[j] ? o[K - 1 - j] : l[j];
+  for (int j = 0; j < K; j++) l[j] = min(l[j], o[K - 1 - j]);
 #pragma unroll
   for (int d = K / 2; d > 0; d >>= 1)
 #pragma unroll
     for (int j = 0; j < K; j++)
       if ((j & d) == 0) {
-        const uint64_t x = l[j], y = l[j + d];
-        l[j] = x < y ? x : y;
-        l[j + d] = x < y ? y : x;
+        const uint32_t x = l[j], y = l[j + d];
+        l[j] = min(x, y);
+        l[j + d] = max(x, y);
       }
 }
+constexpr uint32_t kKeyNone = 0x7FFFFFFFu;  // key base of an empty candidate slot
+constexpr uint32_t kKeyValid = 1u << 30;     // keys of points are below
 
-template <int NK, int K>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(K <= 2 ? 5 : 4))) void k_repair_mfma(RepairArgs a) {
-  constexpr int NT = 4;  // C_i tiles (k_repair <= 64)
-  __shared__ uint32_t cidL[64];
-  __shared__ int cnrL[64];
+template <int NK, int K, int NPL>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_repair_mfma(RepairArgs a) {
+  constexpr int NT = 4;        // C_i tiles (k_repair <= 64)
+  constexpr int W = 64 * NPL;  // positions per chunk
+  __shared__ uint32_t cidL[64];                 // C_i ids by slot (ascending, points first)
+  __shared__ __align__(16) uint32_t ckeyL[64];  // 64 * |c'|^2 + slot (kKeyNone when empty)
+  __shared__ uint32_t xL[W];                    // the chunk's neighbours
+  __shared__ uint32_t rxL[W];                   // slot of each neighbour in C_i, or ~0
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const PoolView &P = a.pool;
-  const uint32_t R = P.R;
   const size_t goff = (size_t)g * 16;
-  const int kr = (int)a.kr, nt = (kr + 15) >> 4;
+  const int kr = (int)a.kr;
   const uint32_t c = a.c;
   if ((size_t)a.rofs[a.n] > a.rcap) return;  // the host grows the buffers and launches again
   const uint32_t total = a.coff[a.n];
   unsigned long long evals = 0, rows = 0, recs = 0;
   for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
     const uint4 d0 = a.cdesc[2 * (size_t)q], d1 = a.cdesc[2 * (size_t)q + 1];
-    const uint32_t i = d0.x, p = d0.y, j = d1.y, rbase = d1.x;
-    const bool inbound = d0.z != kInvalid;
-    // this chunk's neighbours, lane e holding neighbour e
-    const int cnt = (int)d0.w;
-    const uint32_t x =
-        ln < cnt ? (inbound ? a.rev_src[d0.z + ln] : P.adj[(size_t)p * R + ln]) : kInvalid;
-    const bool xok = x != kInvalid && !a.in_batch[x];
+    const uint32_t i = d0.x, p = d0.y, rbase = d1.x, e0 = d1.y, j = d1.w;
+    const int cnt = (int)d1.z;
+    // The chunk's C_i ids (A operand slot 16t + col) and its neighbours
+    // (position e0 + e in xL[e]), then the C_i rows and the neighbours'
+    // batch flags: all loads of a level issued together, their addresses
+    // clamped to valid ones and the results selected afterwards.
+    uint32_t cl[NT];
+#pragma unroll
+    for (int t = 0; t < NT; t++) {
+      const int e = 16 * t + col;
+      cl[t] = a.ci[(size_t)i * kr + (e < kr ? e : 0)];
+    }
+    uint32_t xv[NPL];
+#pragma unroll
+    for (int u = 0; u < NPL; u++) {
+      const uint32_t pe = e0 + (uint32_t)(ln + 64 * u);
+      const uint32_t *src = pe < d0.w ? a.rev_src + d0.z + pe : P.adj + (size_t)p * P.R + (pe - d0.w);
+      xv[u] = *((ln + 64 * u) < cnt ? src : P.adj + (size_t)p * P.R);
+    }
+    // C_i rows (bytes 16g + 64kk of candidate 16t + col); slots past
+    // k_repair or without a point hold the deleted node's row
+    uint4 Cr[NT][NK];
+#pragma unroll
+    for (int t = 0; t < NT; t++) {
+      cl[t] = 16 * t + col < kr ? cl[t] : kInvalid;
+      const uint8_t *row = P.vecs + (size_t)(kvalid(cl[t]) ? cl[t] : p) * P.stride + goff;
+#pragma unroll
+      for (int kk = 0; kk < NK; kk++) Cr[t][kk] = ld16(row + (size_t)kk * 64);
+    }
+    uint8_t inb[NPL];
+#pragma unroll
+    for (int u = 0; u < NPL; u++) inb[u] = a.in_batch[xv[u] != kInvalid ? xv[u] : 0u];
+#pragma unroll
+    for (int u = 0; u < NPL; u++) {
+      const int e = ln + 64 * u;
+      xv[u] = (e < cnt && xv[u] != kInvalid && !inb[u]) ? xv[u] : kInvalid;
+      xL[e] = xv[u];
+      rows += (unsigned long long)popc(ballot(xv[u] != kInvalid));
+    }
+    __syncthreads();
     // The rows of neighbours 16s .. 16s+15 (the B operand of step s): lane
     // (g, col) loads bytes 16g + 64kk of neighbour 16s + col.  The loads of
     // step s + 1 are issued before step s is computed.
     uint4 Xn[NK];
     uint32_t xsn;
-    bool xsokn;
     auto load_step = [&](int s) {
-      xsn = __shfl(x, 16 * s + col, 64);
-      xsokn = __shfl((int)xok, 16 * s + col, 64) != 0;
-      const uint8_t *row = P.vecs + (size_t)(xsokn ? xsn : p) * P.stride + goff;
+      xsn = xL[16 * s + col];
+      const uint8_t *row = P.vecs + (size_t)(xsn != kInvalid ? xsn : p) * P.stride + goff;
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) Xn[kk] = ld16(row + (size_t)kk * 64);
     };
     load_step(0);
-    // C_i tiles (A operand: candidate 16t + col, bytes 16g + 64kk)
+    // C_i tiles (A operand) and their squared norms
     v4i Ct[NT][NK];
+    int cnr[NT];
 #pragma unroll
     for (int t = 0; t < NT; t++) {
-      const int e = 16 * t + col;
-      const uint32_t cv = (t < nt && e < kr) ? a.ci[(size_t)i * kr + e] : kInvalid;
-      const uint8_t *row = P.vecs + (size_t)(kvalid(cv) ? cv : p) * P.stride + goff;
       int sq = 0;
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) {
-        Ct[t][kk] = t < nt ? to_i8x16(ld16(row + (size_t)kk * 64)) : v4i{0, 0, 0, 0};
+        Ct[t][kk] = to_i8x16(Cr[t][kk]);
         sq = sq_i8x16(Ct[t][kk], sq);
       }
       sq += (int)xshfl((uint32_t)sq, 16);
       sq += (int)xshfl((uint32_t)sq, 32);
-      if (g == 0) {
-        cidL[e] = cv;
-        cnrL[e] = sq;
-      }
+      cnr[t] = sq;
+      if (g == 0) cidL[16 * t + col] = cl[t];
     }
     __syncthreads();
-    if (j == 0) rows += (unsigned long long)popc(ballot(ln < kr && kvalid(cidL[ln])));
-    rows += (unsigned long long)popc(ballot(xok));
+    const bool mvalid = kvalid(cidL[ln]);
+    const uint32_t nv = (uint32_t)popc(ballot(mvalid));
+    // lane ln holds slot ln's |c'|^2 in cnr[ln >> 4] (every group has it)
+    int mycnr = cnr[0];
+#pragma unroll
+    for (int t = 1; t < NT; t++) mycnr = (ln >> 4) == t ? cnr[t] : mycnr;
+    ckeyL[ln] = mvalid ? (((uint32_t)mycnr << 6) | (uint32_t)ln) : kKeyNone;
+    __syncthreads();
+    // slot of each neighbour in C_i (binary search over the ascending ids)
+#pragma unroll
+    for (int u = 0; u < NPL; u++) {
+      uint32_t lo = 0, hi = nv;
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (cidL[mid] < xv[u]) lo = mid + 1;
+        else hi = mid;
+      }
+      rxL[ln + 64 * u] = (xv[u] != kInvalid && lo < nv && cidL[lo] == xv[u]) ? lo : ~0u;
+    }
+    __syncthreads();
+    if (j == 0) rows += (unsigned long long)nv;
     for (int s = 0; 16 * s < cnt; s++) {
       // neighbours 16s .. 16s+15 as the B operand
       const uint32_t xs = xsn;
-      const bool xsok = xsokn;
+      const bool xsok = xs != kInvalid;
+      const uint32_t rx = rxL[16 * s + col];
       v4i X[NK];
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) X[kk] = to_i8x16(Xn[kk]);
@@ -279,45 +347,54 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(K <= 2 ? 5 :
       for (int kk = 0; kk < NK; kk++) nx = sq_i8x16(X[kk], nx);
       nx += (int)xshfl((uint32_t)nx, 16);
       nx += (int)xshfl((uint32_t)nx, 32);
-      uint64_t l[K];
+      const uint32_t nx64 = (uint32_t)nx << 6;
+      uint32_t l[K];
 #pragma unroll
-      for (int k = 0; k < K; k++) l[k] = ~0ull;
+      for (int k = 0; k < K; k++) l[k] = ~0u;
+      // two tiles' products at a time
 #pragma unroll
-      for (int t = 0; t < NT; t++) {
-        if (t >= nt) break;
-        v4i acc = {0, 0, 0, 0};
+      for (int t0 = 0; t0 < NT; t0 += 2) {
+        v4i acc[2];
 #pragma unroll
-        for (int kk = 0; kk < NK; kk++) acc = mfma_i8(Ct[t][kk], X[kk], acc);
+        for (int u = 0; u < 2; u++) {
+          acc[u] = v4i{0, 0, 0, 0};
 #pragma unroll
-        for (int ii = 0; ii < 4; ii++) {
-          const int e = 16 * t + 4 * g + ii;
-          const uint32_t cv = cidL[e];
-          const bool ok = xsok && kvalid(cv) && cv != xs;
-          const uint32_t d = (uint32_t)(cnrL[e] + nx - 2 * acc[ii]);
-          evals += ok ? 1u : 0u;
-          kl_insert64<K>(l, ok ? (((uint64_t)d << 32) | cv) : ~0ull);
+          for (int kk = 0; kk < NK; kk++) acc[u] = mfma_i8(Ct[t0 + u][kk], X[kk], acc[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; u++) {
+          const uint4 ck = *reinterpret_cast<const uint4 *>(&ckeyL[16 * (t0 + u) + 4 * g]);
+          const uint32_t cks[4] = {ck.x, ck.y, ck.z, ck.w};
+#pragma unroll
+          for (int ii = 0; ii < 4; ii++) {
+            const uint32_t key = cks[ii] + nx64 - ((uint32_t)acc[u][ii] << 7);
+            kl_insert32<K>(l, key == rx ? ~0u : key);
+          }
         }
       }
 #pragma unroll
       for (int o = 16; o < 64; o <<= 1) {
-        uint64_t ot[K];
+        uint32_t ot[K];
 #pragma unroll
-        for (int k = 0; k < K; k++) ot[k] = xshfl64(l[k], o);
-        kl_merge64<K>(l, ot);
+        for (int k = 0; k < K; k++) ot[k] = xshfl(l[k], o);
+        kl_merge32<K>(l, ot);
       }
+      if (g == 0 && xsok) evals += nv - (rx != ~0u ? 1u : 0u);
       // records of neighbour 16s + col: lane g writes entries g, g+4, ...
       const int e = 16 * s + col;
       if (e < cnt) {
+        const uint32_t pos = e0 + (uint32_t)e;
+        const bool inbound = pos < d0.w;
         const uint32_t nrec = inbound ? c + 1 : c;
-        const uint32_t base = rbase + (uint32_t)e * nrec;
+        const uint32_t base = repair_base(a, d0, rbase, pos);
         for (uint32_t k = (uint32_t)g; k < nrec; k += 4) {
-          uint64_t key = ~0ull;
+          uint32_t key = ~0u;
 #pragma unroll
           for (int kk = 0; kk < K; kk++)
             if ((uint32_t)kk == k) key = l[kk];
-          const bool v = key != ~0ull;
-          const uint32_t yi = v ? (uint32_t)key : kInvalid;
-          const float yd = v ? (float)(uint32_t)(key >> 32) : 0.0f;
+          const bool v = key < kKeyValid;
+          const uint32_t yi = v ? cidL[key & 63u] : kInvalid;
+          const float yd = v ? (float)(key >> 6) : 0.0f;
           if (!xsok) {
             a.rec_t[base + k] = kInvalid;
           } else if (inbound) {
@@ -360,6 +437,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(K <= 2 ? 5 :
 // the oracle performs, so the rounded distances are identical.  Each lane
 // keeps its neighbour's K smallest (distance, id) keys; the records and their
 // offsets are those of the uint8 form.
+// Sorted list of the K smallest 64-bit (distance, id) keys.
+template <int K>
+__device__ __forceinline__ void kl_insert64(uint64_t (&l)[K], uint64_t k) {
+#pragma unroll
+  for (int j = 0; j < K; j++) {
+    const uint64_t lo = k < l[j] ? k : l[j];
+    k = k < l[j] ? l[j] : k;
+    l[j] = lo;
+  }
+}
+
 template <int KIND, int K>
 __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
   constexpr int GC = 16, SL = 64;
@@ -376,12 +464,12 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
   unsigned long long evals = 0, rows = 0, recs = 0;
   for (uint32_t q = blockIdx.x; q < total; q += gridDim.x) {
     const uint4 d0 = a.cdesc[2 * (size_t)q], d1 = a.cdesc[2 * (size_t)q + 1];
-    const uint32_t i = d0.x, p = d0.y, j = d1.y, rbase = d1.x;
-    const bool inbound = d0.z != kInvalid;
-    const int cnt = (int)d0.w;
-    const uint32_t x =
-        ln < cnt ? (inbound ? a.rev_src[d0.z + ln] : P.adj[(size_t)p * R + ln]) : kInvalid;
-    const bool xok = x != kInvalid && !a.in_batch[x];
+    const uint32_t i = d0.x, p = d0.y, rbase = d1.x, j = d1.w;
+    const int cnt = (int)d1.z;
+    const uint32_t pos = d1.y + (uint32_t)ln;  // this lane's position
+    const bool inbound = pos < d0.w;
+    const uint32_t x = ln < cnt ? repair_nbr(a, d0, pos) : kInvalid;
+    const bool xok = x != kInvalid;
     cidL[ln] = ln < kr ? a.ci[(size_t)i * kr + ln] : kInvalid;
     __syncthreads();
     if (j == 0) rows += (unsigned long long)popc(ballot(ln < kr && kvalid(cidL[ln])));
@@ -449,7 +537,7 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
     }
     if (ln < cnt) {
       const uint32_t nrec = inbound ? c + 1 : c;
-      const uint32_t base = rbase + (uint32_t)ln * nrec;
+      const uint32_t base = repair_base(a, d0, rbase, pos);
       for (uint32_t k = 0; k < nrec; k++) {
         uint64_t key = ~0ull;
 #pragma unroll
@@ -498,25 +586,38 @@ bool repair_chunked(int kind, const PoolView &p, uint32_t kr, uint32_t c) {
   if (kind == kU8L2) return p.nch == 4 || p.nch == 8;
   return kind == kF32L2 || kind == kF32IP;
 }
+// Positions per work chunk: two per lane on the matrix-core form (a node's
+// in-neighbours and out-slots, about 2R, usually fit one chunk), one per lane
+// on the fp32 form.
+constexpr int kRepairNpl = 2;
+uint32_t repair_chunk_width(int kind, const PoolView &p, uint32_t kr, uint32_t c) {
+  return (kind == kU8L2 && repair_chunked(kind, p, kr, c)) ? 64u * kRepairNpl : 64u;
+}
 
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
   if (kind == kU8L2 && repair_chunked(kind, a.pool, a.kr, a.c)) {
-    // persistent waves over the chunk map: exactly the resident workgroups
-    static const uint32_t r22 = resident_blocks((const void *)k_repair_mfma<2, 2>);
-    static const uint32_t r24 = resident_blocks((const void *)k_repair_mfma<2, 4>);
-    static const uint32_t r12 = resident_blocks((const void *)k_repair_mfma<1, 2>);
-    static const uint32_t r14 = resident_blocks((const void *)k_repair_mfma<1, 4>);
+    // persistent waves over the chunk descriptors: exactly the resident workgroups
+    if (a.cw != 64u * kRepairNpl) return hipErrorInvalidValue;
+    static const uint32_t r22 = resident_blocks((const void *)k_repair_mfma<2, 2, kRepairNpl>);
+    static const uint32_t r24 = resident_blocks((const void *)k_repair_mfma<2, 4, kRepairNpl>);
+    static const uint32_t r12 = resident_blocks((const void *)k_repair_mfma<1, 2, kRepairNpl>);
+    static const uint32_t r14 = resident_blocks((const void *)k_repair_mfma<1, 4, kRepairNpl>);
     if (a.pool.nch == 8) {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<2, 2>), dim3(clamp_resident(grid, r22)), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<2, 4>), dim3(clamp_resident(grid, r24)), dim3(64), 0, st, a);
+      if (a.c <= 2)
+        hipLaunchKernelGGL((k_repair_mfma<2, 2, kRepairNpl>), dim3(clamp_resident(grid, r22)), dim3(64), 0, st, a);
+      else
+        hipLaunchKernelGGL((k_repair_mfma<2, 4, kRepairNpl>), dim3(clamp_resident(grid, r24)), dim3(64), 0, st, a);
     } else {
-      if (a.c <= 2) hipLaunchKernelGGL((k_repair_mfma<1, 2>), dim3(clamp_resident(grid, r12)), dim3(64), 0, st, a);
-      else hipLaunchKernelGGL((k_repair_mfma<1, 4>), dim3(clamp_resident(grid, r14)), dim3(64), 0, st, a);
+      if (a.c <= 2)
+        hipLaunchKernelGGL((k_repair_mfma<1, 2, kRepairNpl>), dim3(clamp_resident(grid, r12)), dim3(64), 0, st, a);
+      else
+        hipLaunchKernelGGL((k_repair_mfma<1, 4, kRepairNpl>), dim3(clamp_resident(grid, r14)), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }
   if (repair_chunked(kind, a.pool, a.kr, a.c)) {
+    if (a.cw != 64u) return hipErrorInvalidValue;
     if (kind == kF32L2) {
       if (a.c <= 2) hipLaunchKernelGGL((k_repair_vec<kF32L2, 2>), dim3(grid), dim3(64), 0, st, a);
       else hipLaunchKernelGGL((k_repair_vec<kF32L2, 4>), dim3(grid), dim3(64), 0, st, a);

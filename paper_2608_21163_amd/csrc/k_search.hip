@@ -181,7 +181,26 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
   }
 
   if (a.v_n && ln == 0) a.v_n[qi] = nv;
-  if (a.c_ids) {
+  if (a.c_ids && a.c_by_id) {
+    // the same set in ascending id order (delete repair candidates), through
+    // LDS and a wave sort by id
+    int base = 0;
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      const uint32_t id = ci[r] & kIdMask;
+      const bool ok = kvalid(ci[r]) && !(a.c_filter && a.c_filter[id]);
+      const uint64_t mm = ballot(ok);
+      const int pos = base + mbcnt(mm);
+      if (ok && pos < (int)a.c_out) mid[pos] = id;
+      base += popc(mm);
+    }
+    __syncthreads();
+    const int m = base < (int)a.c_out ? base : (int)a.c_out;
+    float sd[1] = {ln < m ? 0.0f : finf()};
+    uint32_t si[1] = {ln < m ? mid[ln] : kInvalid};
+    wave_sort<1>(sd, si);
+    if (ln < (int)a.c_out) a.c_ids[(size_t)qi * a.c_out + ln] = si[0];
+  } else if (a.c_ids) {
     int base = 0;
 #pragma unroll
     for (int r = 0; r < NR; r++) {
