@@ -934,6 +934,303 @@ int32_t oracle_delete_batch(void *hv, const uint32_t *ids, uint32_t n) {
 
 /* Search: BeamSearch from the medoid with l = beam and a cap of 2 * beam
  * expansions; the first k of C, padded with INVALID / +inf. */
+/* ------------------------------------------------------------------------
+ * CAGRA graph construction (Section 2.2 on CAGRA; Section 4.2, CAGRA graph
+ * construction): an approximate k-NN graph by NN-Descent, optimised into a
+ * fixed-degree graph by rank-based edge reordering and pruning, then
+ * reverse-edge addition.  The paper names these steps without their
+ * parameters; the readings used here:
+ *
+ * NN-Descent, batch-synchronous.  Node u keeps a list L(u) of K entries
+ * (Dist, v, new flag), ascending by (Dist, v).  L(u) starts from the K
+ * caller-drawn random neighbours init[u] (all new).  One round:
+ *   1. samples: NS(u) = the first S new entries of L(u) in list order, OS(u)
+ *      = the first S old ones; the sampled new entries become old;
+ *   2. reverse samples: RN(v) = the S smallest (Dist, u) over the u with v in
+ *      NS(u) (Dist from u's entry), RO(v) likewise from OS;
+ *   3. local join at every v: Bn = NS(v) u RN(v), Bo = (OS(v) u RO(v)) \ Bn;
+ *      every pair {a, b} of distinct points of Bn, and every (a in Bn, b in
+ *      Bo), gives Dist(a, b); b is proposed to a when (Dist, b) is below the
+ *      key of the last entry of L(a) at the start of the round, and a to b
+ *      likewise;
+ *   4. merge: L(u) <- the K smallest distinct keys of L(u) and u's
+ *      proposals; a proposal whose key is already in L(u) is dropped (the
+ *      entry keeps its flag), the others enter as new.
+ * Rank-based pruning: the rank of v in L(u) is its position.  An edge u -> y
+ * of rank r has a detourable route through z when z has rank rz < r in L(u)
+ * and y has rank ry < r in L(z).  The pruned list P(u) is the R entries with
+ * the fewest detourable routes, ascending by (routes, r).
+ * Reverse edges: y's reverse neighbours are the u with y in P(u), ascending
+ * by (position of y in P(u), u).  The output list of y is the first R/2
+ * entries of P(y), then its reverse neighbours in order, then the rest of
+ * P(y), skipping ids already taken, up to R.
+ * Positions 0..n-1 stand for ids[0..n-1] until the output is written.
+ * ---------------------------------------------------------------------- */
+typedef struct { float d; uint32_t v; uint8_t isnew; } oent;
+
+static int ent_less(const oent *a, const oent *b) { return a->d < b->d || (a->d == b->d && a->v < b->v); }
+static int ent_cmp(const void *pa, const void *pb) {
+    const oent *a = pa, *b = pb;
+    if (ent_less(a, b)) return -1;
+    if (ent_less(b, a)) return 1;
+    return 0;
+}
+static int okey_cmp_u(const void *pa, const void *pb) { return key_cmp(pa, pb); }
+
+/* the S smallest (d, id) keys over all records (t, id, d) with target t, per
+ * target; out: n x S ids, INVALID padded */
+static void smallest_per_target(uint32_t n, uint32_t S, const orec *rec, uint64_t nrec, uint32_t *out) {
+    uint64_t *cnt = calloc((size_t)n + 1, sizeof(uint64_t));
+    for (uint64_t k = 0; k < nrec; k++) cnt[rec[k].t + 1]++;
+    for (uint32_t t = 0; t < n; t++) cnt[t + 1] += cnt[t];
+    okey *all = malloc(sizeof(okey) * (nrec + 1));
+    uint64_t *fill = malloc(sizeof(uint64_t) * ((size_t)n + 1));
+    memcpy(fill, cnt, sizeof(uint64_t) * ((size_t)n + 1));
+    for (uint64_t k = 0; k < nrec; k++) { okey e = { rec[k].d, rec[k].s }; all[fill[rec[k].t]++] = e; }
+    for (uint32_t t = 0; t < n; t++) {
+        uint64_t a = cnt[t], b = cnt[t + 1];
+        qsort(all + a, b - a, sizeof(okey), okey_cmp_u);
+        for (uint32_t j = 0; j < S; j++) out[(size_t)t * S + j] = a + j < b ? all[a + j].id : O_INVALID;
+    }
+    free(cnt); free(all); free(fill);
+}
+
+static int in_list(const uint32_t *a, uint32_t m, uint32_t v) {
+    for (uint32_t i = 0; i < m; i++) if (a[i] == v) return 1;
+    return 0;
+}
+
+/* NN-Descent over positions 0..n-1 (point p is row ids[p] of the index);
+ * L: n x K, the result, ascending per node. */
+static void nn_descent(const oindex *h, const uint32_t *ids, uint32_t n, const uint32_t *init, uint32_t K,
+                       uint32_t iters, uint32_t S, oent *L) {
+    const int nt = nthreads(h);
+    #pragma omp parallel for schedule(static) num_threads(nt)
+    for (uint32_t u = 0; u < n; u++) {
+        oent *l = L + (size_t)u * K;
+        for (uint32_t j = 0; j < K; j++) {
+            uint32_t v = init[(size_t)u * K + j];
+            l[j].d = dist_ids(h, ids[u], ids[v]); l[j].v = v; l[j].isnew = 1;
+        }
+        qsort(l, K, sizeof(oent), ent_cmp);
+    }
+    uint32_t *NS = malloc(sizeof(uint32_t) * (size_t)n * S), *OS = malloc(sizeof(uint32_t) * (size_t)n * S);
+    uint32_t *RN = malloc(sizeof(uint32_t) * (size_t)n * S), *RO = malloc(sizeof(uint32_t) * (size_t)n * S);
+    orec *rn = malloc(sizeof(orec) * ((size_t)n * S + 1)), *ro = malloc(sizeof(orec) * ((size_t)n * S + 1));
+    for (uint32_t it = 0; it < iters; it++) {
+        /* 1. samples */
+        uint64_t nrn = 0, nro = 0;
+        for (uint32_t u = 0; u < n; u++) {
+            oent *l = L + (size_t)u * K;
+            uint32_t cn = 0, co = 0;
+            for (uint32_t j = 0; j < K; j++) {
+                if (l[j].isnew) {
+                    if (cn < S) {
+                        NS[(size_t)u * S + cn++] = l[j].v;
+                        orec r = { l[j].v, u, l[j].d }; rn[nrn++] = r;
+                        l[j].isnew = 0;
+                    }
+                } else if (co < S) {
+                    OS[(size_t)u * S + co++] = l[j].v;
+                    orec r = { l[j].v, u, l[j].d }; ro[nro++] = r;
+                }
+            }
+            for (; cn < S; cn++) NS[(size_t)u * S + cn] = O_INVALID;
+            for (; co < S; co++) OS[(size_t)u * S + co] = O_INVALID;
+        }
+        /* 2. reverse samples */
+        smallest_per_target(n, S, rn, nrn, RN);
+        smallest_per_target(n, S, ro, nro, RO);
+        /* 3. local joins: proposals against the keys of the round's start */
+        okey *worst = malloc(sizeof(okey) * n);
+        for (uint32_t u = 0; u < n; u++) { worst[u].d = L[(size_t)u * K + K - 1].d; worst[u].id = L[(size_t)u * K + K - 1].v; }
+        uint64_t cap = 1024, np = 0;
+        orec *prop = malloc(sizeof(orec) * cap);
+        for (uint32_t v = 0; v < n; v++) {
+            uint32_t bn[64], bo[64], nb = 0, no = 0;
+            for (uint32_t j = 0; j < S; j++) {
+                uint32_t x = NS[(size_t)v * S + j];
+                if (x != O_INVALID && !in_list(bn, nb, x)) bn[nb++] = x;
+                x = RN[(size_t)v * S + j];
+                if (x != O_INVALID && !in_list(bn, nb, x)) bn[nb++] = x;
+            }
+            for (uint32_t j = 0; j < S; j++) {
+                uint32_t x = OS[(size_t)v * S + j];
+                if (x != O_INVALID && !in_list(bn, nb, x) && !in_list(bo, no, x)) bo[no++] = x;
+                x = RO[(size_t)v * S + j];
+                if (x != O_INVALID && !in_list(bn, nb, x) && !in_list(bo, no, x)) bo[no++] = x;
+            }
+            for (uint32_t i = 0; i < nb; i++) {
+                for (uint32_t j = 0; j < nb + no; j++) {
+                    if (j < nb && j <= i) continue;             /* unordered pairs within Bn */
+                    uint32_t a = bn[i], b = j < nb ? bn[j] : bo[j - nb];
+                    float d = dist_ids(h, ids[a], ids[b]);
+                    okey kb = { d, b }, ka = { d, a };
+                    if (np + 2 > cap) { cap *= 2; prop = realloc(prop, sizeof(orec) * cap); }
+                    if (key_less(kb, worst[a])) { orec r = { a, b, d }; prop[np++] = r; }
+                    if (key_less(ka, worst[b])) { orec r = { b, a, d }; prop[np++] = r; }
+                }
+            }
+        }
+        free(worst);
+        /* 4. merge, per node, its list with its proposals in (Dist, id) order */
+        qsort(prop, np, sizeof(orec), rec_cmp);
+        uint64_t k0 = 0;
+        oent *m = malloc(sizeof(oent) * 2 * K);
+        while (k0 < np) {
+            uint64_t k1 = k0;
+            while (k1 < np && prop[k1].t == prop[k0].t) k1++;
+            oent *l = L + (size_t)prop[k0].t * K;
+            uint32_t nm = 0, i = 0;
+            uint64_t k = k0;
+            while (nm < K && (i < K || k < k1)) {
+                oent c;
+                oent pk = { k < k1 ? prop[k].d : 0.0f, k < k1 ? prop[k].s : 0u, 1 };
+                if (k >= k1 || (i < K && !ent_less(&pk, &l[i]))) c = l[i++];   /* ties: the entry first */
+                else { c = pk; k++; }
+                if (nm > 0 && m[nm - 1].d == c.d && m[nm - 1].v == c.v) continue;  /* a repeat: the earlier stays */
+                m[nm++] = c;
+            }
+            memcpy(l, m, sizeof(oent) * K);
+            k0 = k1;
+        }
+        free(m);
+        free(prop);
+    }
+    free(NS); free(OS); free(RN); free(RO); free(rn); free(ro);
+}
+
+/* Rank-based pruning of the K-lists `lists` (positions, each ascending) to
+ * P (n x R): per node, the R entries with the fewest detourable routes,
+ * ascending by (routes, rank). */
+static void rank_prune(const uint32_t *lists, uint32_t n, uint32_t K, uint32_t R, uint32_t *P, int nt) {
+    #pragma omp parallel num_threads(nt)
+    {
+        uint32_t *rank = malloc(sizeof(uint32_t) * n);
+        for (uint32_t i = 0; i < n; i++) rank[i] = O_INVALID;
+        okey *cnt = malloc(sizeof(okey) * K);   /* (routes, rank) */
+        #pragma omp for schedule(dynamic, 64)
+        for (uint32_t u = 0; u < n; u++) {
+            const uint32_t *l = lists + (size_t)u * K;
+            for (uint32_t r = 0; r < K; r++) rank[l[r]] = r;
+            uint32_t routes[128] = { 0 };
+            for (uint32_t rz = 0; rz < K; rz++) {
+                const uint32_t *lz = lists + (size_t)l[rz] * K;
+                for (uint32_t rzy = 0; rzy < K; rzy++) {
+                    uint32_t ry = rank[lz[rzy]];
+                    if (ry != O_INVALID && rz < ry && rzy < ry) routes[ry]++;
+                }
+            }
+            for (uint32_t r = 0; r < K; r++) { cnt[r].d = (float)routes[r]; cnt[r].id = r; }
+            qsort(cnt, K, sizeof(okey), okey_cmp_u);
+            for (uint32_t t = 0; t < R; t++) P[(size_t)u * R + t] = l[cnt[t].id];
+            for (uint32_t r = 0; r < K; r++) rank[l[r]] = O_INVALID;
+        }
+        free(rank); free(cnt);
+    }
+}
+
+/* Reverse edges merged into the pruned lists P (n x R) -> out (n x R, with
+ * the list lengths in nout). */
+static void reverse_merge(const uint32_t *P, uint32_t n, uint32_t R, uint32_t *out, uint32_t *nout, int nt) {
+    orec *rv = malloc(sizeof(orec) * ((size_t)n * R + 1));
+    uint64_t nrv = 0;
+    for (uint32_t u = 0; u < n; u++)
+        for (uint32_t t = 0; t < R; t++) { orec r = { P[(size_t)u * R + t], u, (float)t }; rv[nrv++] = r; }
+    qsort(rv, nrv, sizeof(orec), rec_cmp);          /* (target, position, source) */
+    uint64_t *rs = calloc((size_t)n + 1, sizeof(uint64_t));
+    for (uint64_t k = 0; k < nrv; k++) rs[rv[k].t + 1]++;
+    for (uint32_t t = 0; t < n; t++) rs[t + 1] += rs[t];
+    const uint32_t half = R / 2;
+    #pragma omp parallel for schedule(static) num_threads(nt)
+    for (uint32_t y = 0; y < n; y++) {
+        uint32_t *o = out + (size_t)y * R, no = 0;
+        const uint32_t *py = P + (size_t)y * R;
+        for (uint32_t t = 0; t < half; t++) o[no++] = py[t];
+        for (uint64_t k = rs[y]; k < rs[y + 1] && no < R; k++)
+            if (!in_list(o, no, rv[k].s)) o[no++] = rv[k].s;
+        for (uint32_t t = half; t < R && no < R; t++)
+            if (!in_list(o, no, py[t])) o[no++] = py[t];
+        nout[y] = no;
+        for (uint32_t t = no; t < R; t++) o[t] = O_INVALID;
+    }
+    free(rv); free(rs);
+}
+
+static int check_init(oindex *h, const uint32_t *init, uint32_t n, uint32_t K) {
+    for (uint32_t u = 0; u < n; u++)
+        for (uint32_t j = 0; j < K; j++) {
+            uint32_t v = init[(size_t)u * K + j];
+            if (v >= n || v == u || in_list(init + (size_t)u * K, j, v)) {
+                snprintf(h->err, sizeof h->err, "initial list of position %u is not K distinct other positions", u);
+                return O_E_ARG;
+            }
+        }
+    return O_OK;
+}
+
+int32_t oracle_build_cagra(void *hv, const void *vecs, const uint32_t *ids, uint32_t n, const uint32_t *init,
+                           uint32_t K, uint32_t iters, uint32_t S) {
+    oindex *h = hv;
+    const uint32_t R = h->cfg.R;
+    if (h->cfg.algo != O_CAGRA) { snprintf(h->err, sizeof h->err, "graph construction is for the CAGRA variant"); return O_E_ARG; }
+    if (h->n_active != 0) { snprintf(h->err, sizeof h->err, "graph construction needs an empty index"); return O_E_ARG; }
+    if (K < R || K > 128 || n <= K || S == 0 || S > 32) {
+        snprintf(h->err, sizeof h->err, "need R <= K <= 128, K < n and 1 <= S <= 32");
+        return O_E_ARG;
+    }
+    int rc = validate_ids(h, ids, n, 0);
+    if (rc == O_OK) rc = validate_vectors(h, vecs, n, 0);
+    if (rc == O_OK) rc = check_init(h, init, n, K);
+    if (rc != O_OK) return rc;
+    stage(h, vecs, ids, n);
+    const int nt = nthreads(h);
+    oent *L = malloc(sizeof(oent) * (size_t)n * K);
+    nn_descent(h, ids, n, init, K, iters, S, L);
+    uint32_t *lists = malloc(sizeof(uint32_t) * (size_t)n * K);
+    for (size_t i = 0; i < (size_t)n * K; i++) lists[i] = L[i].v;
+    free(L);
+    uint32_t *P = malloc(sizeof(uint32_t) * (size_t)n * R), *out = malloc(sizeof(uint32_t) * (size_t)n * R);
+    uint32_t *nout = malloc(sizeof(uint32_t) * n);
+    rank_prune(lists, n, K, R, P, nt);
+    reverse_merge(P, n, R, out, nout, nt);
+    for (uint32_t y = 0; y < n; y++) {
+        uint32_t *row = h->adj + (size_t)ids[y] * R;
+        for (uint32_t t = 0; t < R; t++) row[t] = t < nout[y] ? ids[out[(size_t)y * R + t]] : O_INVALID;
+        h->deg[ids[y]] = nout[y];
+    }
+    free(lists); free(P); free(out); free(nout);
+    h->medoid = compute_medoid(h);
+    return O_OK;
+}
+
+/* The three steps on their own (positions, no index state changed). */
+int32_t oracle_nn_descent(void *hv, const void *vecs, uint32_t n, const uint32_t *init, uint32_t K, uint32_t iters,
+                          uint32_t S, uint32_t *out_ids, float *out_d) {
+    oindex *h = hv;
+    if (K == 0 || K > 128 || n <= K || S == 0 || S > 32 || n > h->cfg.capacity || h->n_active != 0) {
+        snprintf(h->err, sizeof h->err, "bad NN-Descent arguments");
+        return O_E_ARG;
+    }
+    if (check_init(h, init, n, K) != O_OK) return O_E_ARG;
+    uint32_t *ids = malloc(sizeof(uint32_t) * n);
+    for (uint32_t i = 0; i < n; i++) ids[i] = i;
+    size_t row = (size_t)h->cfg.dim * h->esize;
+    for (uint32_t i = 0; i < n; i++)
+        store_row(h, (const uint8_t *)vecs + (size_t)i * row, h->vecs + (size_t)i * h->sdim * h->esize, 0);
+    oent *L = malloc(sizeof(oent) * (size_t)n * K);
+    nn_descent(h, ids, n, init, K, iters, S, L);
+    for (size_t i = 0; i < (size_t)n * K; i++) { out_ids[i] = L[i].v; out_d[i] = L[i].d; }
+    free(L); free(ids);
+    return O_OK;
+}
+void oracle_rank_prune(const uint32_t *lists, uint32_t n, uint32_t K, uint32_t R, uint32_t *P) {
+    rank_prune(lists, n, K, R, P, 1);
+}
+void oracle_reverse_merge(const uint32_t *P, uint32_t n, uint32_t R, uint32_t *out, uint32_t *nout) {
+    reverse_merge(P, n, R, out, nout, 1);
+}
+
 int32_t oracle_search(void *hv, const void *queries, uint32_t nq, uint32_t k, uint32_t beam,
                       uint32_t *out_ids, float *out_d) {
     oindex *h = hv;

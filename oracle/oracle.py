@@ -71,6 +71,14 @@ def _load():
     lib.oracle_medoid.argtypes = [P]
     lib.oracle_reverse_csr.restype = U64
     lib.oracle_reverse_csr.argtypes = [P, P, U32, U32, P, P]
+    lib.oracle_build_cagra.restype = I32
+    lib.oracle_build_cagra.argtypes = [P, P, P, U32, P, U32, U32, U32]
+    lib.oracle_nn_descent.restype = I32
+    lib.oracle_nn_descent.argtypes = [P, P, U32, P, U32, U32, U32, P, P]
+    lib.oracle_rank_prune.restype = None
+    lib.oracle_rank_prune.argtypes = [P, U32, U32, U32, P]
+    lib.oracle_reverse_merge.restype = None
+    lib.oracle_reverse_merge.argtypes = [P, U32, U32, P, P]
     lib.oracle_bruteforce_knn.restype = I32
     lib.oracle_bruteforce_knn.argtypes = [P, P, U32, U32, P, P]
     _lib = lib
@@ -93,6 +101,25 @@ class _Stats(ctypes.Structure):
 
 def _ptr(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data
+
+
+def rank_prune(lists: np.ndarray, R: int) -> np.ndarray:
+    """CAGRA rank-based pruning of ascending k-NN lists (n x K positions)."""
+    lists = np.ascontiguousarray(lists, np.uint32)
+    n, K = lists.shape
+    out = np.empty((n, R), np.uint32)
+    _load().oracle_rank_prune(_ptr(lists), n, K, R, _ptr(out))
+    return out
+
+
+def reverse_merge(P: np.ndarray):
+    """CAGRA reverse-edge merge of pruned lists (n x R positions): (lists, lengths)."""
+    P = np.ascontiguousarray(P, np.uint32)
+    n, R = P.shape
+    out = np.empty((n, R), np.uint32)
+    nout = np.empty(n, np.uint32)
+    _load().oracle_reverse_merge(_ptr(P), n, R, _ptr(out), _ptr(nout))
+    return out, nout
 
 
 def reverse_csr(adj: np.ndarray, active: np.ndarray):
@@ -147,6 +174,29 @@ class Oracle:
         ids = np.ascontiguousarray(ids, np.uint32)
         vecs = self._vecs(vecs)
         return self.lib.oracle_insert_batch(self.h, _ptr(vecs), _ptr(ids), ids.size)
+
+    def build_cagra(self, ids, vecs, init, knn: int, iters: int, sample: int) -> int:
+        """CAGRA graph construction over an empty CAGRA index (NN-Descent,
+        rank-based pruning, reverse edges); init is n x knn batch positions."""
+        ids = np.ascontiguousarray(ids, np.uint32)
+        vecs = self._vecs(vecs)
+        init = np.ascontiguousarray(init, np.uint32)
+        assert init.shape == (ids.size, knn)
+        return self.lib.oracle_build_cagra(self.h, _ptr(vecs), _ptr(ids), ids.size, _ptr(init), knn, iters, sample)
+
+    def nn_descent(self, vecs, init, knn: int, iters: int, sample: int):
+        """NN-Descent alone over positions 0..n-1 (an empty index's rows 0..n-1
+        are overwritten); returns (ids, dists), each n x knn, ascending."""
+        vecs = self._vecs(vecs)
+        init = np.ascontiguousarray(init, np.uint32)
+        n = vecs.shape[0]
+        assert init.shape == (n, knn)
+        ids = np.empty((n, knn), np.uint32)
+        d = np.empty((n, knn), np.float32)
+        rc = self.lib.oracle_nn_descent(self.h, _ptr(vecs), n, _ptr(init), knn, iters, sample, _ptr(ids), _ptr(d))
+        if rc != 0:
+            raise ValueError(self.last_error())
+        return ids, d
 
     def delete(self, ids) -> int:
         ids = np.ascontiguousarray(ids, np.uint32)

@@ -491,3 +491,27 @@ class PatternStream:
                     yield self._insert(pts)
                 else:
                     yield self._search()
+
+
+_P_INIT = 9
+
+
+def cagra_init_lists(n: int, knn: int, seed: int = 0) -> np.ndarray:
+    """Random initial neighbour lists for the CAGRA graph construction's
+    NN-Descent: row u holds ``knn`` distinct positions in [0, n) other than u,
+    drawn uniformly.  These are the random numbers the construction starts
+    from; both the GPU library and the oracle take them as input."""
+    if not 0 < knn < n:
+        raise ValueError("need 0 < knn < n")
+    g = _rng(seed, _P_INIT)
+    off = np.sort(g.integers(0, n - 1, size=(n, knn), dtype=np.int64), axis=1)
+    while True:  # redraw repeated offsets until every row is distinct
+        dup = np.zeros_like(off, dtype=bool)
+        dup[:, 1:] = off[:, 1:] == off[:, :-1]
+        k = int(dup.sum())
+        if k == 0:
+            break
+        off[dup] = g.integers(0, n - 1, size=k, dtype=np.int64)
+        off.sort(axis=1)
+    u = np.arange(n, dtype=np.int64)[:, None]
+    return ((u + 1 + off) % n).astype(np.uint32)
