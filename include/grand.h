@@ -125,6 +125,32 @@ grand_status grand_set_stream(grand_index *h, void *stream);
  * with GRAND_MIPS a vector whose norm exceeds mips_norm). */
 grand_status grand_insert_batch(grand_index *h, const void *vecs, const uint32_t *ids, uint32_t n);
 
+/* CAGRA graph construction (Section 2.2 on CAGRA; Section 4.2, CAGRA graph
+ * construction): builds the fixed-degree graph of an empty GRAND_CAGRA
+ * index over n points in one call, instead of growing it by batches.
+ *   1. an approximate k-NN graph of degree knn by NN-Descent, `iters` rounds
+ *      with `sample` new and `sample` old entries sampled per list per round
+ *      (local joins between the sampled neighbours and reverse neighbours;
+ *      every round reads the lists of the round's start);
+ *   2. rank-based pruning: per node, the R neighbours with the fewest
+ *      detourable routes (a route u -> z -> y with both ranks below the rank
+ *      of y in u's list), by (routes, rank);
+ *   3. reverse edges: the output list of y is the first R/2 of its pruned
+ *      list, then the nodes whose pruned list holds y (ascending by that
+ *      position, then id), then the rest of its pruned list, up to R.
+ * vecs, ids: as for grand_insert_batch (n distinct inactive ids).
+ * init: n x knn row-major batch positions (host or device): row p holds knn
+ *   distinct positions in [0, n) other than p, the random initial neighbours
+ *   (drawn by the caller, so that a run can be reproduced).
+ * Requires R <= knn <= 128, knn < n, 1 <= sample <= 32, and
+ * n * (12 sample^2 - 2 sample) < 2^32 (proposals of one round).  The medoid
+ * is computed at the end.  Argument and validation errors change nothing.
+ * Errors: GRAND_E_ARG
+ * (wrong variant, index not empty, bad sizes or initial lists, non-finite
+ * element), GRAND_E_ID, GRAND_E_CAPACITY, GRAND_E_OOM. */
+grand_status grand_build_cagra(grand_index *h, const void *vecs, const uint32_t *ids, uint32_t n,
+                               const uint32_t *init, uint32_t knn, uint32_t iters, uint32_t sample);
+
 /* BatchDelete (Alg. 3; Vamana Alg. 6; CAGRA Alg. 8), in place.
  * ids: n distinct active ids.  In-neighbours of the deleted nodes are found
  * exactly from a reverse graph built on the GPU for this batch; their lists

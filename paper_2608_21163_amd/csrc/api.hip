@@ -223,6 +223,9 @@ grand_status read_validation(grand_index *h) {
     case kErrRepeat: snprintf(buf, sizeof buf, "id %u is repeated in the batch", id); return fail(h, GRAND_E_ID, buf);
     case kErrState: snprintf(buf, sizeof buf, "id %u is in the wrong active state", id); return fail(h, GRAND_E_ID, buf);
     case kErrNorm: snprintf(buf, sizeof buf, "row %u has a norm above mips_norm", id); return fail(h, GRAND_E_ARG, buf);
+    case kErrInit:
+      snprintf(buf, sizeof buf, "initial list of position %u is not knn distinct other positions below n", id);
+      return fail(h, GRAND_E_ARG, buf);
     default: snprintf(buf, sizeof buf, "row %u holds a non-finite element", id); return fail(h, GRAND_E_ARG, buf);
   }
 }
@@ -844,6 +847,138 @@ grand_status grand_insert_batch(grand_index *h, const void *vecs, const uint32_t
   if (n0 == 0 && (s = run_medoid(h, nullptr, 1)) != GRAND_OK) return s;
   h->st.inserted += n;
   return finish(h);
+}
+
+// Device buffers of one graph construction; freed when the call ends.
+struct BuildBufs {
+  uint32_t *init = nullptr, *lid = nullptr, *nid = nullptr, *ns = nullptr, *os = nullptr, *cand = nullptr,
+           *cnb = nullptr, *pcnt = nullptr, *poff = nullptr, *prn = nullptr;
+  float *ld = nullptr, *nd = nullptr;
+  ~BuildBufs() {
+    dfree(init); dfree(lid); dfree(nid); dfree(ns); dfree(os); dfree(cand); dfree(cnb); dfree(pcnt);
+    dfree(poff); dfree(prn); dfree(ld); dfree(nd);
+  }
+};
+
+grand_status grand_build_cagra(grand_index *h, const void *vecs, const uint32_t *ids, uint32_t n,
+                               const uint32_t *init, uint32_t knn, uint32_t iters, uint32_t sample) {
+  grand_status s = check_usable(h);
+  if (s != GRAND_OK) return s;
+  if (!vecs || !ids || !init) return fail(h, GRAND_E_ARG, "null argument");
+  if (h->p.algo != GRAND_CAGRA) return fail(h, GRAND_E_ARG, "graph construction is for the CAGRA variant");
+  if (h->n_active != 0) return fail(h, GRAND_E_ARG, "graph construction needs an empty index");
+  const uint32_t R = h->p.R, K = knn, S = sample;
+  if (K < R || K > 128 || n <= K || S == 0 || S > 32)
+    return fail(h, GRAND_E_ARG, "need R <= knn <= 128, knn < n and 1 <= sample <= 32");
+  if (n > h->p.capacity) return fail(h, GRAND_E_CAPACITY, "more points than the capacity");
+  const uint64_t max_prop = 12ull * S * S - 2ull * S;  // proposals of one node in one round
+  if ((uint64_t)n * max_prop >= (1ull << 32)) return fail(h, GRAND_E_CAPACITY, "sample too large for n points");
+  HCHK(h, hipSetDevice(h->p.device));
+  if ((s = ensure_batch(h, n)) != GRAND_OK) return s;
+  BuildBufs b;
+  const size_t nk = (size_t)n * K, nsz = (size_t)n * S;
+  if (dalloc(&b.init, nk) || dalloc(&b.lid, nk) || dalloc(&b.nid, nk) || dalloc(&b.ld, nk) || dalloc(&b.nd, nk) ||
+      dalloc(&b.ns, nsz) || dalloc(&b.os, nsz) || dalloc(&b.cand, 4 * nsz) || dalloc(&b.cnb, n) ||
+      dalloc(&b.pcnt, n) || dalloc(&b.poff, (size_t)n + 1) || dalloc(&b.prn, (size_t)n * R)) {
+    (void)hipGetLastError();
+    return fail(h, GRAND_E_OOM, "device allocation of the construction buffers failed");
+  }
+  // the record buffers the index holds for its batches, grown to the sample
+  // and reverse-edge records if needed; the proposals of a round are written
+  // in chunks of nodes that fit them
+  const size_t need = std::max<size_t>(std::max<size_t>((size_t)n * 2 * S, (size_t)n * R), max_prop);
+  if ((s = ensure_records(h, need)) != GRAND_OK) return s;
+  BuildArgs a{};
+  a.pool = h->pool;
+  a.ids = h->b_ids;
+  a.n = n;
+  a.K = K;
+  a.S = S;
+  a.R = R;
+  a.init = b.init;
+  a.lid = b.lid;
+  a.ld = b.ld;
+  a.nid = b.nid;
+  a.nd = b.nd;
+  a.ns = b.ns;
+  a.os = b.os;
+  a.cand = b.cand;
+  a.cnb = b.cnb;
+  a.pcnt = b.pcnt;
+  a.poff = b.poff;
+  a.rec_t = h->rec_t;
+  a.rec_s = h->rec_s;
+  a.rec_d = h->rec_d;
+  a.goff = h->off;
+  a.gsrc = h->gsrc;
+  a.gd = h->gd;
+  a.dirty = h->dirty;
+  a.n_dirty = &h->ds->n_dirty;
+  a.prn = b.prn;
+  a.ds = h->ds;
+  {
+    Phase ph(h, GRAND_PH_VALIDATE);
+    HCHK(h, hipMemcpyAsync(h->b_ids, ids, (size_t)n * 4, hipMemcpyDefault, h->stream));
+    HCHK(h, hipMemcpyAsync(b.init, init, nk * 4, hipMemcpyDefault, h->stream));
+    if ((s = stage_rows(h, h->b_vecs, vecs, n)) != GRAND_OK) return s;
+    if ((s = clear_errors(h)) != GRAND_OK) return s;
+    h->epoch++;
+    HCHK(h, launch_validate_ids(h->b_ids, n, h->p.capacity, h->pool.active, h->mark, h->epoch, 0, h->ds, h->stream));
+    if (h->p.dtype == GRAND_F32)
+      HCHK(h, launch_check_finite(h->b_vecs, n, h->stride, h->p.dim, h->ds, h->stream));
+    HCHK(h, launch_build_check(a, h->stream));
+  }
+  if ((s = read_validation(h)) != GRAND_OK) {
+    (void)finish(h);
+    return s;
+  }
+  {
+    Phase ph(h, GRAND_PH_STAGE);
+    HCHK(h, launch_stage(h->pool, h->b_vecs, h->b_ids, n, h->bidx, h->stream));
+  }
+  h->n_active = n;
+  HCHK(h, launch_build_init(h->kind, a, h->stream));
+  std::vector<uint32_t> poff((size_t)n + 1);
+  for (uint32_t it = 0; it < iters; it++) {
+    // samples, recorded at their targets and grouped
+    HCHK(h, launch_build_sample(a, h->stream));
+    if ((s = run_group(h, (size_t)n * 2 * S)) != GRAND_OK) return s;
+    HCHK(h, launch_build_cands(a, h->stream));
+    HCHK(h, hipMemcpyAsync(a.nid, a.lid, nk * 4, hipMemcpyDeviceToDevice, h->stream));
+    HCHK(h, hipMemcpyAsync(a.nd, a.ld, nk * 4, hipMemcpyDeviceToDevice, h->stream));
+    // proposals per node, then written and merged chunk by chunk
+    a.v0 = 0;
+    a.v1 = n;
+    HCHK(h, launch_build_join(h->kind, a, false, h->stream));
+    HCHK(h, launch_scan(b.pcnt, b.poff, n, h->scan_tmp, h->stream));
+    HCHK(h, hipMemcpyAsync(poff.data(), b.poff, poff.size() * 4, hipMemcpyDeviceToHost, h->stream));
+    HCHK(h, hipStreamSynchronize(h->stream));
+    uint32_t v0 = 0;
+    while (v0 < n) {
+      uint32_t v1 = v0 + 1;
+      while (v1 < n && (size_t)(poff[v1 + 1] - poff[v0]) <= h->rcap) v1++;
+      const size_t nrec = poff[v1] - poff[v0];  // at most rcap: one node proposes at most max_prop
+      if (nrec) {
+        a.v0 = v0;
+        a.v1 = v1;
+        HCHK(h, launch_build_join(h->kind, a, true, h->stream));
+        if ((s = run_group(h, nrec)) != GRAND_OK) return s;
+        HCHK(h, launch_build_merge(a, persistent_grid(v1 - v0 + n / 8), h->stream));
+      }
+      v0 = v1;
+    }
+    std::swap(a.lid, a.nid);
+    std::swap(a.ld, a.nd);
+  }
+  // rank-based pruning, then the reverse edges
+  HCHK(h, launch_build_rank(a, h->stream));
+  if ((s = run_group(h, (size_t)n * R)) != GRAND_OK) return s;
+  HCHK(h, launch_build_out(a, h->stream));
+  if ((s = run_medoid(h, nullptr, 1)) != GRAND_OK) return s;
+  h->st.inserted += n;
+  s = finish(h);
+  HCHK(h, hipStreamSynchronize(h->stream));  // the construction buffers are freed on return
+  return s;
 }
 
 grand_status grand_delete_batch(grand_index *h, const uint32_t *ids, uint32_t n) {

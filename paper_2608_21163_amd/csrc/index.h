@@ -63,7 +63,7 @@ __device__ __forceinline__ void stat_add(DevScalars *ds, int id, unsigned long l
   if (v) atomicAdd(&ds->stat[(size_t)(blockIdx.x % kStatSlots) * kStatWords + id], v);
 }
 
-enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4, kErrNorm = 5 };
+enum { kErrRange = 1, kErrRepeat = 2, kErrState = 3, kErrNonFinite = 4, kErrNorm = 5, kErrInit = 6 };
 
 // Vector-layout classes: lanes per row (LPV) and 16-byte chunks per lane
 // (CPL) of the distance machinery, chosen from the padded row length.
@@ -175,6 +175,41 @@ struct RepairArgs {
   float *rec_d;
   DevScalars *ds;
 };
+
+// CAGRA graph construction (k_build.hip); positions 0..n-1 stand for pool
+// rows ids[0..n-1].
+struct BuildArgs {
+  PoolView pool;
+  const uint32_t *ids;        // position -> pool id
+  uint32_t n, K, S, R;        // points, k-NN degree, sample size, output degree
+  const uint32_t *init;       // n x K initial positions
+  uint32_t *lid;              // n x K lists, ascending by (Dist, position); top bit: not yet sampled
+  float *ld;
+  uint32_t *nid;              // the lists the merges of a round write
+  float *nd;
+  uint32_t *ns, *os;          // n x S new and old samples
+  uint32_t *cand, *cnb;       // n x 4S join candidates (Bn, then Bo) and nb | no << 16
+  uint32_t *pcnt;             // proposals per node
+  const uint32_t *poff;       // their exclusive scan (n + 1)
+  uint32_t v0, v1;            // nodes of one join chunk
+  int stage_rows;             // join: candidate rows staged in dynamic LDS
+  uint32_t *rec_t, *rec_s;    // records (target, source, key)
+  float *rec_d;
+  const uint32_t *goff, *gsrc;  // grouped records (offsets per target, sources, keys)
+  const float *gd;
+  const uint32_t *dirty;      // targets with records and their number (device)
+  const uint32_t *n_dirty;
+  uint32_t *prn;              // n x R pruned lists
+  DevScalars *ds;
+};
+hipError_t launch_build_check(const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_init(int kind, const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_sample(const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_cands(const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_join(int kind, const BuildArgs &a, bool write, hipStream_t s);
+hipError_t launch_build_merge(const BuildArgs &a, uint32_t grid, hipStream_t s);
+hipError_t launch_build_rank(const BuildArgs &a, hipStream_t s);
+hipError_t launch_build_out(const BuildArgs &a, hipStream_t s);
 
 struct CagraArgs {
   PoolView pool;

@@ -31,7 +31,7 @@ PHASES = ["validate", "stage", "search_insert", "bootstrap", "prune_fwd", "group
           "reverse", "repair", "clear", "medoid", "search_query", "cagra_detour", "cagra_pickone"]
 
 EXPORTED = ["grand_default_params", "grand_create", "grand_destroy", "grand_set_stream", "grand_insert_batch",
-            "grand_delete_batch", "grand_search", "grand_search_static", "grand_count_in_edges", "grand_reader_create",
+            "grand_build_cagra", "grand_delete_batch", "grand_search", "grand_search_static", "grand_count_in_edges", "grand_reader_create",
             "grand_reader_search", "grand_reader_destroy", "grand_reader_last_error", "grand_export_graph", "grand_import_graph", "grand_set_timing",
             "grand_set_counting", "grand_stats", "grand_reset_stats", "grand_last_error"]
 
@@ -92,6 +92,8 @@ def load_library(path: str = LIB_PATH):
     lib.grand_destroy.argtypes = [P]
     lib.grand_set_stream.argtypes = [P, P]
     lib.grand_insert_batch.argtypes = [P, P, P, U32]
+    lib.grand_build_cagra.restype = I32
+    lib.grand_build_cagra.argtypes = [P, P, P, U32, P, U32, U32, U32]
     lib.grand_delete_batch.argtypes = [P, P, U32]
     lib.grand_search.argtypes = [P, P, U32, U32, U32, P, P]
     lib.grand_search_static.argtypes = [P, P, U32, U32, U32, P, P]
@@ -242,6 +244,21 @@ class GrandIndex:
             vecs = _np(vecs, self.np_dtype)
         n = int(ids.shape[0])
         rc = self.lib.grand_insert_batch(self.h, _ptr(vecs), _ptr(ids), n)
+        return self._check(rc) if check else rc
+
+    def build_cagra(self, ids, vecs, init, knn: int, iters: int, sample: int, check: bool = True) -> int:
+        """CAGRA graph construction over this empty CAGRA index; init is
+        n x knn batch positions (the random initial neighbour lists)."""
+        if not _is_torch(ids):
+            ids = _np(ids, np.uint32)
+        if not _is_torch(vecs):
+            vecs = _np(vecs, self.np_dtype)
+        if not _is_torch(init):
+            init = _np(init, np.uint32)
+        n = int(ids.shape[0])
+        if tuple(init.shape) != (n, knn):
+            raise ValueError("init must be n x knn")
+        rc = self.lib.grand_build_cagra(self.h, _ptr(vecs), _ptr(ids), n, _ptr(init), knn, iters, sample)
         return self._check(rc) if check else rc
 
     def delete(self, ids, check: bool = True) -> int:
