@@ -80,8 +80,16 @@ def parse():
     ap.add_argument("--build-batch", type=int, default=0, help="override the batch size of the untimed base build")
     ap.add_argument("--build-frac", type=float, default=-1.0, help="override the growth fraction of the base build")
     ap.add_argument("--build-min", type=int, default=0, help="override the smallest base build batch")
-    ap.add_argument("--refresh-passes", type=int, default=1,
-                    help="after the base build, delete and re-insert every base batch this many times (untimed)")
+    ap.add_argument("--refresh-passes", type=int, default=-1,
+                    help="after the base build, delete and re-insert every base batch this many times (untimed; "
+                         "default 1 for Vamana, 0 for CAGRA, whose delete repair the refresh would only degrade)")
+    ap.add_argument("--cagra-seed", choices=["construct", "bootstrap", "full"], default="construct",
+                    help="CAGRA base build: the first base batch by the CAGRA graph construction (construct) or by "
+                         "the empty-index bootstrap of a batch insert (bootstrap), then batched inserts; or the "
+                         "whole base by one construction (full)")
+    ap.add_argument("--cagra-knn", type=int, default=128, help="construction: k-NN degree")
+    ap.add_argument("--cagra-rounds", type=int, default=8, help="construction: NN-Descent rounds")
+    ap.add_argument("--cagra-sample", type=int, default=16, help="construction: NN-Descent sample size")
     ap.add_argument("--prune-rule", choices=["alpha_on_sq", "alpha_on_l2"], default=None,
                     help="override the alpha test of GrANDRobustPrune")
     ap.add_argument("--rev-mode", choices=["full", "batch"], default="batch")
@@ -515,6 +523,7 @@ def main():
     from paper_2608_21163_amd import GrandIndex
     from paper_2608_21163_amd.grand import REV_BATCH, REV_FULL
     from workloads import make_workload
+    from workloads.generators import Op, cagra_init_lists
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.backends.cuda.matmul.allow_tf32 = False
@@ -548,12 +557,30 @@ def main():
         return torch.from_numpy(a).to(dev)
 
     # ---- build (untimed)
+    cagra = cfg.algo == "cagra"
+    refresh = args.refresh_passes if args.refresh_passes >= 0 else (0 if cagra else 1)
     t0 = time.perf_counter()
     nb = npts = 0
     base_ops = []
-    for op in w.base_batches():
+    construct_s = None
+    batches = list(w.base_batches())
+    if cagra and args.cagra_seed == "full":  # the whole base in one construction
+        batches = [Op("insert", np.concatenate([b.ids for b in batches]), np.concatenate([b.vecs for b in batches]))]
+    for op in batches:
         ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
-        g.insert(ids, vecs)
+        if cagra and nb == 0 and args.cagra_seed != "bootstrap":
+            # the seed graph by the CAGRA graph construction (random initial
+            # lists drawn here, as the library takes them as input)
+            init = torch.from_numpy(cagra_init_lists(len(op.ids), args.cagra_knn, args.seed).view(np.int32)).to(dev)
+            torch.cuda.synchronize()
+            tc = time.perf_counter()
+            g.build_cagra(ids, vecs, init, args.cagra_knn, args.cagra_rounds, args.cagra_sample)
+            torch.cuda.synchronize()
+            construct_s = time.perf_counter() - tc
+            log(f"build: seed graph of {len(op.ids):,} points constructed in {construct_s:.2f} s")
+            del init
+        else:
+            g.insert(ids, vecs)
         mirror.insert(ids, vecs)
         base_ops.append((ids, vecs))
         nb += 1
@@ -562,7 +589,7 @@ def main():
             log(f"build: {npts:,} points, {time.perf_counter() - t0:.1f} s")
     # refresh passes: the same points leave and re-enter batch by batch, so
     # every list is rebuilt against the complete base set
-    for _ in range(args.refresh_passes):
+    for _ in range(refresh):
         for ids, vecs in base_ops:
             g.delete(ids)
             g.insert(ids, vecs)
@@ -570,6 +597,16 @@ def main():
     torch.cuda.synchronize()
     build_s = time.perf_counter() - t0
     log(f"build done: {spec.base_n:,} points in {build_s:.1f} s")
+    if cagra and args.cagra_seed != "bootstrap":
+        how = ("the whole base by one CAGRA graph construction" if args.cagra_seed == "full" else
+               f"the first {len(batches[0].ids):,} points by the CAGRA graph construction, then "
+               f"{len(batches) - 1} insert batches")
+        base_build_label = (f"{how} (NN-Descent k-NN degree {args.cagra_knn}, {args.cagra_rounds} rounds, sample "
+                            f"{args.cagra_sample}; rank-based pruning; reverse edges), {refresh} refresh pass(es) "
+                            f"(untimed)")
+    else:
+        base_build_label = (f"{len(spec.build_sizes())} insert batches, then {refresh} refresh pass(es) deleting "
+                            f"and re-inserting each base batch (untimed)")
 
     if args.reverse_microbench:
         reverse_microbench(g, w, spec)
@@ -770,8 +807,7 @@ def main():
                    "delete_batch": spec.n_delete, "queries": spec.n_query, "k": spec.k, "beam": spec.beam,
                    "R": cfg.R, "L": cfg.L_build, "alpha": cfg.alpha, "P": cfg.P, "c": cfg.c,
                    "k_repair": cfg.k_repair, "reverse_graph": args.rev_mode, "parallelism": "single GPU",
-                   "base_build": f"{len(spec.build_sizes())} insert batches, then {args.refresh_passes} refresh "
-                                 f"pass(es) deleting and re-inserting each base batch (untimed)"},
+                   "base_build": base_build_label},
         "search_qps": round(q_n / (q_ms / 1e3), 1),
         "insert_per_s": round(spec.n_insert * K / (ins_ms / 1e3), 1),
         "delete_per_s": round(spec.n_delete * K / (del_ms / 1e3), 1),
@@ -779,6 +815,7 @@ def main():
         "recall_at_10_mean": round(float(np.mean(recalls)), 4) if recalls else None,
         "recall_at_10_per_round": [round(x, 4) for x in recalls],
         "build_s": round(build_s, 2),
+        "construct_s": round(construct_s, 3) if construct_s is not None else None,
         "roofline": roofline,
         "roofline_other_phases": others,
         "cpu_baseline": cpu,
