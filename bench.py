@@ -82,7 +82,8 @@ def parse():
     ap.add_argument("--build-min", type=int, default=0, help="override the smallest base build batch")
     ap.add_argument("--refresh-passes", type=int, default=-1,
                     help="after the base build, delete and re-insert every base batch this many times (untimed; "
-                         "default 1 for Vamana, 0 for CAGRA, whose delete repair the refresh would only degrade)")
+                         "default: the workload's, 1 for most, 3 for the 960-d and 768-d sets, 0 for CAGRA, whose "
+                         "delete repair the refresh would only degrade)")
     ap.add_argument("--cagra-seed", choices=["construct", "bootstrap", "full"], default="construct",
                     help="CAGRA base build: the first base batch by the CAGRA graph construction (construct) or by "
                          "the empty-index bootstrap of a batch insert (bootstrap), then batched inserts; or the "
@@ -558,7 +559,7 @@ def main():
 
     # ---- build (untimed)
     cagra = cfg.algo == "cagra"
-    refresh = args.refresh_passes if args.refresh_passes >= 0 else (0 if cagra else 1)
+    refresh = args.refresh_passes if args.refresh_passes >= 0 else spec.refresh
     t0 = time.perf_counter()
     nb = npts = 0
     base_ops = []

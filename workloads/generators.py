@@ -78,6 +78,9 @@ class StreamSpec:
     # most build_batch (the first batch, into the empty index, is build_min)
     build_frac: float = 0.0
     build_min: int = 0
+    # untimed refresh passes after the base build: every base batch is
+    # deleted and re-inserted, so each list is rebuilt against the whole base
+    refresh: int = 1
 
     def build_sizes(self):
         if self.build_frac <= 0.0:
@@ -130,22 +133,22 @@ CONFIGS = {
         "glove1m_cagra", "1M x 100 fp32 IP, CAGRA fixed degree 64",
         IndexConfig("cagra", "f32", "ip", 100, 1_000_000, 64, 64),
         StreamSpec(1_000_000, 10_000, 10, 10_000, 30_000, 10_000, 10, 64,
-                   order=("delete", "insert", "search")),
+                   order=("delete", "insert", "search"), refresh=0),
         "mix_t_norm", (1000, 0.3, 3.0)),
-    # 500K x 960 fp32, 128-component mixture, per-dimension scale U[0.1,1],
-    # clipped at zero; 10 rounds of +5K / -5K / 5K queries (beam 128).
     # 500K x 768 fp32 inner-product data with varying norms (a Gaussian
     # mixture, norms clipped at 40), searched through the L2 augmentation
     # with M = 40; 10 rounds of +5K / -5K / 5K queries (beam 128).
     "ip768_mips": WorkloadDef(
         "ip768_mips", "500K x 768 fp32 inner product (MIPS via L2 augmentation), Vamana R=64 L=128",
         IndexConfig("vamana", "f32", "mips", 768, 505_000, 64, 128, mips_norm=40.0),
-        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128),
+        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128, refresh=3),
         "mix_ip", (128, 0.35, 40.0)),
+    # 500K x 960 fp32, 128-component mixture, per-dimension scale U[0.1,1],
+    # clipped at zero; 10 rounds of +5K / -5K / 5K queries (beam 128).
     "gist500k": WorkloadDef(
         "gist500k", "500K x 960 fp32 scaled clipped mixture, Vamana R=64 L=128",
         IndexConfig("vamana", "f32", "l2", 960, 505_000, 64, 128),
-        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128),
+        StreamSpec(500_000, 5_000, 10, 5_000, 5_000, 5_000, 10, 128, refresh=3),
         "mix_relu_scaled", (128, 0.5)),
 }
 
