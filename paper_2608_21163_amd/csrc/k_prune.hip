@@ -400,11 +400,15 @@ __device__ __forceinline__ uint32_t first_bits(uint32_t m, int n) {
 // The largest integer distance d with coef * d <= D (fp64 product, as in the
 // prune test), for an integer-valued D >= 0; every d up to it passes, since
 // rounding is monotone.
-__device__ __forceinline__ int kill_threshold(double coef, float D) {
+// inv is 1 / coef (rounded): the quotient estimate is off by at most one,
+// and the two exact tests correct it.
+__device__ __forceinline__ int kill_threshold(double coef, double inv, float D) {
   if (!(coef > 0.0)) return 0x7FFFFFFF;
   const double dd = (double)D;
   if (!(dd < 2147483647.0)) return 0x7FFFFFFF;
-  int t = (int)floor(dd / coef);
+  const double q = floor(dd * inv);
+  if (!(q < 2147483646.0)) return 0x7FFFFFFF;
+  int t = (int)q;
   t = coef * (double)(t + 1) <= dd ? t + 1 : t;
   t = coef * (double)t <= dd ? t : t - 1;
   return t;
@@ -430,6 +434,7 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
                          const float *dpos, bool (&valid)[NR], uint32_t &sid, float &sdist,
                          unsigned long long &evals) {
   const int ln = lane(), g = ln >> 4, col = ln & 15;
+  const double inv = 1.0 / coef;
   const size_t goff = (size_t)g * 16;
   const int nt = (m + 15) >> 4;
   auto load_tile = [&](v4i (&dst)[NK], int t) -> int {
@@ -466,7 +471,7 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
     for (int ii = 0; ii < 4; ii++) rn[ii] = __shfl(na, 4 * g + ii, 64);
     uint32_t kmd = 0;
     {
-      const int thr = kill_threshold(coef, dpos[16 * b + col]);
+      const int thr = kill_threshold(coef, inv, dpos[16 * b + col]);
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(A[kk], A[kk], acc);
@@ -525,7 +530,7 @@ __device__ int greedy_u8(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
           const uint8_t *row = P.vecs + (size_t)(e < m ? spos[e] : p) * P.stride + goff;
 #pragma unroll
           for (int kk = 0; kk < NK; kk++) Bt[q][kk] = to_i8x16(ld16(row + (size_t)kk * 64));
-          thr[q] = kill_threshold(coef, dpos[e]);
+          thr[q] = kill_threshold(coef, inv, dpos[e]);
         }
       }
 #pragma unroll
@@ -571,6 +576,7 @@ template <int NK, int NT>
 __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
                              const float *dpos, int *thr, int *nrmL, uint32_t *oid, float *od, uint32_t &ntile) {
   const int ln = lane(), g = ln >> 4, col = ln & 15;
+  const double inv = 1.0 / coef;
   const size_t goff = (size_t)g * 16;
   const int nt = (m + 15) >> 4;
   constexpr int NR = (NT + 3) / 4;
@@ -593,7 +599,7 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
 #pragma unroll
   for (int r = 0; r < NR; r++) {
     const int e = r * 64 + ln;
-    thr[e] = e < m ? kill_threshold(coef, dpos[e]) : -1;
+    thr[e] = e < m ? kill_threshold(coef, inv, dpos[e]) : -1;
   }
   __syncthreads();
   int t2[NT];
@@ -651,15 +657,10 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
     }
     nsel += ns;
     if (done) break;
-    // lanes (g, col) whose block row 4g + ii was selected
-    uint64_t selm[4];
+    // whether block row 4g + ii (this lane's rows) was selected
+    bool sb[4];
 #pragma unroll
-    for (int ii = 0; ii < 4; ii++) {
-      uint64_t mk = 0;
-#pragma unroll
-      for (int gg = 0; gg < 4; gg++) mk |= ((S >> (4 * gg + ii)) & 1u) ? (0xFFFFull << (16 * gg)) : 0ull;
-      selm[ii] = mk;
-    }
+    for (int ii = 0; ii < 4; ii++) sb[ii] = ((S >> (4 * g + ii)) & 1u) != 0u;
 #pragma unroll
     for (int c = b + 1; c < NT; c++) {
       if (c >= nt) break;
@@ -667,10 +668,14 @@ __device__ int greedy_u8_reg(const PoolView &P, uint32_t p, int m, uint32_t R, d
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < NK; kk++) acc = mfma_i8(T[b][kk], T[c][kk], acc);
-      uint64_t dm = 0;
+      // column col of tile c dies when a selected row of the block kills it
+      bool k = false;
 #pragma unroll
-      for (int ii = 0; ii < 4; ii++) dm |= ballot(rn[ii] - 2 * acc[ii] <= t2[c]) & selm[ii];
-      const uint64_t d = (dm | (dm >> 16) | (dm >> 32) | (dm >> 48)) & 0xFFFFull;
+      for (int ii = 0; ii < 4; ii++) k |= sb[ii] && (rn[ii] - 2 * acc[ii] <= t2[c]);
+      uint32_t kw = k ? 1u : 0u;
+      kw |= xshfl(kw, 16);
+      kw |= xshfl(kw, 32);
+      const uint64_t d = ballot(kw != 0u && g == 0) & 0xFFFFull;
       vm[c >> 2] &= ~(d << (16 * (c & 3)));
       ntile++;
     }

@@ -196,43 +196,55 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
 // (Dist, id) (Dist < 2^23 for 128 uint8 dimensions).  A slot without a point
 // gets a key of at least 2^30.  The key of x itself (when x is in C_i) is its
 // slot alone, Dist being 0, which is how it is excluded.
+//
+// Inside the step the keys of one neighbour x are handled as the signed
+// values n = 128 x.c' - 64 |c'|^2 - slot = 64 |x|^2 - key (one shift-add per
+// candidate from the MFMA product), largest first; the 64 |x|^2 term, the
+// same for all of x's candidates, is added back when the key is written.
+// Every |n| stays below 2^31 (empty slots near -1.5 * 2^30), so the
+// signed order is exact.
 
-// Sorted list of the K smallest keys.
+// Sorted (descending) list of the K largest values.
 template <int K>
-__device__ __forceinline__ void kl_insert32(uint32_t (&l)[K], uint32_t k) {
+__device__ __forceinline__ void kl_insert_max(int32_t (&l)[K], int32_t k) {
 #pragma unroll
   for (int j = 0; j < K; j++) {
-    const uint32_t lo = min(k, l[j]);
-    k = max(k, l[j]);
-    l[j] = lo;
+    const int32_t hi = max(k, l[j]);
+    k = min(k, l[j]);
+    l[j] = hi;
   }
 }
-// l <- the K smallest of the two sorted lists l and o (bitonic merge).
+// l <- the K largest of the two descending lists l and o (bitonic merge).
 template <int K>
-__device__ __forceinline__ void kl_merge32(uint32_t (&l)[K], const uint32_t (&o)[K]) {
+__device__ __forceinline__ void kl_merge_max(int32_t (&l)[K], const int32_t (&o)[K]) {
 #pragma unroll
-  for (int j = 0; j < K; j++) l[j] = min(l[j], o[K - 1 - j]);
+  for (int j = 0; j < K; j++) l[j] = max(l[j], o[K - 1 - j]);
 #pragma unroll
   for (int d = K / 2; d > 0; d >>= 1)
 #pragma unroll
     for (int j = 0; j < K; j++)
       if ((j & d) == 0) {
-        const uint32_t x = l[j], y = l[j + d];
-        l[j] = min(x, y);
-        l[j + d] = max(x, y);
+        const int32_t x = l[j], y = l[j + d];
+        l[j] = max(x, y);
+        l[j + d] = min(x, y);
       }
 }
-constexpr uint32_t kKeyNone = 0x7FFFFFFFu;  // key base of an empty candidate slot
-constexpr uint32_t kKeyValid = 1u << 30;     // keys of points are below
+constexpr int32_t kSlotNone = 0x60000000;  // 64 |c'|^2 + slot of an empty candidate slot
+constexpr int32_t kNone = INT32_MIN;       // below every value: an excluded candidate
+constexpr uint32_t kKeyValid = 1u << 30;   // keys of points are below
 
 template <int NK, int K, int NPL>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_repair_mfma(RepairArgs a) {
   constexpr int NT = 4;        // C_i tiles (k_repair <= 64)
   constexpr int W = 64 * NPL;  // positions per chunk
   __shared__ uint32_t cidL[64];                 // C_i ids by slot (ascending, points first)
-  __shared__ __align__(16) uint32_t ckeyL[64];  // 64 * |c'|^2 + slot (kKeyNone when empty)
+  __shared__ __align__(16) int32_t ckeyL[64];   // -(64 |c'|^2 + slot) (-kSlotNone when empty)
   __shared__ uint32_t xL[W];                    // the chunk's neighbours
   __shared__ uint32_t rxL[W];                   // slot of each neighbour in C_i, or ~0
+  // the chunk's records, staged and written out together at its end (one
+  // contiguous range: at most c + 1 <= K + 1 per position)
+  __shared__ uint32_t rtL[W * (K + 1)], rsL[W * (K + 1)];
+  __shared__ float rdL[W * (K + 1)];
   const int ln = lane(), g = ln >> 4, col = ln & 15;
   const PoolView &P = a.pool;
   const size_t goff = (size_t)g * 16;
@@ -318,7 +330,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
     int mycnr = cnr[0];
 #pragma unroll
     for (int t = 1; t < NT; t++) mycnr = (ln >> 4) == t ? cnr[t] : mycnr;
-    ckeyL[ln] = mvalid ? (((uint32_t)mycnr << 6) | (uint32_t)ln) : kKeyNone;
+    ckeyL[ln] = -(mvalid ? (mycnr << 6) | ln : kSlotNone);
     __syncthreads();
     // slot of each neighbour in C_i (binary search over the ascending ids)
 #pragma unroll
@@ -333,6 +345,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
     }
     __syncthreads();
     if (j == 0) rows += (unsigned long long)nv;
+    const uint32_t rb0 = repair_base(a, d0, rbase, e0);
     for (int s = 0; 16 * s < cnt; s++) {
       // neighbours 16s .. 16s+15 as the B operand
       const uint32_t xs = xsn;
@@ -348,9 +361,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
       nx += (int)xshfl((uint32_t)nx, 16);
       nx += (int)xshfl((uint32_t)nx, 32);
       const uint32_t nx64 = (uint32_t)nx << 6;
-      uint32_t l[K];
+      // x's own value (key rx) when x is in C_i; otherwise a value no
+      // candidate takes (key ~0)
+      const int32_t rxn = (int32_t)(nx64 - rx);
+      int32_t l[K];
 #pragma unroll
-      for (int k = 0; k < K; k++) l[k] = ~0u;
+      for (int k = 0; k < K; k++) l[k] = kNone;
       // two tiles' products at a time
 #pragma unroll
       for (int t0 = 0; t0 < NT; t0 += 2) {
@@ -363,21 +379,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
         }
 #pragma unroll
         for (int u = 0; u < 2; u++) {
-          const uint4 ck = *reinterpret_cast<const uint4 *>(&ckeyL[16 * (t0 + u) + 4 * g]);
-          const uint32_t cks[4] = {ck.x, ck.y, ck.z, ck.w};
+          const int4 ck = *reinterpret_cast<const int4 *>(&ckeyL[16 * (t0 + u) + 4 * g]);
+          const int32_t cks[4] = {ck.x, ck.y, ck.z, ck.w};
 #pragma unroll
           for (int ii = 0; ii < 4; ii++) {
-            const uint32_t key = cks[ii] + nx64 - ((uint32_t)acc[u][ii] << 7);
-            kl_insert32<K>(l, key == rx ? ~0u : key);
+            const int32_t n = (int32_t)((uint32_t)acc[u][ii] << 7) + cks[ii];
+            kl_insert_max<K>(l, n == rxn ? kNone : n);
           }
         }
       }
 #pragma unroll
       for (int o = 16; o < 64; o <<= 1) {
-        uint32_t ot[K];
+        int32_t ot[K];
 #pragma unroll
-        for (int k = 0; k < K; k++) ot[k] = xshfl(l[k], o);
-        kl_merge32<K>(l, ot);
+        for (int k = 0; k < K; k++) ot[k] = (int32_t)xshfl((uint32_t)l[k], o);
+        kl_merge_max<K>(l, ot);
       }
       if (g == 0 && xsok) evals += nv - (rx != ~0u ? 1u : 0u);
       // records of neighbour 16s + col: lane g writes entries g, g+4, ...
@@ -386,31 +402,43 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
         const uint32_t pos = e0 + (uint32_t)e;
         const bool inbound = pos < d0.w;
         const uint32_t nrec = inbound ? c + 1 : c;
-        const uint32_t base = repair_base(a, d0, rbase, pos);
+        const uint32_t base = repair_base(a, d0, rbase, pos) - rb0;
         for (uint32_t k = (uint32_t)g; k < nrec; k += 4) {
-          uint32_t key = ~0u;
+          int32_t n = kNone;
 #pragma unroll
           for (int kk = 0; kk < K; kk++)
-            if ((uint32_t)kk == k) key = l[kk];
+            if ((uint32_t)kk == k) n = l[kk];
+          const uint32_t key = nx64 - (uint32_t)n;
           const bool v = key < kKeyValid;
           const uint32_t yi = v ? cidL[key & 63u] : kInvalid;
           const float yd = v ? (float)(key >> 6) : 0.0f;
-          if (!xsok) {
-            a.rec_t[base + k] = kInvalid;
-          } else if (inbound) {
+          uint32_t rt = kInvalid, rs = kInvalid;
+          float rd = 0.0f;
+          if (xsok && inbound) {
             const bool marker = k == c;
-            a.rec_t[base + k] = xs;
-            a.rec_s[base + k] = marker ? kInvalid : yi;
-            a.rec_d[base + k] = marker ? 0.0f : yd;
+            rt = xs;
+            rs = marker ? kInvalid : yi;
+            rd = marker ? 0.0f : yd;
             recs++;
-          } else {
-            a.rec_t[base + k] = yi;
-            a.rec_s[base + k] = v ? xs : kInvalid;
-            a.rec_d[base + k] = yd;
+          } else if (xsok) {
+            rt = yi;
+            rs = v ? xs : kInvalid;
+            rd = yd;
             recs += v ? 1u : 0u;
           }
+          rtL[base + k] = rt;
+          rsL[base + k] = rs;
+          rdL[base + k] = rd;
         }
       }
+    }
+    __syncthreads();
+    // the chunk's records, written out in order
+    const uint32_t nr = repair_base(a, d0, rbase, e0 + (uint32_t)cnt) - rb0;
+    for (uint32_t o = (uint32_t)ln; o < nr; o += 64) {
+      a.rec_t[rb0 + o] = rtL[o];
+      a.rec_s[rb0 + o] = rsL[o];
+      a.rec_d[rb0 + o] = rdL[o];
     }
     __syncthreads();
   }
