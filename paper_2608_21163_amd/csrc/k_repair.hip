@@ -201,33 +201,24 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
 // values n = 128 x.c' - 64 |c'|^2 - slot = 64 |x|^2 - key (one shift-add per
 // candidate from the MFMA product), largest first; the 64 |x|^2 term, the
 // same for all of x's candidates, is added back when the key is written.
+// The lists keep K + 1 values, x's own included, and x's value is taken out
+// of the merged list.
 // Every |n| stays below 2^31 (empty slots near -1.5 * 2^30), so the
 // signed order is exact.
 
-// Sorted (descending) list of the K largest values.
-template <int K>
-__device__ __forceinline__ void kl_insert_max(int32_t (&l)[K], int32_t k) {
+// Sorted (descending) list of the L largest values: entry j of the new list
+// is the median of old entries j - 1 and j and the new value (one v_med3).
+template <int L>
+__device__ __forceinline__ void kl_insert_max(int32_t (&l)[L], int32_t k) {
 #pragma unroll
-  for (int j = 0; j < K; j++) {
-    const int32_t hi = max(k, l[j]);
-    k = min(k, l[j]);
-    l[j] = hi;
-  }
+  for (int j = L - 1; j > 0; j--) l[j] = max(min(l[j - 1], l[j]), min(max(l[j - 1], l[j]), k));
+  l[0] = max(l[0], k);
 }
-// l <- the K largest of the two descending lists l and o (bitonic merge).
-template <int K>
-__device__ __forceinline__ void kl_merge_max(int32_t (&l)[K], const int32_t (&o)[K]) {
+// l <- the L largest of the two descending lists l and o.
+template <int L>
+__device__ __forceinline__ void kl_merge_max(int32_t (&l)[L], const int32_t (&o)[L]) {
 #pragma unroll
-  for (int j = 0; j < K; j++) l[j] = max(l[j], o[K - 1 - j]);
-#pragma unroll
-  for (int d = K / 2; d > 0; d >>= 1)
-#pragma unroll
-    for (int j = 0; j < K; j++)
-      if ((j & d) == 0) {
-        const int32_t x = l[j], y = l[j + d];
-        l[j] = max(x, y);
-        l[j + d] = min(x, y);
-      }
+  for (int j = 0; j < L; j++) kl_insert_max<L>(l, o[j]);
 }
 constexpr int32_t kSlotNone = 0x60000000;  // 64 |c'|^2 + slot of an empty candidate slot
 constexpr int32_t kNone = INT32_MIN;       // below every value: an excluded candidate
@@ -364,9 +355,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
       // x's own value (key rx) when x is in C_i; otherwise a value no
       // candidate takes (key ~0)
       const int32_t rxn = (int32_t)(nx64 - rx);
-      int32_t l[K];
+      constexpr int L = K + 1;
+      int32_t l[L];
 #pragma unroll
-      for (int k = 0; k < K; k++) l[k] = kNone;
+      for (int k = 0; k < L; k++) l[k] = kNone;
       // two tiles' products at a time
 #pragma unroll
       for (int t0 = 0; t0 < NT; t0 += 2) {
@@ -384,26 +376,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4))) void k_
 #pragma unroll
           for (int ii = 0; ii < 4; ii++) {
             const int32_t n = (int32_t)((uint32_t)acc[u][ii] << 7) + cks[ii];
-            kl_insert_max<K>(l, n == rxn ? kNone : n);
+            kl_insert_max<L>(l, n);
           }
         }
       }
 #pragma unroll
       for (int o = 16; o < 64; o <<= 1) {
-        int32_t ot[K];
+        int32_t ot[L];
 #pragma unroll
-        for (int k = 0; k < K; k++) ot[k] = (int32_t)xshfl((uint32_t)l[k], o);
-        kl_merge_max<K>(l, ot);
+        for (int k = 0; k < L; k++) ot[k] = (int32_t)xshfl((uint32_t)l[k], o);
+        kl_merge_max<L>(l, ot);
       }
+      // without x: the entries from x's value on move up by one
+      bool has_x = false;
+#pragma unroll
+      for (int k = 0; k < L; k++) has_x |= l[k] == rxn;
+#pragma unroll
+      for (int k = 0; k < K; k++) l[k] = (has_x && l[k] <= rxn) ? l[k + 1] : l[k];
       if (g == 0 && xsok) evals += nv - (rx != ~0u ? 1u : 0u);
-      // records of neighbour 16s + col: lane g writes entries g, g+4, ...
+      // records of neighbour 16s + col (at most c + 1 <= K + 1): lane g
+      // stages entries g, g + 4, ...
       const int e = 16 * s + col;
       if (e < cnt) {
         const uint32_t pos = e0 + (uint32_t)e;
         const bool inbound = pos < d0.w;
         const uint32_t nrec = inbound ? c + 1 : c;
         const uint32_t base = repair_base(a, d0, rbase, pos) - rb0;
-        for (uint32_t k = (uint32_t)g; k < nrec; k += 4) {
+#pragma unroll
+        for (int kq = 0; kq < (K + 4) / 4; kq++) {
+          const uint32_t k = (uint32_t)(g + 4 * kq);
+          if (k >= nrec) break;
           int32_t n = kNone;
 #pragma unroll
           for (int kk = 0; kk < K; kk++)
@@ -625,7 +627,9 @@ uint32_t repair_chunk_width(int kind, const PoolView &p, uint32_t kr, uint32_t c
 hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
   if (kind == kU8L2 && repair_chunked(kind, a.pool, a.kr, a.c)) {
-    // persistent waves over the chunk descriptors: exactly the resident workgroups
+    // persistent waves over the chunk descriptors, twice the resident
+    // workgroups: the second half starts as the first ones finish, which
+    // evens out the work per wave (chunks differ in length)
     if (a.cw != 64u * kRepairNpl) return hipErrorInvalidValue;
     static const uint32_t r22 = resident_blocks((const void *)k_repair_mfma<2, 2, kRepairNpl>);
     static const uint32_t r24 = resident_blocks((const void *)k_repair_mfma<2, 4, kRepairNpl>);
@@ -633,14 +637,14 @@ hipError_t launch_repair(int kind, int vc, const RepairArgs &a, uint32_t grid, h
     static const uint32_t r14 = resident_blocks((const void *)k_repair_mfma<1, 4, kRepairNpl>);
     if (a.pool.nch == 8) {
       if (a.c <= 2)
-        hipLaunchKernelGGL((k_repair_mfma<2, 2, kRepairNpl>), dim3(clamp_resident(grid, r22)), dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_repair_mfma<2, 2, kRepairNpl>), dim3(clamp_resident(grid, 2 * r22)), dim3(64), 0, st, a);
       else
-        hipLaunchKernelGGL((k_repair_mfma<2, 4, kRepairNpl>), dim3(clamp_resident(grid, r24)), dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_repair_mfma<2, 4, kRepairNpl>), dim3(clamp_resident(grid, 2 * r24)), dim3(64), 0, st, a);
     } else {
       if (a.c <= 2)
-        hipLaunchKernelGGL((k_repair_mfma<1, 2, kRepairNpl>), dim3(clamp_resident(grid, r12)), dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_repair_mfma<1, 2, kRepairNpl>), dim3(clamp_resident(grid, 2 * r12)), dim3(64), 0, st, a);
       else
-        hipLaunchKernelGGL((k_repair_mfma<1, 4, kRepairNpl>), dim3(clamp_resident(grid, r14)), dim3(64), 0, st, a);
+        hipLaunchKernelGGL((k_repair_mfma<1, 4, kRepairNpl>), dim3(clamp_resident(grid, 2 * r14)), dim3(64), 0, st, a);
     }
     return hipGetLastError();
   }
