@@ -1078,18 +1078,47 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
     }
     if (!P.adjd) evals += (unsigned long long)m;
     __syncthreads();
-    uint64_t key[NC];
+    // Candidates by (D_u, id): 32-bit keys D << 7 | list position (uint8
+    // distances are integers below 2^23) order them when no two share a
+    // distance; a tie, which the id decides, takes the 64-bit key sort.
+    uint32_t k32[NC];
 #pragma unroll
     for (int r = 0; r < NC; r++) {
       const int e = r * 64 + ln;
-      key[r] = e < m ? key64(dpos[e], cl[e]) : ~0ull;
+      k32[r] = e < m ? ((uint32_t)dpos[e] << 7) | (uint32_t)e : ~0u;
     }
-    __syncthreads();
-    wave_sort64<NC>(key);
+    wave_sort32<NC>(k32);
+    bool tie = false;
 #pragma unroll
     for (int r = 0; r < NC; r++) {
-      spos[r * 64 + ln] = (uint32_t)key[r];
-      dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
+      // the next element's key (lane 63 of a row: lane 0 of the next row)
+      uint32_t nx = __shfl(k32[r], (ln + 1) & 63, 64);
+      if (ln == 63) nx = r + 1 < NC ? rdlane(k32[r + 1 < NC ? r + 1 : r], 0) : ~0u;
+      tie |= r * 64 + ln + 1 < m && (k32[r] >> 7) == (nx >> 7);
+    }
+    if (!ballot(tie)) {
+      uint32_t sid[NC];
+#pragma unroll
+      for (int r = 0; r < NC; r++) sid[r] = r * 64 + ln < m ? cl[k32[r] & 127u] : kInvalid;
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        spos[r * 64 + ln] = sid[r];
+        dpos[r * 64 + ln] = r * 64 + ln < m ? (float)(k32[r] >> 7) : finf();
+      }
+    } else {
+      uint64_t key[NC];
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        const int e = r * 64 + ln;
+        key[r] = e < m ? key64(dpos[e], cl[e]) : ~0ull;
+      }
+      __syncthreads();
+      wave_sort64<NC>(key);
+#pragma unroll
+      for (int r = 0; r < NC; r++) {
+        spos[r * 64 + ln] = (uint32_t)key[r];
+        dpos[r * 64 + ln] = unsortable((uint32_t)(key[r] >> 32));
+      }
     }
     __syncthreads();
     int nsel;
@@ -1636,14 +1665,16 @@ static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st
     }
   }
   if constexpr (KIND == kU8L2 && NC == 2 && NP == 1) {
+    // persistent waves, twice the resident workgroups: the second half
+    // starts as the first ones finish, which evens out the work per wave
     if (a.pool.R <= 64 && a.pool.nch == 8) {
       static const uint32_t res = resident_blocks((const void *)k_rebuild_mr<2>);
-      hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
+      hipLaunchKernelGGL(k_rebuild_mr<2>, dim3(clamp_resident(grid, 2 * res)), dim3(64), 0, st, a);
       return;
     }
     if (a.pool.R <= 64 && a.pool.nch == 4) {
       static const uint32_t res = resident_blocks((const void *)k_rebuild_mr<1>);
-      hipLaunchKernelGGL(k_rebuild_mr<1>, dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
+      hipLaunchKernelGGL(k_rebuild_mr<1>, dim3(clamp_resident(grid, 2 * res)), dim3(64), 0, st, a);
       return;
     }
   }

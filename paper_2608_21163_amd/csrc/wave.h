@@ -480,6 +480,40 @@ __device__ __forceinline__ void wave_sort64(uint64_t (&k)[N]) {
   }
 }
 
+// Bitonic sort, ascending, of N*64 32-bit keys held as element e = r*64 + lane.
+template <int N>
+__device__ __forceinline__ void wave_sort32(uint32_t (&k)[N]) {
+  const int ln = lane();
+#pragma unroll
+  for (int kk = 2; kk <= 64 * N; kk <<= 1) {
+#pragma unroll
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      if (j >= 64) {
+        const int jr = j >> 6;
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const int p = r ^ jr;
+          if (p > r) {
+            const bool up = ((r * 64 + ln) & kk) == 0;
+            const uint32_t a = k[r], b = k[p];
+            const bool sw = (b < a) == up;
+            k[r] = sw ? b : a;
+            k[p] = sw ? a : b;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < N; r++) {
+          const bool up = ((r * 64 + ln) & kk) == 0;
+          const bool keep_min = ((ln & j) == 0) == up;
+          const uint32_t o = xshfl(k[r], j);
+          k[r] = keep_min ? min(o, k[r]) : max(o, k[r]);
+        }
+      }
+    }
+  }
+}
+
 // Exclusive wave prefix sum of small non-negative ints.
 __device__ __forceinline__ int wave_excl_scan(int v, int& total) {
   int x = v;
