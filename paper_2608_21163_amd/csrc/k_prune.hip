@@ -1660,7 +1660,7 @@ static void launch_rebuild_t(const RebuildArgs &a, uint32_t grid, hipStream_t st
   if constexpr (KIND != kU8L2 && NC == 2 && NP == 1) {
     if (a.pool.R <= 64) {
       static const uint32_t res = resident_blocks((const void *)k_rebuild_vec<KIND>);
-      hipLaunchKernelGGL((k_rebuild_vec<KIND>), dim3(clamp_resident(grid, res)), dim3(64), 0, st, a);
+      hipLaunchKernelGGL((k_rebuild_vec<KIND>), dim3(clamp_resident(grid, 2 * res)), dim3(64), 0, st, a);
       return;
     }
   }
