@@ -1302,10 +1302,18 @@ __device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids
   if (k >= ns) return;
   const uint32_t id = ids[k];
   const float *row = reinterpret_cast<const float *>(P.vecs + (size_t)(kvalid(id) ? id : 0u) * P.stride);
+  // all four loads issued before any is used: addresses clamped into the
+  // row, the values past it replaced by zeros afterwards
+  uint4 v4[4];
 #pragma unroll
   for (int h = 0; h < 4; h++) {
     const int f = d0 + 16 * part + 4 * h;
-    const uint4 v = (kvalid(id) && f < nfl) ? *reinterpret_cast<const uint4 *>(row + f) : make_uint4(0, 0, 0, 0);
+    v4[h] = *reinterpret_cast<const uint4 *>(row + (f < nfl ? f : 0));
+  }
+#pragma unroll
+  for (int h = 0; h < 4; h++) {
+    const int f = d0 + 16 * part + 4 * h;
+    const uint4 v = (kvalid(id) && f < nfl) ? v4[h] : make_uint4(0, 0, 0, 0);
     double2 *dst = reinterpret_cast<double2 *>(&st[k][16 * part + 4 * h]);
     dst[0] = make_double2((double)__uint_as_float(v.x), (double)__uint_as_float(v.y));
     dst[1] = make_double2((double)__uint_as_float(v.z), (double)__uint_as_float(v.w));
@@ -1314,27 +1322,37 @@ __device__ __forceinline__ void vec_stage(const PoolView &P, const uint32_t *ids
 
 // acc[r][k] += the terms of floats [d0, d0 + kVecSlice) between this lane's
 // row own[r] and staged row k, for every register row r with work (act[r],
-// uniform).
+// uniform) and every k in kmask (uniform).
 template <int KIND, int NCL, int NS>
 __device__ __forceinline__ void vec_accumulate(const double (*st)[kVecSlice], const float *const (&own)[NCL],
                                                const bool (&act)[NCL], int d0, int nfl,
-                                               double (&acc)[NCL][NS]) {
+                                               double (&acc)[NCL][NS], uint32_t kmask = ~0u) {
   for (int pc = 0; pc < kVecSlice && d0 + pc < nfl; pc += 16) {
 #pragma unroll
     for (int r = 0; r < NCL; r++) {
       if (!act[r]) continue;
       float xv[16];
+      // rows hold nfl floats, a multiple of 4; all four loads are issued
+      // before any is used (addresses clamped into the row, the values past
+      // it replaced by zeros afterwards)
+      uint4 v4[4];
 #pragma unroll
       for (int h = 0; h < 4; h++) {
-        const int f = d0 + pc + 4 * h;  // rows hold nfl floats, a multiple of 4
-        const uint4 v = f < nfl ? *reinterpret_cast<const uint4 *>(own[r] + f) : make_uint4(0, 0, 0, 0);
+        const int f = d0 + pc + 4 * h;
+        v4[h] = *reinterpret_cast<const uint4 *>(own[r] + (f < nfl ? f : 0));
+      }
+#pragma unroll
+      for (int h = 0; h < 4; h++) {
+        const int f = d0 + pc + 4 * h;
+        const uint4 v = f < nfl ? v4[h] : make_uint4(0, 0, 0, 0);
         xv[4 * h + 0] = __uint_as_float(v.x);
         xv[4 * h + 1] = __uint_as_float(v.y);
         xv[4 * h + 2] = __uint_as_float(v.z);
         xv[4 * h + 3] = __uint_as_float(v.w);
       }
 #pragma unroll
-      for (int k = 0; k < NS; k++)
+      for (int k = 0; k < NS; k++) {
+        if (!((kmask >> k) & 1u)) continue;  // staged row k is not needed
 #pragma unroll
         for (int t = 0; t < 16; t++) {
           if (KIND == kF32IP) {
@@ -1344,6 +1362,7 @@ __device__ __forceinline__ void vec_accumulate(const double (*st)[kVecSlice], co
             acc[r][k] = __builtin_fma(df, df, acc[r][k]);
           }
         }
+      }
     }
   }
 }
@@ -1356,7 +1375,7 @@ __device__ __forceinline__ void vec_accumulate(const double (*st)[kVecSlice], co
 // fp64 work follows the live positions, not the register rows); the block's
 // own selections come from the parallel fixpoint, and later positions that a
 // selected pivot kills (coef * Dist <= D, in fp64 on the rounded distance)
-// are dropped.  The selections go to oid/od (LDS) in order; returns their
+// are dropped.  Pivots already dead take no distance work.  The selections go to oid/od (LDS) in order; returns their
 // number.
 template <int KIND, int NCL, int NPB>
 __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, double coef, const uint32_t *spos,
@@ -1409,7 +1428,7 @@ __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       __syncthreads();
       vec_stage(P, spos + p0, min(NPB, m - p0), d0, nfl, st);
       __syncthreads();
-      vec_accumulate<KIND, NCL, NPB>(st, own, act, d0, nfl, acc);
+      vec_accumulate<KIND, NCL, NPB>(st, own, act, d0, nfl, acc, vb);
     }
     // kill masks of the packed positions, scattered back by position
 #pragma unroll
@@ -1420,12 +1439,12 @@ __device__ int prune_vec(const PoolView &P, uint32_t p, int m, uint32_t R, doubl
       uint32_t km = 0;
 #pragma unroll
       for (int k = 0; k < NPB; k++) {
-        const bool kill = e > p0 + k && coef * (double)finalize<KIND>(acc[r][k]) <= De;
+        const bool kill = ((vb >> k) & 1u) && e > p0 + k && coef * (double)finalize<KIND>(acc[r][k]) <= De;
         km |= kill ? (1u << k) : 0u;
       }
       kmL[e] = km;
     }
-    evals += (uint32_t)(NPB * nl);
+    evals += (uint32_t)(__popc(vb) * nl);
     __syncthreads();
     // km[r]: pivots of the block that kill this lane's position
     uint32_t km[NCL];
