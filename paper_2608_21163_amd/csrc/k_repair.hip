@@ -521,10 +521,18 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
           const int e = g0 + cand;
           const uint32_t cv = e < kr ? cidL[e] : kInvalid;
           const float *crow = reinterpret_cast<const float *>(P.vecs + (size_t)(kvalid(cv) ? cv : p) * P.stride);
+          // all four loads issued before any is used (addresses clamped into
+          // the row, the values past it replaced by zeros afterwards)
+          uint4 v4[4];
 #pragma unroll
           for (int h = 0; h < 4; h++) {
             const int f = d0 + 16 * part + 4 * h;
-            const uint4 v = (kvalid(cv) && f < nfl) ? *reinterpret_cast<const uint4 *>(crow + f) : make_uint4(0, 0, 0, 0);
+            v4[h] = *reinterpret_cast<const uint4 *>(crow + (f < nfl ? f : 0));
+          }
+#pragma unroll
+          for (int h = 0; h < 4; h++) {
+            const int f = d0 + 16 * part + 4 * h;
+            const uint4 v = (kvalid(cv) && f < nfl) ? v4[h] : make_uint4(0, 0, 0, 0);
             double2 *dst = reinterpret_cast<double2 *>(&cs[cand][16 * part + 4 * h]);
             dst[0] = make_double2((double)__uint_as_float(v.x), (double)__uint_as_float(v.y));
             dst[1] = make_double2((double)__uint_as_float(v.z), (double)__uint_as_float(v.w));
@@ -533,10 +541,16 @@ __global__ __launch_bounds__(64) void k_repair_vec(RepairArgs a) {
         __syncthreads();
         for (int pc = 0; pc < SL && d0 + pc < nfl; pc += 16) {
           float xv[16];
+          uint4 v4[4];
 #pragma unroll
           for (int h = 0; h < 4; h++) {
             const int f = d0 + pc + 4 * h;  // rows hold nfl floats, a multiple of 4
-            const uint4 v = f < nfl ? *reinterpret_cast<const uint4 *>(xrow + f) : make_uint4(0, 0, 0, 0);
+            v4[h] = *reinterpret_cast<const uint4 *>(xrow + (f < nfl ? f : 0));
+          }
+#pragma unroll
+          for (int h = 0; h < 4; h++) {
+            const int f = d0 + pc + 4 * h;
+            const uint4 v = f < nfl ? v4[h] : make_uint4(0, 0, 0, 0);
             xv[4 * h + 0] = __uint_as_float(v.x);
             xv[4 * h + 1] = __uint_as_float(v.y);
             xv[4 * h + 2] = __uint_as_float(v.z);
