@@ -946,6 +946,12 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
   const float rdv = cdl && ln < (int)R ? P.adjd[(size_t)u * R + ln] : 0.0f;
   nrec = g1 - g0;
+  // the first 64 records, loaded beside the list's batch flags (lanes past
+  // the records read a valid one and drop it)
+  const uint32_t j0 = g0 + (uint32_t)ln;
+  const uint32_t jc = j0 < g1 ? j0 : (g1 > g0 ? g0 : 0u);
+  const uint32_t s0 = a.gsrc[jc];
+  const float d0 = a.gd[jc];
   const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
   const uint64_t kmask = ballot(keep);
   const int kr = popc(kmask);
@@ -960,8 +966,8 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   uint32_t si[1] = {kInvalid};
   for (uint32_t base = g0; base < g1; base += 64) {
     const uint32_t j = base + ln;
-    uint32_t sv = j < g1 ? a.gsrc[j] : kInvalid;
-    float dv = j < g1 ? a.gd[j] : finf();
+    uint32_t sv = j < g1 ? (base == g0 ? s0 : a.gsrc[j]) : kInvalid;
+    float dv = j < g1 ? (base == g0 ? d0 : a.gd[j]) : finf();
     if (!kvalid(sv)) { sv = kInvalid; dv = finf(); }
     wave_merge_new_fast<1>(sd, si, dv, sv, (int)a.P);
   }
@@ -1016,8 +1022,11 @@ __global__ __launch_bounds__(64, 4) void k_rebuild_mr(RebuildArgs a) {
   const size_t goff = (size_t)g * 16;
   unsigned long long evals = 0;
   uint32_t prunes = 0, nodes = 0, recs = 0, cand = 0;
+  // the next node of this wave is read while the current one is rebuilt
+  uint32_t u_next = blockIdx.x < nd_total ? a.list[blockIdx.x] : 0u;
   for (uint32_t it = blockIdx.x; it < nd_total; it += gridDim.x) {
-    const uint32_t u = a.list[it];
+    const uint32_t u = u_next;
+    u_next = a.list[it + gridDim.x < nd_total ? it + gridDim.x : it];
     nodes++;
     uint32_t nrec;
     const int m = collect_candidates(a, u, rowL, cl, nrec, P.adjd ? cdL : nullptr);
