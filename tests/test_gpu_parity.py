@@ -49,6 +49,11 @@ CASES = {
                    dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     "u8_d128_r1": ("sift1m_u8", dict(capacity=12_000, R=1),
                    dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
+    # uint8 points within about one unit of their component's centre: the
+    # distances among a node's candidates repeat often, so ties broken by id
+    # decide searches, prunes, repairs and the rebuild's key order
+    "u8_d128_ties": ("sift1m_u8", dict(capacity=12_000),
+                     dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     # inner-product data through the L2 augmentation (Section 5.4)
     "mips_f32_d64": ("ip768_mips", dict(capacity=9_000, dim=64),
                      dict(base_n=6_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.001),
@@ -71,9 +76,14 @@ def _ctx(case, w, pre_state, batch_ids):
 _BASE = {}
 
 
+# sampler arguments of the cases that change them (mixture components, sigma)
+SAMPLER = {"u8_d128_ties": (16, 0.7)}
+
+
 def _workload(case):
     name, idx, st, _ = CASES[case]
-    return make_workload(name, seed=7, index=idx or None, stream=st or None).keep_vectors()
+    return make_workload(name, seed=7, index=idx or None, stream=st or None,
+                         sampler_args=SAMPLER.get(case)).keep_vectors()
 
 
 def base_state(case):

@@ -329,13 +329,15 @@ class Workload:
 
 
 def make_workload(name: str, seed: int = 0, index: Optional[dict] = None,
-                  stream: Optional[dict] = None) -> Workload:
+                  stream: Optional[dict] = None, sampler_args: Optional[Tuple] = None) -> Workload:
     """Build a workload by name, optionally overriding index or stream fields
-    (used to make small variants of the large workloads for tests)."""
+    or the sampler's arguments (used to make small variants of the large
+    workloads for tests)."""
     w = CONFIGS[name]
     idx = dataclasses.replace(w.index, **(index or {}))
     st = dataclasses.replace(w.stream, **(stream or {}))
-    return Workload(WorkloadDef(w.name, w.description, idx, st, w.sampler, w.sampler_args), seed)
+    sa = w.sampler_args if sampler_args is None else tuple(sampler_args)
+    return Workload(WorkloadDef(w.name, w.description, idx, st, w.sampler, sa), seed)
 
 
 # ---------------------------------------------------------------------------
