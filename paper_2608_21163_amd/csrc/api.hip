@@ -583,11 +583,22 @@ grand_status cagra_delete(grand_index *h, uint32_t n) {
   if (s != GRAND_OK) return s;
   Phase ph(h, GRAND_PH_CAGRA_PICKONE);
   h->epoch++;
-  HCHK(h, launch_cagra_affected(h->b_ids, n, h->in_batch, h->rev_off, h->rev_src, by_batch, h->mark, h->epoch,
-                                h->dirty, h->ds, h->stream));
   CagraArgs c{};
+  if (by_batch) {
+    // the batch's reverse rows are one contiguous array: every entry is an
+    // in-neighbour of the batch, the first one to mark a node takes it
+    c.list = h->rev_src;
+    c.list_n = h->rev_off + n;
+    c.dedupe = 1;
+    c.mark = h->mark;
+    c.epoch = h->epoch;
+  } else {
+    HCHK(h, launch_cagra_affected(h->b_ids, n, h->in_batch, h->rev_off, h->rev_src, by_batch, h->mark, h->epoch,
+                                  h->dirty, h->ds, h->stream));
+    c.list = h->dirty;
+    c.list_n = &h->ds->n_dirty;
+  }
   c.pool = h->pool;
-  c.list = h->dirty;
   c.bidx = h->bidx;
   c.in_batch = h->in_batch;
   c.rev_off = h->rev_off;

@@ -226,6 +226,13 @@ struct CagraArgs {
   const uint32_t *rec_t, *rec_s;   // racing mode: raw records
   uint32_t nrec;
   DevScalars *ds;
+  // pickone: number of list entries (device); with `dedupe` the list may
+  // repeat a node and hold nodes of the batch: an entry is taken when its
+  // node is outside the batch and its mark is first set to `epoch`
+  const uint32_t *list_n;
+  int dedupe;
+  uint32_t *mark;
+  uint32_t epoch;
 };
 
 // ---- launchers (defined in the kernel translation units) ----------------

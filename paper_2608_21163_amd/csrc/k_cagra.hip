@@ -247,14 +247,20 @@ hipError_t launch_cagra_affected(const uint32_t *ids, uint32_t n, const uint8_t 
 
 __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   __shared__ uint32_t lc[64];
+  __shared__ uint8_t lcb[64];  // batch flags of lc
   __shared__ uint4 uL[16];  // u's current row, for the membership test
   const int ln = lane();
   const PoolView &P = a.pool;
   const bool inrow = ln < (int)P.R;
-  const uint32_t nt = a.ds->n_dirty;
+  const uint32_t nt = *a.list_n;
   uint32_t nodes = 0;
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
     const uint32_t u = a.list[it];
+    if (a.dedupe) {
+      bool take = false;
+      if (ln == 0) take = u != kInvalid && !a.in_batch[u] && atomicExch(&a.mark[u], a.epoch) != a.epoch;
+      if (!__shfl((int)take, 0, 64)) continue;
+    }
     uint32_t rv = inrow ? P.adj[(size_t)u * P.R + ln] : kInvalid;
     reinterpret_cast<uint32_t *>(uL)[ln] = rv;
     // slots holding a deleted out-neighbour, found with one parallel lookup;
@@ -266,13 +272,19 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
       dels &= dels - 1;
       const uint32_t p = rdlane(rv, (int)s);
       // valid entries of N_out(p) in slot order (p's row is not edited here)
+      // with their batch flags, and p's reverse row: the loads that do not
+      // depend on each other are issued together
       const uint32_t lv = inrow ? P.adj[(size_t)p * P.R + ln] : kInvalid;
-      const uint64_t vm = ballot(lv != kInvalid);
-      const int nl = popc(vm);
-      if (lv != kInvalid) lc[mbcnt(vm)] = lv;
-      // rank of u among p's in-neighbours (rows hold distinct sources)
       const uint32_t row = a.rev_by_batch ? a.bidx[p] : p;
       const uint32_t b0 = a.rev_off[row], b1 = a.rev_off[row + 1];
+      const bool lvb = a.in_batch[lv != kInvalid ? lv : 0u] != 0;
+      const uint64_t vm = ballot(lv != kInvalid);
+      const int nl = popc(vm);
+      if (lv != kInvalid) {
+        lc[mbcnt(vm)] = lv;
+        lcb[mbcnt(vm)] = lvb ? 1 : 0;
+      }
+      // rank of u among p's in-neighbours (rows hold distinct sources)
       uint32_t below = 0;
       for (uint32_t j = b0 + ln; j < b1; j += 64) below += a.rev_src[j] < u ? 1u : 0u;
 #pragma unroll
@@ -284,8 +296,9 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
         uint32_t r = kInvalid;
         bool ok = false;
         if (ln < nl) {
-          r = lc[(start + (uint32_t)ln) % (uint32_t)nl];
-          ok = !a.in_batch[r] && r != u;
+          const uint32_t e = (start + (uint32_t)ln) % (uint32_t)nl;
+          r = lc[e];
+          ok = !lcb[e] && r != u;
         }
         // r must not already be in u's row (16-byte LDS reads, all lanes
         // at the same address)
