@@ -254,14 +254,19 @@ __global__ __launch_bounds__(64) void k_cagra_pickone(CagraArgs a) {
   const bool inrow = ln < (int)P.R;
   const uint32_t nt = *a.list_n;
   uint32_t nodes = 0;
+  // the next entry of this wave is read during the current one; u's row is
+  // loaded beside the mark that decides whether u is taken
+  uint32_t u_next = blockIdx.x < nt ? a.list[blockIdx.x] : 0u;
   for (uint32_t it = blockIdx.x; it < nt; it += gridDim.x) {
-    const uint32_t u = a.list[it];
+    const uint32_t u = u_next;
+    u_next = a.list[it + gridDim.x < nt ? it + gridDim.x : it];
+    uint32_t rv = P.adj[(size_t)(u != kInvalid ? u : 0u) * P.R + (inrow ? ln : 0)];
+    if (!inrow) rv = kInvalid;
     if (a.dedupe) {
       bool take = false;
       if (ln == 0) take = u != kInvalid && !a.in_batch[u] && atomicExch(&a.mark[u], a.epoch) != a.epoch;
       if (!__shfl((int)take, 0, 64)) continue;
     }
-    uint32_t rv = inrow ? P.adj[(size_t)u * P.R + ln] : kInvalid;
     reinterpret_cast<uint32_t *>(uL)[ln] = rv;
     // slots holding a deleted out-neighbour, found with one parallel lookup;
     // they are then handled in slot order (replacements only ever put
