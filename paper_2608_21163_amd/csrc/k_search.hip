@@ -93,10 +93,12 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
   typedef decltype(H::word(0u)) Word;
   constexpr int kSlots = H::kSlots;
   __shared__ Word hsh[kSlots];
-  __shared__ uint32_t nid[64];
-  __shared__ float nkey[64];
+  // the merge's scratch; its first 64 entries also hold a hop's new ids and
+  // their distances (read into registers before the merge writes)
   __shared__ uint32_t mid[64 * NR];
   __shared__ float mkey[64 * NR];
+  uint32_t *const nid = mid;
+  float *const nkey = mkey;
   const int ln = lane();
   const uint32_t qi = blockIdx.x;
   if (qi >= a.nq) return;
