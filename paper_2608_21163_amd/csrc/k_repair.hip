@@ -188,8 +188,8 @@ __global__ __launch_bounds__(64) void k_repair(RepairArgs a) {
 // one deleted node (persistent waves over the chunk list).  Per chunk the
 // C_i tiles are the MFMA A operand and 16 neighbours at a time the B
 // operand: lane (g, col) then holds 16 candidate distances of neighbour col,
-// keeps its K smallest keys, and the four lanes of a neighbour merge their
-// lists (two exchanges).
+// keeps its K + 1 smallest keys, and the four lanes of a neighbour merge
+// their lists (two exchanges).
 //
 // C_i arrives in ascending id order (points first), so a candidate's slot
 // is its rank among the ids and 32-bit keys 64 * Dist + slot order like
@@ -221,7 +221,7 @@ __device__ __forceinline__ void kl_merge_max(int32_t (&l)[L], const int32_t (&o)
   for (int j = 0; j < L; j++) kl_insert_max<L>(l, o[j]);
 }
 constexpr int32_t kSlotNone = 0x60000000;  // 64 |c'|^2 + slot of an empty candidate slot
-constexpr int32_t kNone = INT32_MIN;       // below every value: an excluded candidate
+constexpr int32_t kNone = INT32_MIN;       // below every value: a list entry not yet filled
 constexpr uint32_t kKeyValid = 1u << 30;   // keys of points are below
 
 template <int NK, int K, int NPL>
