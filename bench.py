@@ -509,8 +509,8 @@ def reverse_microbench(g, w, spec, reps=5):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs the update path on one GPU only; "
-              "a multi-GPU run (sharding by id, one index per GPU) is not part of it", file=sys.stderr)
+        print("bench.py: the update path runs on one GPU; a multi-GPU run "
+              "(sharding by id, one index per GPU) is not implemented", file=sys.stderr)
         sys.exit(2)
     if args.copy_probe:
         copy_probe()
