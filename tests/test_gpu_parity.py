@@ -51,8 +51,10 @@ CASES = {
                    dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     # uint8 points within about one unit of their component's centre: the
     # distances among a node's candidates repeat often, so ties broken by id
-    # decide searches, prunes, repairs and the rebuild's key order
-    "u8_d128_ties": ("sift1m_u8", dict(capacity=12_000),
+    # decide searches, prunes, repairs and the rebuild's key order; with
+    # alpha = 1.25 (exact in binary) alpha * Dist also equals D_p often, the
+    # boundary of the prune test
+    "u8_d128_ties": ("sift1m_u8", dict(capacity=12_000, alpha=1.25),
                      dict(base_n=8_000, build_batch=2_000, n_insert=1_000, n_delete=1_000, n_query=200), 0.0),
     # inner-product data through the L2 augmentation (Section 5.4)
     "mips_f32_d64": ("ip768_mips", dict(capacity=9_000, dim=64),
