@@ -75,6 +75,15 @@ MUTATIONS = {
         "                if (in_batch[r] || r == u) continue;", "                if (r == u) continue;"),
     # Section 5.4: the augmented coordinate is sqrt(M^2 - |x|^2)
     "mips_plus": ("    double t = M2 - s;", "    double t = M2 + s;"),
+    # CAGRA construction: a route u -> z -> y counts when z is ranked before
+    # y in L(u) and y's position in L(z) is below y's rank in L(u)
+    "rank_route_condition": (
+        "if (ry != O_INVALID && rz < ry && rzy < ry) routes[ry]++;",
+        "if (ry != O_INVALID && rz < ry) routes[ry]++;"),
+    # the merged list starts with the first R/2 pruned entries
+    "merge_quarter": ("    const uint32_t half = R / 2;", "    const uint32_t half = R / 4;"),
+    "merge_reverse_repeats": (
+        "            if (!in_list(o, no, rv[k].s)) o[no++] = rv[k].s;", "            o[no++] = rv[k].s;"),
 }
 
 
