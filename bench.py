@@ -24,7 +24,8 @@ before timing.  One JSON line is printed:
                 evaluation the timed kernel made is given beside it.  The
                 other phases' figures are listed in roofline_other_phases;
   cpu_baseline= the CPU oracle on the host cores allotted to the job, on the
-                state the timed rounds start from, for the first timed round.
+                state the timed rounds start from, for the first three timed
+                rounds.
 Other workloads (--workload) are the fp32 sliding window, the CAGRA
 inner-product set, the 960-d set and the tiny set; their lines carry their
 own metric and data labels.
@@ -260,9 +261,13 @@ def oracle_threads():
     return min(int(share), aff) if share and share.isdigit() and int(share) > 0 else aff
 
 
-def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
+# timed rounds the CPU baseline replays (about 10-30 s of oracle work at 1M points)
+CPU_ROUNDS = 3
+
+
+def cpu_baseline(cfg, spec, snap, host_round, n_rounds, threads, max_seconds=60.0):
     """The oracle (plain C, OpenMP over batch items) on the state the timed
-    rounds start from (imported), timed on the first timed round's own
+    rounds start from (imported), timed on the first timed rounds' own
     batches: the same workload at the same scale, on `threads` host cores."""
     from oracle.oracle import Oracle
     o = Oracle(cfg, threads=threads)
@@ -271,7 +276,7 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
     log(f"cpu baseline: state imported in {time.perf_counter() - t0:.1f} s; oracle on {threads} threads ...")
     t_upd = t_q = 0.0
     n_upd = n_q = 0
-    done = []
+    done = {"inserts": 0, "deletes": 0, "searches": 0}
     for kind, ids, vecs in host_round:
         t0 = time.perf_counter()
         if kind == "insert":
@@ -286,13 +291,14 @@ def cpu_baseline(cfg, spec, snap, host_round, threads, max_seconds=60.0):
             o.search(vecs, spec.k, spec.beam)
             t_q += time.perf_counter() - t0
             n_q += len(vecs)
-        plural = {"insert": "inserts", "delete": "deletes", "search": "searches"}.get(kind, kind)
-        done.append(f"{len(ids) if ids is not None else len(vecs):,} {plural}")
+        plural = {"insert": "inserts", "delete": "deletes", "search": "searches"}[kind]
+        done[plural] += len(ids) if ids is not None else len(vecs)
         log(f"cpu baseline: {kind} done, {time.perf_counter() - t0:.1f} s")
     out = {"value": round(n_upd / t_upd, 1) if t_upd > 0 else None, "unit": "updates/s", "cores": threads,
            "kind": "oracle", "search_qps": round(n_q / t_q, 1) if t_q > 0 else None,
            "sample": (f"oracle on the {int(snap['active'].sum()):,}-point index the timed rounds start from "
-                      f"(imported from the GPU), timed on the first timed round: " + ", ".join(done)),
+                      f"(imported from the GPU), timed on the first {n_rounds} timed round"
+                      f"{'s' if n_rounds != 1 else ''}: " + ", ".join(f"{v:,} {k}" for k, v in done.items() if v)),
            "cpu": host_cpu()}
     return out
 
@@ -615,7 +621,8 @@ def main():
 
     # ---- stage every round's inputs on the device, with exact ground truth;
     # the pool as the timed rounds find it is kept for the counting rerun and
-    # the CPU baseline, and the first timed round's batches on the host
+    # the CPU baseline, and the first CPU_ROUNDS timed rounds' batches on the
+    # host
     rounds = []
     snap_vecs = None
     host_round = []
@@ -624,7 +631,7 @@ def main():
             snap_vecs = mirror.pool.clone()
         ops = []
         for op in w.round_ops(r):
-            if r == W:
+            if W <= r < W + CPU_ROUNDS:
                 host_round.append((op.kind, op.ids, op.vecs))
             if op.kind == "insert":
                 ids, vecs = dev_ids(op.ids), dev_vecs(op.vecs)
@@ -793,9 +800,10 @@ def main():
     if not args.no_cpu_baseline:
         snap_host = dict(snap)
         snap_host["vecs"] = snap["vecs"].cpu().numpy()
-        cpu = cpu_baseline(cfg, spec, snap_host, host_round, oracle_threads())
+        n_cpu = min(CPU_ROUNDS, K)
+        cpu = cpu_baseline(cfg, spec, snap_host, host_round, n_cpu, oracle_threads())
         if args.workload == "tiny":
-            cpu["one_core"] = cpu_baseline(cfg, spec, snap_host, host_round, 1)
+            cpu["one_core"] = cpu_baseline(cfg, spec, snap_host, host_round, n_cpu, 1)
 
     value = upd_n / (upd_ms / 1e3)
     rmin = round(min(recalls), 4) if recalls else None
