@@ -488,20 +488,26 @@ __global__ __launch_bounds__(kGrpThreads) void k_grp_part(const uint32_t *rec_t,
   for (uint32_t b = threadIdx.x; b < nb1; b += kGrpThreads) cur[b] = mato[(size_t)b * ntiles + blockIdx.x];
   __syncthreads();
   const size_t base = (size_t)blockIdx.x * kGrpTile + threadIdx.x;
-  uint32_t t[kGrpPer];
+  // every record of the thread is loaded before the first is placed
+  // (indices past the records read record 0 and are dropped)
+  uint32_t t[kGrpPer], sv[kGrpPer];
+  float dv[kGrpPer];
 #pragma unroll
   for (int k = 0; k < kGrpPer; k++) {
     const size_t i = base + (size_t)k * kGrpThreads;
-    t[k] = i < nrec ? rec_t[i] : kInvalid;
+    const size_t ic = i < nrec ? i : 0;
+    t[k] = rec_t[ic];
+    sv[k] = rec_s[ic];
+    dv[k] = rec_d[ic];
+    if (i >= nrec) t[k] = kInvalid;
   }
 #pragma unroll
   for (int k = 0; k < kGrpPer; k++) {
     if (t[k] >= cap) continue;
-    const size_t i = base + (size_t)k * kGrpThreads;
     const uint32_t pos = atomicAdd(&cur[t[k] >> kGrpShift], 1u);
     pt[pos] = t[k];
-    ps[pos] = rec_s[i];
-    pd[pos] = rec_d[i];
+    ps[pos] = sv[k];
+    pd[pos] = dv[k];
   }
 }
 
