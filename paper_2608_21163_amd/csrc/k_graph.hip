@@ -383,12 +383,16 @@ __global__ __launch_bounds__(kScanThreads) void k_cf_tiles(const uint32_t *flags
   __shared__ uint32_t wsum[kScanThreads / 64];
   const size_t n = *np;
   const size_t base = (size_t)blockIdx.x * kScanTile + threadIdx.x;
-  uint32_t f = 0;
+  // loads issued together: indices past n read flag 0 and are dropped
+  uint32_t fl[kScanPer];
 #pragma unroll
   for (int k = 0; k < kScanPer; k++) {
     const size_t i = base + (size_t)k * kScanThreads;
-    f += (i < n && flags[i] != 0u) ? 1u : 0u;
+    fl[k] = flags[i < n ? i : 0];
   }
+  uint32_t f = 0;
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) f += (base + (size_t)k * kScanThreads < n && fl[k] != 0u) ? 1u : 0u;
   uint32_t total;
   block_excl_scan(f, wsum, total);
   if (threadIdx.x == 0) tsum[blockIdx.x] = total;
@@ -399,18 +403,26 @@ __global__ __launch_bounds__(kScanThreads) void k_cf_apply(const uint32_t *flags
   __shared__ uint32_t wsum[kScanThreads / 64];
   const size_t n = *np;
   const size_t base = (size_t)blockIdx.x * kScanTile + (size_t)threadIdx.x * kScanPer;
-  uint32_t f[kScanPer];
+  // flags and items loaded together: indices past n read entry 0 and are
+  // dropped
+  uint32_t f[kScanPer], it[kScanPer];
   uint32_t s = 0;
 #pragma unroll
   for (int k = 0; k < kScanPer; k++) {
-    f[k] = (base + k < n && flags[base + k] != 0u) ? 1u : 0u;
+    const size_t i = base + k < n ? base + k : 0;
+    f[k] = flags[i];
+    it[k] = items[i];
+  }
+#pragma unroll
+  for (int k = 0; k < kScanPer; k++) {
+    f[k] = (base + k < n && f[k] != 0u) ? 1u : 0u;
     s += f[k];
   }
   uint32_t total;
   uint32_t run = tsum[blockIdx.x] + block_excl_scan(s, wsum, total);
 #pragma unroll
   for (int k = 0; k < kScanPer; k++)
-    if (f[k]) out[run++] = items[base + k];
+    if (f[k]) out[run++] = it[k];
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *out_n = tsum[nt];
 }
 hipError_t launch_compact_flags(const uint32_t *flags, const uint32_t *items, const uint32_t *n, uint32_t cap,
@@ -788,10 +800,15 @@ __global__ __launch_bounds__(kRevrThreads) void k_revr_find(PoolView P, const ui
       const uint4 *adj4 = reinterpret_cast<const uint4 *>(P.adj);
       const uint32_t q0 = e0 / 4, q1 = e1 / 4, step = blockDim.x;
       for (uint32_t q = q0 + threadIdx.x; q < q1; q += 4 * step) {
+        // the four loads issued together (indices past the range read group
+        // q0 and are dropped)
         uint4 w[4];
 #pragma unroll
-        for (int k = 0; k < 4; k++)
-          w[k] = q + k * step < q1 ? adj4[q + k * step] : make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+        for (int k = 0; k < 4; k++) {
+          const uint32_t qk = q + k * step;
+          w[k] = adj4[qk < q1 ? qk : q0];
+          if (qk >= q1) w[k] = make_uint4(kInvalid, kInvalid, kInvalid, kInvalid);
+        }
 #pragma unroll
         for (int k = 0; k < 4; k++) {
           const uint32_t e = 4 * (q + k * step);
@@ -806,7 +823,11 @@ __global__ __launch_bounds__(kRevrThreads) void k_revr_find(PoolView P, const ui
       for (uint32_t i = e0 + threadIdx.x; i < e1; i += 4 * step) {
         uint32_t v[4];
 #pragma unroll
-        for (int k = 0; k < 4; k++) v[k] = i + k * step < e1 ? P.adj[i + k * step] : kInvalid;
+        for (int k = 0; k < 4; k++) {
+          const uint32_t ik = i + k * step;
+          v[k] = P.adj[ik < e1 ? ik : e0];
+          if (ik >= e1) v[k] = kInvalid;
+        }
 #pragma unroll
         for (int k = 0; k < 4; k++) test(i + k * step, v[k]);
       }
