@@ -946,13 +946,27 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   const uint32_t rv = ln < (int)R ? P.adj[(size_t)u * R + ln] : kInvalid;
   const float rdv = cdl && ln < (int)R ? P.adjd[(size_t)u * R + ln] : 0.0f;
   nrec = g1 - g0;
-  // the first 64 records, loaded beside the list's batch flags (lanes past
-  // the records read a valid one and drop it)
+  // the first 64 records, loaded beside the row (lanes past the records
+  // read a valid one and drop it); then the batch flags of the row's ids and
+  // of those records' sources together (index 0 stands in for an id that
+  // is not checked)
   const uint32_t j0 = g0 + (uint32_t)ln;
   const uint32_t jc = j0 < g1 ? j0 : (g1 > g0 ? g0 : 0u);
   const uint32_t s0 = a.gsrc[jc];
   const float d0 = a.gd[jc];
-  const bool keep = rv != kInvalid && rv != u && !(a.in_batch && a.in_batch[rv]);
+  const bool rok = rv != kInvalid && rv != u;
+  const bool sok = j0 < g1 && kvalid(s0);
+  bool rin = false, sin = false;
+  if (a.in_batch) {
+    const uint8_t fr = a.in_batch[rok ? rv : 0u];
+    const uint8_t fs = a.in_batch[sok ? s0 : 0u];
+    rin = rok && fr;
+    sin = sok && fs;
+  }
+  // the merged sources below are all among these records when there are
+  // at most 64; then none of them needs its flag loaded again
+  const bool recheck = a.in_batch && (g1 - g0 > 64u || ballot(sin) != 0);
+  const bool keep = rok && !rin;
   const uint64_t kmask = ballot(keep);
   const int kr = popc(kmask);
   reinterpret_cast<uint32_t *>(rowL)[ln] = keep ? rv : kInvalid;
@@ -974,7 +988,7 @@ __device__ int collect_candidates(const RebuildArgs &a, uint32_t u, uint4 *rowL,
   bool isnew;
   {
     const uint32_t sv = si[0];
-    bool ok = kvalid(sv) && sv != u && !(a.in_batch && a.in_batch[sv]);
+    bool ok = kvalid(sv) && sv != u && !(recheck && a.in_batch[sv]);
 #pragma unroll 4
     for (int t = 0; t < 16; t++) {
       const uint4 r4 = rowL[t];
