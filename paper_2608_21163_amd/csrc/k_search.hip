@@ -126,6 +126,12 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
   }
   __syncthreads();
   uint32_t nv = 0, evals = 1;
+  // V in expansion order, written out 64 entries at a time: lane j holds the
+  // entry of the hop nv with nv % 64 == j until its group of 64 is complete
+  // (one store per 64 hops, so the waits for the lists of the others do not
+  // also wait for stores)
+  uint32_t vq = 0;
+  float vdq = 0.0f;
 
   while (nv < a.max_iters) {
     // u = argmin over C \ V
@@ -146,9 +152,16 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
         du = rdlane(cd[r], el);
         if (ln == el) ci[r] |= kVisit;
       }
-    if (a.v_ids && ln == 0) {
-      a.v_ids[(size_t)qi * a.v_stride + nv] = u;
-      a.v_d[(size_t)qi * a.v_stride + nv] = du;
+    if (a.v_ids) {
+      if (ln == (int)(nv & 63u)) {
+        vq = u;
+        vdq = du;
+      }
+      if ((nv & 63u) == 63u) {
+        const size_t o = (size_t)qi * a.v_stride + (nv - 63u) + (uint32_t)ln;
+        a.v_ids[o] = vq;
+        a.v_d[o] = vdq;
+      }
     }
     nv++;
     // C <- C u N_out(u), skipping ids already evaluated
@@ -182,6 +195,11 @@ __device__ __forceinline__ void search_one(SearchArgs a) {
     __syncthreads();
   }
 
+  if (a.v_ids && ln < (int)(nv & 63u)) {  // the last, incomplete group
+    const size_t o = (size_t)qi * a.v_stride + (nv & ~63u) + (uint32_t)ln;
+    a.v_ids[o] = vq;
+    a.v_d[o] = vdq;
+  }
   if (a.v_n && ln == 0) a.v_n[qi] = nv;
   if (a.c_ids && a.c_by_id) {
     // the same set in ascending id order (delete repair candidates), through
